@@ -1,0 +1,225 @@
+/*
+ * turbo_attn.h — C ABI of the MI355X (gfx950) TurboAttention hot path.
+ *
+ * TurboAttention (Kang et al., MLSys 2025) replaces FP16 FlashAttention by
+ *   - FlashQ: blockwise symmetric int8 quantization of Q, K and V tiles
+ *     (Sec. 3.1, eq. step1bpq) followed, for K and V only, by channel-wise
+ *     asymmetric int4 / int2 compression of the int8 values into a cache
+ *     (Sec. 3.1, eq. step2bpq; Sec. 2.3 progressive quantization), with the
+ *     bit width chosen per KV head (Sec. 3.2);
+ *   - SAS: the exponential of the online softmax is replaced by a lookup
+ *     table for the integer part and a cubic polynomial for the fractional
+ *     part, and scores more than |n_r| = 6 below the running row maximum are
+ *     dropped (Sec. 4; Appendix B, Algorithm 3);
+ *   - integer QK^T and PV contractions inside a FlashAttention-style tiled
+ *     loop (Appendix A, Algorithm 1 prefill, Algorithm 2 decode).
+ *
+ * This header declares the three calls of that path plus their helpers.
+ *
+ * General rules for every entry point
+ *   - All tensor arguments are DEVICE pointers allocated and owned by the
+ *     caller, unless stated "host".  The library never allocates, frees or
+ *     synchronizes; every launch is queued on `stream` and outputs are valid
+ *     once that stream has completed.
+ *   - Return value: TURBO_OK (0) on success, a negative turbo_status
+ *     otherwise.  All argument checks run on the host before any launch; on
+ *     an error nothing is launched.  No C++ exception crosses this boundary.
+ *   - fp16 means IEEE binary16 stored as 16-bit words.
+ *   - Fixed constants: head dimension d = 128; query block B_r, key block
+ *     B_c and the channel-group length of the int4/int2 step are all 64
+ *     tokens (Sec. 5.2 fixes B_r = B_c = n_b = 64); cache pages hold 16
+ *     tokens; the symmetric int8 divisor is 119 (Algorithms 1 and 2); the SAS
+ *     threshold is n_r = -6 (Sec. 5.2).
+ *   - Index types are int32 for shapes and table entries.
+ */
+#ifndef TURBO_ATTN_H
+#define TURBO_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TURBO_ABI_VERSION 1
+
+#define TURBO_HEAD_DIM 128       /* d */
+#define TURBO_BLOCK 64           /* B_r = B_c = step-2 group length (tokens) */
+#define TURBO_PAGE_TOKENS 16     /* tokens per cache page */
+#define TURBO_PAGES_PER_GROUP 4  /* TURBO_BLOCK / TURBO_PAGE_TOKENS */
+#define TURBO_MAX_KV_HEADS 64
+#define TURBO_MAX_GQA 16         /* max query heads per KV head */
+
+typedef enum turbo_status {
+  TURBO_OK = 0,
+  TURBO_ERR_INVALID_ARG = -1,         /* null pointer, bad shape, bad bits */
+  TURBO_ERR_UNSUPPORTED = -2,         /* device is not gfx950 */
+  TURBO_ERR_WORKSPACE_TOO_SMALL = -3, /* decode workspace smaller than needed */
+  TURBO_ERR_HIP = -4                  /* a HIP runtime call or launch failed */
+} turbo_status;
+
+/*
+ * Compressed paged KV cache (Sec. 3.1 eq. step2bpq; Sec. 2.3: the int4/int2
+ * data with integer scale and zero point per group, plus the float scales of
+ * the int8 step).  The cache is shared by all sequences of a batch: pages and
+ * group slots are handed out through the block and group tables.
+ *
+ * pages        device, uint8 [num_pages][page_bytes].  A page holds 16
+ *              consecutive tokens of one sequence for ALL KV heads.  KV head h
+ *              occupies 512*bits_h bytes starting at byte offset
+ *              sum_{h'<h} 512*bits_{h'}: first the K codes (256*bits_h bytes),
+ *              then the V codes (256*bits_h bytes).
+ *                K codes are token-major: token t (0..15) uses 16*bits_h
+ *                bytes; int4: byte j holds channel 2j in bits 0-3 and channel
+ *                2j+1 in bits 4-7; int2: byte j holds channels 4j..4j+3 in
+ *                bits (0-1, 2-3, 4-5, 6-7).
+ *                V codes are channel-major: channel c (0..127) uses 2*bits_h
+ *                bytes for the page's 16 tokens; int4: byte j holds token 2j
+ *                in bits 0-3 and token 2j+1 in bits 4-7; int2: byte j holds
+ *                tokens 4j..4j+3 in bits (0-1, 2-3, 4-5, 6-7).
+ *              Codes are the unsigned step-2 levels, 0 .. 2^bits-1.
+ * group_meta   device, int8 [num_group_slots][num_kv_heads][4][128]: per
+ *              64-token group and channel the integer step-2 parameters:
+ *              [0] K scale s^int (stored as uint8, 1..255), [1] K zero point
+ *              z^int (int8), [2] V scale (uint8), [3] V zero point (int8).
+ *              The int8 value is recovered as code * s^int + z^int.
+ * group_scale  device, fp32 [num_group_slots][num_kv_heads][2]: the step-1
+ *              block scales s_K and s_V of the group (int8 value * s = real).
+ * head_bits    HOST array inside the struct: 4 or 2 for each KV head.
+ */
+typedef struct turbo_kv_cache {
+  uint8_t* pages;
+  int8_t* group_meta;
+  float* group_scale;
+  int64_t num_pages;
+  int64_t num_group_slots;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  uint8_t head_bits[TURBO_MAX_KV_HEADS];
+} turbo_kv_cache;
+
+/* ABI version of the loaded library (TURBO_ABI_VERSION). */
+int turbo_abi_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* turbo_strerror(int status);
+
+/* Bytes of one cache page for the given host array of per-head bit widths
+ * (sum over heads of 512*bits).  Returns 0 if any width is not 2 or 4 or
+ * num_kv_heads is outside 1..TURBO_MAX_KV_HEADS. */
+size_t turbo_page_bytes(const uint8_t* head_bits, int num_kv_heads);
+
+/*
+ * turbo_quantize_kv — FlashQ for K and V (Algorithm 1, the step-1 int8
+ * quantization of K_j, V_j and the step-2 channel-wise int4/int2 compression
+ * with its writes of K^q2, V^q2, s^int, z^int, s_K, s_V; eq. step1bpq and
+ * step2bpq of Sec. 3.1).
+ *
+ * k, v        fp16 [B][Hkv][N][128].
+ * k8          int8 [B][Hkv][Np][128], Np = 64*ceil(N/64), token-major; the
+ *             int8 codes round(x * 119 / max|block|) of each 64-token block.
+ *             Rows N..Np-1 are written as 0.
+ * v8          int8 [B][Hkv][Np/64][128][64]: the same codes for V, stored
+ *             channel-major inside each 64-token block (element (token t,
+ *             channel c) at [t/64][c][t%64]); rows >= N are written as 0.
+ * s_k, s_v    fp32 [B][Hkv][Np/64]: block scales max|block| / 119 (0 for an
+ *             all-zero block).  A partial last block uses its valid rows only.
+ * cache       may be NULL (no cache write).  Otherwise the full 64-token
+ *             groups g = 0 .. floor(N/64)-1 of sequence b are compressed
+ *             into pages block_table[b][4g .. 4g+3] and group slot
+ *             group_table[b][g].  The N mod 64 trailing tokens stay in k8/v8
+ *             only.  cache->num_kv_heads must equal Hkv.
+ * block_table device int32 [B][4*max_groups_per_seq] (ignored if cache NULL).
+ * group_table device int32 [B][max_groups_per_seq]   (ignored if cache NULL).
+ *             Entries must lie in [0, num_pages) / [0, num_group_slots) and
+ *             the pages and slots of different (b, g) must be distinct; the
+ *             kernel skips the cache write of a group whose entries are out
+ *             of range (never touching memory for it).
+ * B, Hkv, N   B >= 0, 1 <= Hkv <= 64, N >= 0; B == 0 or N == 0 is a no-op.
+ *             max_groups_per_seq >= floor(N/64) when cache != NULL.
+ * d           must be 128.
+ */
+int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d,
+                      int8_t* k8, int8_t* v8, float* s_k, float* s_v,
+                      const turbo_kv_cache* cache, const int32_t* block_table,
+                      const int32_t* group_table, int max_groups_per_seq,
+                      hipStream_t stream);
+
+/*
+ * turbo_attn_prefill — Algorithm 1 (TurboAttention prefill): per 64-row query
+ * block, int8 quantization of Q_i; for each key block j, int8 QK^T scaled by
+ * s_Q * s_K * sm_scale, online row maximum, SAS in place of exp, running sum
+ * of the unquantized SAS values, int8 quantization of the 64x64 SAS tile with
+ * scale max/119, int8 PV scaled by s_P * s_V, and the rescale of the
+ * accumulator by SAS(m_old - m_new); finally O / l and L = m + ln l.
+ *
+ * q           fp16 [B][Hq][N][128].
+ * k8, v8, s_k, s_v  as written by turbo_quantize_kv for the same B, Hkv, N.
+ * B, Hq, Hkv  Hq % Hkv == 0, Hq / Hkv <= 16; query head h reads KV head
+ *             h / (Hq / Hkv).
+ * sm_scale    the softmax temperature 1/sqrt(d) of eq. threesteps (any
+ *             positive finite value is accepted).
+ * causal      nonzero: key t is visible to query r only if t <= r.
+ * o           fp16 [B][Hq][N][128] (output, round-to-nearest-even of O/l).
+ * lse         fp32 [B][Hq][N] or NULL: L = m + ln(l).
+ * B == 0 or N == 0 is a no-op.
+ */
+int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
+                       const float* s_v, int B, int Hq, int Hkv, int N, int d, float sm_scale,
+                       int causal, void* o, float* lse, hipStream_t stream);
+
+/*
+ * turbo_attn_decode — Algorithm 2 (TurboAttention decode): the new query of
+ * each sequence is quantized to int8 per (b, query head); every cached
+ * 64-token group is expanded from int4/int2 to int8 in the kernel with
+ * code * s^int + z^int, and the same SAS online softmax as prefill runs with
+ * one query row (P scale per row and group).
+ *
+ * Split-KV extension (not in the paper): the groups of a sequence are cut
+ * into chunks of kv_split_groups groups.  Each chunk runs the online loop
+ * from m = -inf; with more than one chunk the partial states are merged with
+ * m* = max m_s, w_s = SAS(m_s - m*), O = sum w_s O_s / sum w_s l_s,
+ * L = m* + ln(sum w_s l_s), chunks in ascending order.  With one chunk the
+ * result is the unsplit Algorithm 2.
+ *
+ * q               fp16 [B][Hq][128].
+ * cache           as filled by turbo_quantize_kv (num_kv_heads = Hkv).
+ * seq_lens        device int32 [B]: cached tokens of each sequence; only the
+ *                 floor(seq_len/64) full groups are attended (the int8 tail
+ *                 buffer of Sec. 3.3 is not part of this call); values are
+ *                 clamped to [0, 64*max_groups_per_seq].  A sequence with no
+ *                 full group yields o = 0 and lse = -inf.
+ * block_table,
+ * group_table     as for turbo_quantize_kv.  A group whose page or slot entry
+ *                 is out of range is skipped (its memory is never read).
+ * B, Hq           Hq % Hkv == 0, Hq / Hkv <= 16.
+ * kv_split_groups groups per chunk, >= 1; 0 selects
+ *                 turbo_decode_auto_split(B, Hq / Hkv ... ) (see below).
+ * workspace       device scratch of at least turbo_decode_workspace_bytes()
+ *                 bytes (may be NULL when that is 0).
+ * o               fp16 [B][Hq][128];  lse fp32 [B][Hq] or NULL.
+ */
+int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+                      const int32_t* block_table, const int32_t* group_table,
+                      int max_groups_per_seq, int B, int Hq, float sm_scale, int kv_split_groups,
+                      void* workspace, size_t workspace_bytes, void* o, float* lse,
+                      hipStream_t stream);
+
+/* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
+ * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq. */
+int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq);
+
+/* Workspace bytes turbo_attn_decode needs for these arguments (0 when every
+ * sequence fits one chunk).  kv_split_groups = 0 means the automatic value
+ * for Hkv = Hq (an upper bound for any Hkv dividing Hq is obtained by
+ * passing the explicit split). */
+size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
+                                    int kv_split_groups);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TURBO_ATTN_H */

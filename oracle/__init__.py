@@ -1,0 +1,242 @@
+"""CPU oracle of TurboAttention (FlashQ + SAS) — TEST INFRASTRUCTURE ONLY.
+
+Only tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  It wraps ``turbo_oracle.c`` (plain C,
+written from the paper, sharing nothing with the GPU library) with numpy.
+
+Each wrapper names the paper passage its C function follows; the arithmetic
+and its readings are documented in ``turbo_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "turbo_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+# -O2 without fast-math and without FMA contraction: every binary32 operation
+# of the C source is one IEEE operation.  Generic x86-64 code (no -march).
+CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+          "-fno-fast-math", "-Wall", "-Wno-unused-function"]
+
+
+def build(force: bool = True) -> str:
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Opts(ctypes.Structure):
+    _fields_ = [("quant", ctypes.c_int), ("sas", ctypes.c_int)]
+
+
+class Trace(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int), ("h", ctypes.c_int), ("i", ctypes.c_int), ("j", ctypes.c_int),
+                ("hit", ctypes.c_int),
+                ("q8", ctypes.c_void_p), ("sacc", ctypes.c_void_p), ("qp", ctypes.c_void_p),
+                ("pvacc", ctypes.c_void_p), ("sq", ctypes.c_float), ("pmax", ctypes.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        I, F, L, D = ctypes.c_int, ctypes.c_float, ctypes.c_long, ctypes.c_double
+        sig = {
+            "or_num_threads": ([], I),
+            "or_lut": ([I], F),
+            "or_poly": ([F], F),
+            "or_sas_y": ([F], F),
+            "or_sas": ([F], F),
+            "or_sas_y_vec": ([P, L, P], None),
+            "or_poly_vec": ([P, L, P], None),
+            "or_block_quant_vec": ([P, L, L, P, P], None),
+            "or_step2_vec": ([P, I, I, I, P, P, P], None),
+            "or_sas_softmax_rows": ([P, I, I, P], None),
+            "or_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P], None),
+            "or_attn_prefill": ([P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P], None),
+            "or_attn_decode": ([P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P],
+                               None),
+            "or_attn_exact": ([P, P, P, I, I, I, I, I, I, D, I, P, P], None),
+        }
+        for name, (args, res) in sig.items():
+            fn = getattr(_lib, name)
+            fn.argtypes = args
+            fn.restype = res
+    return _lib
+
+
+def _p(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f32(x) -> np.ndarray:
+    """fp16 (numpy or torch) -> contiguous float32 numpy (exact)."""
+    if hasattr(x, "detach"):
+        x = x.detach().cpu().float().numpy()
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+
+
+def num_threads() -> int:
+    return lib().or_num_threads()
+
+
+# ---- SAS (Sec. 4; Algorithm 3) -------------------------------------------
+def lut(k: int) -> float:
+    return lib().or_lut(k)
+
+
+def sas_y(y) -> np.ndarray:
+    """SAS of x = -y for y >= 0 (binary32), elementwise."""
+    y = np.ascontiguousarray(np.asarray(y, dtype=np.float32))
+    out = np.empty_like(y)
+    lib().or_sas_y_vec(_p(y), y.size, _p(out))
+    return out
+
+
+def sas(x) -> np.ndarray:
+    """SAS(x) in the paper's sign convention (x <= 0)."""
+    return sas_y(-np.asarray(x, dtype=np.float32))
+
+
+def poly(f) -> np.ndarray:
+    f = np.ascontiguousarray(np.asarray(f, dtype=np.float32))
+    out = np.empty_like(f)
+    lib().or_poly_vec(_p(f), f.size, _p(out))
+    return out
+
+
+def sas_softmax_rows(x) -> np.ndarray:
+    """Algorithm 3 on the rows of a 2-D array."""
+    x = _f32(x)
+    out = np.empty(x.shape, dtype=np.float64)
+    lib().or_sas_softmax_rows(_p(x), x.shape[0], x.shape[1], _p(out))
+    return out
+
+
+# ---- FlashQ (eq. step1bpq, step2bpq) ---------------------------------------
+def block_quant(x) -> tuple:
+    """Symmetric int8 of blocks: x [..., n] -> (q int8 [..., n], s float32 [...])."""
+    x = _f32(x)
+    n = x.shape[-1]
+    nblk = x.size // n if n else 0
+    q = np.empty(x.shape, dtype=np.int8)
+    s = np.empty(x.shape[:-1], dtype=np.float32)
+    lib().or_block_quant_vec(_p(x), nblk, n, _p(q), _p(s))
+    return q, s
+
+
+def step2(q1, bits: int) -> tuple:
+    """Asymmetric step 2 of groups along axis 0: q1 int8 [n][ncol] ->
+    (s uint8 [ncol], z int8 [ncol], code uint8 [n][ncol])."""
+    q1 = np.ascontiguousarray(np.asarray(q1, dtype=np.int8))
+    n, ncol = q1.shape
+    s = np.empty(ncol, np.uint8)
+    z = np.empty(ncol, np.int8)
+    code = np.empty((n, ncol), np.uint8)
+    lib().or_step2_vec(_p(q1), n, ncol, bits, _p(s), _p(z), _p(code))
+    return s, z, code
+
+
+def quantize_kv(k, v, bits) -> dict:
+    """FlashQ of K/V [B][Hkv][N][d] (fp16 values) with per-head bits."""
+    k, v = _f32(k), _f32(v)
+    B, Hkv, N, d = k.shape
+    nb, ng = (N + 63) // 64, N // 64
+    bits = np.ascontiguousarray(np.asarray(bits, dtype=np.int32))
+    out = dict(
+        k8=np.empty((B, Hkv, N, d), np.int8), v8=np.empty((B, Hkv, N, d), np.int8),
+        sk=np.empty((B, Hkv, nb), np.float32), sv=np.empty((B, Hkv, nb), np.float32),
+        kc=np.empty((B, Hkv, ng * 64, d), np.uint8), vc=np.empty((B, Hkv, ng * 64, d), np.uint8),
+        ks=np.empty((B, Hkv, ng, d), np.uint8), kz=np.empty((B, Hkv, ng, d), np.int8),
+        vs=np.empty((B, Hkv, ng, d), np.uint8), vz=np.empty((B, Hkv, ng, d), np.int8))
+    o = out
+    lib().or_quantize_kv(_p(k), _p(v), B, Hkv, N, d, _p(bits), _p(o["k8"]), _p(o["v8"]),
+                         _p(o["sk"]), _p(o["sv"]), _p(o["kc"]), _p(o["vc"]), _p(o["ks"]),
+                         _p(o["kz"]), _p(o["vs"]), _p(o["vz"]))
+    out["bits"] = bits
+    return out
+
+
+def _trace(d: int, sel):
+    if sel is None:
+        return None, None
+    bufs = dict(q8=np.zeros((64, d), np.int8), sacc=np.zeros((64, 64), np.int32),
+                qp=np.zeros((64, 64), np.int8), pvacc=np.zeros((64, d), np.int32))
+    b, h, i, j = sel
+    tr = Trace(b, h, i, j, 0, _p(bufs["q8"]).value, _p(bufs["sacc"]).value, _p(bufs["qp"]).value,
+               _p(bufs["pvacc"]).value, 0.0, 0.0)
+    return tr, bufs
+
+
+def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = True,
+                 sas: bool = True, trace=None):
+    """Algorithm 1.  q [B][Hq][N][d], k, v [B][Hkv][N][d] (fp16 values).
+    Returns (o float64 [B][Hq][N][d] = O/l before fp16 rounding, lse float64
+    [B][Hq][N]) and, with trace=(b, h, i, j), a dict of that tile's integers."""
+    q, k, v = _f32(q), _f32(k), _f32(v)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    o = np.empty((B, Hq, N, d), np.float64)
+    lse = np.empty((B, Hq, N), np.float64)
+    tr, bufs = _trace(d, trace)
+    lib().or_attn_prefill(_p(q), _p(k), _p(v), B, Hq, Hkv, N, d, float(np.float32(sm_scale)),
+                          int(causal), _Opts(int(quant), int(sas)), _p(o), _p(lse),
+                          ctypes.byref(tr) if tr is not None else None)
+    if tr is None:
+        return o, lse
+    bufs.update(hit=tr.hit, sq=np.float32(tr.sq), pmax=np.float32(tr.pmax))
+    return o, lse, bufs
+
+
+def attn_decode(q, qkv: dict, seq_lens, sm_scale: float, split: int, quant: bool = True,
+                sas: bool = True, trace=None):
+    """Algorithm 2 (+ split-KV merge).  q [B][Hq][d] fp16 values; qkv is the
+    dict of quantize_kv; seq_lens int [B].  trace=(b, h, group)."""
+    q = _f32(q)
+    B, Hq, d = q.shape
+    Hkv = qkv["kc"].shape[1]
+    Nc = qkv["kc"].shape[2]
+    ng = Nc // 64
+    sk = np.ascontiguousarray(qkv["sk"][:, :, :ng])
+    sv = np.ascontiguousarray(qkv["sv"][:, :, :ng])
+    sl = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int32))
+    o = np.empty((B, Hq, d), np.float64)
+    lse = np.empty((B, Hq), np.float64)
+    tr, bufs = _trace(d, None if trace is None else (trace[0], trace[1], 0, trace[2]))
+    c = {n: np.ascontiguousarray(qkv[n]) for n in ("kc", "vc", "ks", "kz", "vs", "vz")}
+    lib().or_attn_decode(_p(q), _p(c["kc"]), _p(c["vc"]), _p(c["ks"]), _p(c["kz"]), _p(c["vs"]),
+                         _p(c["vz"]), _p(sk), _p(sv), _p(sl), B, Hq, Hkv, Nc, d,
+                         float(np.float32(sm_scale)), int(split), _Opts(int(quant), int(sas)),
+                         _p(o), _p(lse), ctypes.byref(tr) if tr is not None else None)
+    if tr is None:
+        return o, lse
+    bufs.update(hit=tr.hit, sq=np.float32(tr.sq), pmax=np.float32(tr.pmax))
+    return o, lse, bufs
+
+
+def attn_exact(q, k, v, sm_scale: float, causal: bool = True):
+    """Exact softmax attention in double (eq. stdattn).  q [B][Hq][Nq][d],
+    k, v [B][Hkv][Nk][d]; query r sits at position r + Nk - Nq."""
+    q, k, v = _f32(q), _f32(k), _f32(v)
+    B, Hq, Nq, d = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
+    o = np.empty((B, Hq, Nq, d), np.float64)
+    lse = np.empty((B, Hq, Nq), np.float64)
+    lib().or_attn_exact(_p(q), _p(k), _p(v), B, Hq, Hkv, Nq, Nk, d, float(sm_scale), int(causal),
+                        _p(o), _p(lse))
+    return o, lse

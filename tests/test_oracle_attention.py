@@ -1,0 +1,187 @@
+"""Pins of the oracle's attention loops (Algorithms 1 and 2).
+
+- With FlashQ and SAS switched off the online loop must reduce to exact softmax
+  attention (eq. stdattn) — checked against torch's CPU attention in float64.
+- Integer contractions of a traced tile equal brute-force matrix products.
+- Uniform scores reduce the loop to a closed form that exposes the tile order,
+  the per-tile P scale and the rescale factor SAS(0) of an unchanged maximum.
+- Invariants: causality per key block, GQA = MHA with repeated KV heads,
+  decode with one chunk = unsplit decode, split merge exact under exp.
+"""
+import numpy as np
+import pytest
+import torch
+
+D = 128
+SM = 1.0 / np.sqrt(128.0)
+
+
+def _rand(shape, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(*shape, generator=g) * scale).half()
+
+
+def _torch_attn(q, k, v, causal):
+    qf, kf, vf = (t.double() for t in (q, k, v))
+    G = qf.shape[1] // kf.shape[1]
+    kf = kf.repeat_interleave(G, dim=1)
+    vf = vf.repeat_interleave(G, dim=1)
+    return torch.nn.functional.scaled_dot_product_attention(qf, kf, vf, is_causal=causal,
+                                                           scale=float(np.float32(SM))).numpy()
+
+
+@pytest.mark.parametrize("N,causal,Hq,Hkv", [(64, True, 2, 2), (200, True, 4, 2), (130, False, 2, 1),
+                                             (257, True, 3, 3)])
+def test_skeleton_reduces_to_exact_attention(orc, N, causal, Hq, Hkv):
+    q, k, v = _rand((2, Hq, N, D), 1), _rand((2, Hkv, N, D), 2, 2.0), _rand((2, Hkv, N, D), 3)
+    o, lse = orc.attn_prefill(q, k, v, SM, causal, quant=False, sas=False)
+    ref = _torch_attn(q, k, v, causal)
+    assert np.max(np.abs(o - ref)) < 1e-12
+    oe, lsee = orc.attn_exact(q, k, v, float(np.float32(SM)), causal)
+    assert np.max(np.abs(oe - ref)) < 1e-12
+    assert np.max(np.abs(lse - lsee)) < 1e-12
+
+
+def test_traced_tile_integers_are_matrix_products(orc):
+    B, H, N = 1, 2, 64 * 3
+    q, k, v = _rand((B, H, N, D), 4), _rand((B, H, N, D), 5), _rand((B, H, N, D), 6)
+    c = orc.quantize_kv(k, v, [4, 4])
+    for (i, j) in [(2, 0), (2, 2), (1, 1)]:
+        _, _, tr = orc.attn_prefill(q, k, v, SM, True, trace=(0, 1, i, j))
+        assert tr["hit"]
+        q8, s = orc.block_quant(q[0, 1, 64 * i:64 * i + 64].float().numpy().reshape(1, -1))
+        assert np.array_equal(tr["q8"], q8.reshape(64, D)) and tr["sq"] == s[0]
+        k8 = c["k8"][0, 1, 64 * j:64 * j + 64].astype(np.int64)
+        v8 = c["v8"][0, 1, 64 * j:64 * j + 64].astype(np.int64)
+        sacc = tr["q8"].astype(np.int64) @ k8.T
+        vis = np.ones((64, 64), bool) if j < i else np.tril(np.ones((64, 64), bool))
+        assert np.array_equal(tr["sacc"][vis], sacc[vis])
+        qp = tr["qp"].astype(np.int64)
+        assert qp.min() >= 0 and qp.max() == 119 and np.all(qp[~vis] == 0)
+        assert np.array_equal(tr["pvacc"], qp @ v8)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_uniform_scores_closed_form(orc, causal):
+    """Q = 0 makes every score 0, so every kept P~ is SAS(0) = a, every tile
+    quantizes P~ to 119 with s_P = a/119, and the maximum never moves, so each
+    later tile multiplies the history by a.  Row r then averages the dequantized
+    V rows with weight a^(age of the tile) — a closed form."""
+    N = 64 * 3 + 21
+    q = torch.zeros(1, 1, N, D, dtype=torch.float16)
+    k, v = _rand((1, 1, N, D), 7), _rand((1, 1, N, D), 8)
+    o, lse = orc.attn_prefill(q, k, v, SM, causal)
+    a = np.float64(np.float32(0.9996))
+    sp = np.float32(np.float32(0.9996) / np.float32(119))
+    nb = (N + 63) // 64
+    v8, sv = [], []
+    for j in range(nb):
+        qq, s = orc.block_quant(v[0, 0, 64 * j:64 * j + 64].float().numpy().reshape(1, -1))
+        v8.append(qq.reshape(-1, D).astype(np.float64))
+        sv.append(s[0])
+    for r in range(N):
+        i = r // 64
+        last = i if causal else nb - 1
+        num = np.zeros(D)
+        den = 0.0
+        for j in range(last + 1):
+            keys = v8[j] if (not causal or j < i) else v8[j][: r % 64 + 1]
+            w = a ** (last - j)
+            num += w * np.float64(np.float32(sp * sv[j])) * 119 * keys.sum(axis=0)
+            den += w * a * keys.shape[0]
+        assert np.allclose(o[0, 0, r], num / den, rtol=1e-12, atol=1e-15), r
+        assert abs(lse[0, 0, r] - np.log(den)) < 1e-12
+
+
+def test_causality_per_key_block(orc):
+    """Changing K/V in key blocks after query block i leaves rows of block i
+    unchanged bit for bit (block scales of earlier blocks do not move)."""
+    N = 64 * 4
+    q, k, v = _rand((1, 2, N, D), 10), _rand((1, 2, N, D), 11), _rand((1, 2, N, D), 12)
+    o1, l1 = orc.attn_prefill(q, k, v, SM, True)
+    k2, v2 = k.clone(), v.clone()
+    k2[:, :, 128:] = _rand((1, 2, N - 128, D), 13, 3.0)
+    v2[:, :, 128:] = _rand((1, 2, N - 128, D), 14, 3.0)
+    o2, l2 = orc.attn_prefill(q, k2, v2, SM, True)
+    assert np.array_equal(o1[:, :, :128], o2[:, :, :128])
+    assert np.array_equal(l1[:, :, :128], l2[:, :, :128])
+    assert not np.array_equal(o1[:, :, 128:], o2[:, :, 128:])
+
+
+def test_gqa_equals_mha_with_repeated_heads(orc):
+    N = 64 * 2 + 5
+    q, k, v = _rand((2, 4, N, D), 20), _rand((2, 2, N, D), 21), _rand((2, 2, N, D), 22)
+    o1, l1 = orc.attn_prefill(q, k, v, SM, True)
+    o2, l2 = orc.attn_prefill(q, k.repeat_interleave(2, 1), v.repeat_interleave(2, 1), SM, True)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+def test_prefill_error_vs_exact_is_moderate(orc):
+    """Not a parity gate (the paper fixes accuracy only through task scores):
+    FlashQ+SAS stays within a few percent of exact attention on N(0,1) data."""
+    N = 512
+    q, k, v = _rand((1, 2, N, D), 30), _rand((1, 2, N, D), 31), _rand((1, 2, N, D), 32)
+    o, _ = orc.attn_prefill(q, k, v, SM, True)
+    ex, _ = orc.attn_exact(q, k, v, float(np.float32(SM)), True)
+    rel = np.linalg.norm(o - ex) / np.linalg.norm(ex)
+    assert rel < 0.08
+
+
+def _decode_setup(orc, B=2, Hq=4, Hkv=2, Nc=64 * 5, seed=40, bits=(4, 2)):
+    k, v = _rand((B, Hkv, Nc, D), seed), _rand((B, Hkv, Nc, D), seed + 1)
+    k[..., 3] *= 10
+    q = _rand((B, Hq, D), seed + 2)
+    c = orc.quantize_kv(k, v, list(bits))
+    return q, k, v, c
+
+
+def test_decode_single_chunk_equals_unsplit(orc):
+    q, k, v, c = _decode_setup(orc)
+    sl = [320, 192]
+    o1, l1 = orc.attn_decode(q, c, sl, SM, split=5)
+    o2, l2 = orc.attn_decode(q, c, sl, SM, split=100)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+def test_decode_merge_is_exact_without_approximations(orc):
+    """With FlashQ and SAS off, every chunking equals exact attention over the
+    dequantized cache values (the merge with exp is exact)."""
+    q, k, v, c = _decode_setup(orc)
+    sl = [320, 256]
+    B, Hkv, Nc = 2, 2, 320
+    kd = (c["kc"].astype(np.float64) * c["ks"].repeat(64, axis=2) + c["kz"].repeat(64, axis=2)) \
+        * c["sk"][:, :, :5].repeat(64, axis=2)[..., None]
+    vd = (c["vc"].astype(np.float64) * c["vs"].repeat(64, axis=2) + c["vz"].repeat(64, axis=2)) \
+        * c["sv"][:, :, :5].repeat(64, axis=2)[..., None]
+    for split in (1, 2, 5):
+        o, lse = orc.attn_decode(q, c, sl, SM, split=split, quant=False, sas=False)
+        for b in range(B):
+            n = sl[b]
+            ref = _torch_attn(q[b:b + 1, :, None].float(),
+                              torch.from_numpy(kd[b:b + 1, :, :n]).float(),
+                              torch.from_numpy(vd[b:b + 1, :, :n]).float(), False)[0, :, 0]
+            # kd/vd went through float32 for torch; compare loosely
+            assert np.max(np.abs(o[b] - ref)) < 1e-5, (split, b)
+
+
+def test_decode_traced_group_integers(orc):
+    q, k, v, c = _decode_setup(orc)
+    _, _, tr = orc.attn_decode(q, c, [320, 320], SM, split=2, trace=(1, 3, 4))
+    assert tr["hit"]
+    kh, g = 3 // 2, 4
+    k1 = c["kc"][1, kh, 64 * g:64 * g + 64].astype(np.int64) * c["ks"][1, kh, g].astype(np.int64) \
+        + c["kz"][1, kh, g].astype(np.int64)
+    v1 = c["vc"][1, kh, 64 * g:64 * g + 64].astype(np.int64) * c["vs"][1, kh, g].astype(np.int64) \
+        + c["vz"][1, kh, g].astype(np.int64)
+    q8, s = orc.block_quant(q[1, 3].float().numpy().reshape(1, -1))
+    assert np.array_equal(tr["q8"][0], q8[0]) and tr["sq"] == s[0]
+    assert np.array_equal(tr["sacc"][0], k1 @ q8[0].astype(np.int64))
+    qp = tr["qp"][0].astype(np.int64)
+    assert qp.max() == 119 and qp.min() >= 0
+    assert np.array_equal(tr["pvacc"][0], qp @ v1)
+
+
+def test_decode_empty_sequence(orc):
+    q, k, v, c = _decode_setup(orc)
+    o, lse = orc.attn_decode(q, c, [0, 63], SM, split=2)
+    assert not o.any() and np.all(np.isneginf(lse))
