@@ -1,0 +1,229 @@
+"""Benchmark of the TurboAttention hot path on one MI355X.
+
+A step is one pass of the whole path over one batch of synthetic input:
+  turbo_quantize_kv  (FlashQ step 1 + step 2, K/V -> int8 blocks + int4/int2 cache)
+  turbo_attn_prefill (Algorithm 1: causal FlashQ + SAS attention)
+  turbo_attn_decode  (Algorithm 2: one new query per sequence over the cache)
+on the Phi-3-medium-shaped prefill workload (batch 4, 40 query / 10 KV heads,
+head_dim 128, 4096 tokens, int4 cache) unless --workload says otherwise.
+Inputs are resident in HBM before the timed region.
+
+The JSON line reports the attention int-op rate of the step (dense causal
+count: 4*d ops per visible (query, key) pair of prefill plus 4*d per cached
+key and query head of decode), per-kernel times, the roofline of the dominant
+kernel (HIP-event timed on the stream its launches go to), and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_INT8_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
+PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, 8 TB/s
+
+
+def decode_bytes_per_token(bits: int) -> float:
+    """Compressed K+V bytes read per cached token and KV head: codes plus the
+    per-channel integer scale/zero (4 x 128 B per 64-token group) plus the
+    two fp32 block scales per group."""
+    return 2 * 128 * bits / 8 + 4 * 128 / 64 + 8 / 64
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="phi3m-prefill-4k")
+    ap.add_argument("--kernel-iters", type=int, default=30)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["quantize", "prefill", "decode"], default=None,
+                    help="launch only this kernel --steps times (for profiler passes)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding "
+                          "is described in DESIGN.md but not implemented"}))
+        sys.exit(2)
+    import torch
+
+    import paper_2412_08585_amd as ta
+    from paper_2412_08585_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.WORKLOADS[args.workload]
+    assert w.kind == "prefill", "the step runs prefill then one decode token"
+    B, Hq, Hkv, N, G = w.B, w.Hq, w.Hkv, w.N, w.G
+    d = 128
+
+    # ---- inputs (resident in HBM) -------------------------------------------
+    q, k, v = W.prefill_inputs(w, device=dev)
+    qd = W.decode_query(w, device=dev)
+    bits = W.head_bits(w)
+    bt, gt = W.tables(w)
+    btd, gtd = torch.from_numpy(bt).to(dev), torch.from_numpy(gt).to(dev)
+    cache = ta.PagedKVCache(bt.size, gt.size, bits, dev)
+    nb = (N + 63) // 64
+    k8 = torch.empty(B, Hkv, nb * 64, d, dtype=torch.int8, device=dev)
+    v8 = torch.empty(B, Hkv, nb, d, 64, dtype=torch.int8, device=dev)
+    sk = torch.empty(B, Hkv, nb, dtype=torch.float32, device=dev)
+    sv = torch.empty_like(sk)
+    o = torch.empty_like(q)
+    od = torch.empty_like(qd)
+    lse = torch.empty(B, Hq, N, dtype=torch.float32, device=dev)
+    sl = torch.full((B,), N, dtype=torch.int32, device=dev)
+    split = ta.decode_split(B, Hkv, w.max_groups, 0)
+    ws = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev)
+
+    def run_quant():
+        ta.turbo_quantize_kv(k, v, cache, btd, gtd, out=(k8, v8, sk, sv))
+
+    def run_prefill():
+        ta.turbo_attn_prefill(q, k8, v8, sk, sv, w.sm_scale, True, out=o)
+
+    def run_decode():
+        ta.turbo_attn_decode(qd, cache, sl, btd, gtd, w.sm_scale, split, workspace=ws, out=od)
+
+    def step():
+        run_quant()
+        run_prefill()
+        run_decode()
+
+    if args.only:
+        fn = {"quantize": run_quant, "prefill": run_prefill, "decode": run_decode}[args.only]
+        run_quant()
+        for _ in range(args.warmup + args.steps):
+            fn()
+        torch.cuda.synchronize()
+        print(json.dumps({"only": args.only, "launches": args.warmup + args.steps}))
+        return
+
+    # ---- whole-step timing ----------------------------------------------------
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    # ---- per-kernel timing (same stream, events around repeated launches) ----
+    def time_kernel(fn, iters):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(iters):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / iters
+
+    ms_q = time_kernel(run_quant, args.kernel_iters)
+    ms_p = time_kernel(run_prefill, args.kernel_iters)
+    ms_d = time_kernel(run_decode, args.kernel_iters)
+
+    # ---- algorithmic work -------------------------------------------------------
+    prefill_ops = 2.0 * d * N * (N + 1) * B * Hq          # QK^T + PV over causal pairs
+    decode_ops = 4.0 * d * (N // 64 * 64) * B * Hq
+    step_ops = prefill_ops + decode_ops
+    quant_bytes = B * Hkv * N * d * 2 * 2                 # fp16 K, V in
+    quant_bytes += B * Hkv * nb * 64 * d * 2 + B * Hkv * nb * 8   # int8 K8/V8 + scales out
+    quant_bytes += sum(decode_bytes_per_token(int(bits[h])) for h in range(Hkv)) * B * (N // 64 * 64)
+    decode_bytes = sum(decode_bytes_per_token(int(bits[h])) for h in range(Hkv)) * B * (N // 64 * 64)
+    decode_bytes += B * Hq * d * 2 * 2                    # q in, o out (fp16)
+    prefill_tops = prefill_ops / (ms_p * 1e-3) / 1e12
+
+    result = {
+        "metric": "attention TOPS (prefill) & HBM GB/s (decode), % of MI355X roofline",
+        "value": round(step_ops / (ms_step * 1e-3) / 1e12, 3),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic (seeded N(0,1) fp16 with 4 K outlier channels x10; no weights)",
+        "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "seq_len": N,
+                   "head_dim": d, "causal": True, "kv_cache": w.bits, "decode_tokens": 1,
+                   "decode_kv_split_groups": split},
+        "kernels": {
+            "quantize_kv": {"ms": round(ms_q, 4), "GB/s": round(quant_bytes / ms_q / 1e6, 1),
+                            "frac_hbm": round(quant_bytes / ms_q / 1e6 / PEAK_HBM_GBS, 4)},
+            "attn_prefill": {"ms": round(ms_p, 4), "TOPS": round(prefill_tops, 2),
+                             "frac_int8_mfma": round(prefill_tops / PEAK_INT8_TOPS, 4)},
+            "attn_decode": {"ms": round(ms_d, 4),
+                            "GB/s": round(decode_bytes / ms_d / 1e6, 1),
+                            "frac_hbm": round(decode_bytes / ms_d / 1e6 / PEAK_HBM_GBS, 4),
+                            "note": "cache of this workload (22 MB) may sit in the 256 MB MALL"},
+        },
+        "roofline": {"kernel": "k_attn_prefill", "bound": "mfma",
+                     "achieved": round(prefill_tops, 2), "peak": PEAK_INT8_TOPS,
+                     "unit": "TOP/s", "frac": round(prefill_tops / PEAK_INT8_TOPS, 4),
+                     "traffic": None,
+                     "per_launch_ops": prefill_ops},
+    }
+
+    # ---- CPU oracle on a bounded sample -----------------------------------------
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = oracle.num_threads()
+        n_units = max(1, min(B * Hkv, math.ceil(threads * 5 / G)))
+        rng = np.random.default_rng(0)
+        units = [divmod(int(u), Hkv) for u in rng.choice(B * Hkv, n_units, replace=False)]
+        qs = torch.stack([q[b, h * G:(h + 1) * G] for b, h in units])[:, :, :, :].cpu()
+        ks = torch.stack([k[b, h] for b, h in units])[:, None].cpu()
+        vs = torch.stack([v[b, h] for b, h in units])[:, None].cpu()
+        # one sampled unit = one sequence with one KV head and its G query heads
+        qs = qs.reshape(n_units, G, N, d)
+        qds = torch.stack([qd[b, h * G:(h + 1) * G] for b, h in units]).cpu()
+        t0 = time.perf_counter()
+        ref = oracle.quantize_kv(ks.reshape(n_units, 1, N, d), vs.reshape(n_units, 1, N, d),
+                                 [4])
+        ro, _ = oracle.attn_prefill(qs, ks.reshape(n_units, 1, N, d), vs.reshape(n_units, 1, N, d),
+                                    w.sm_scale, True)
+        oracle.attn_decode(qds, ref, [N] * n_units, w.sm_scale, split=split)
+        dt = time.perf_counter() - t0
+        sample_ops = (prefill_ops + decode_ops) * n_units / (B * Hkv)
+        result["cpu_baseline"] = {
+            "value": round(sample_ops / dt / 1e12, 6), "unit": "TOPS",
+            "cores": min(threads, n_units * G), "kind": "oracle",
+            "sample": f"{n_units} of {B * Hkv} (sequence, KV head) units, full length "
+                      f"(quantize + prefill + decode), {dt:.1f} s"}
+        # parity and error of the sampled units (reported, not gated here)
+        got = torch.stack([o[b, h * G:(h + 1) * G] for b, h in units]).float().cpu().numpy()
+        rowmax = np.abs(ro).max(axis=-1, keepdims=True)
+        b0, h0 = units[0]
+        ex, _ = oracle.attn_exact(qs[:1], ks[:1].reshape(1, 1, N, d), vs[:1].reshape(1, 1, N, d),
+                                  float(np.float32(w.sm_scale)), True)
+        rel = lambda a, r: float(np.linalg.norm(a - r) / np.linalg.norm(r))
+        result["parity"] = {
+            "max_err_vs_oracle_rel_rowmax": float(np.max(np.abs(got - ro) / rowmax)),
+            "rel_l2_vs_exact_fp64_gpu": rel(got[:1], ex), "rel_l2_vs_exact_fp64_oracle": rel(ro[:1], ex),
+            "sample_units": n_units}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

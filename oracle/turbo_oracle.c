@@ -315,7 +315,8 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
  * Query head h uses KV head h / (Hq/Hkv).  causal: key t visible to query r
  * iff t <= r; a (row, tile) pair without a visible key is not processed.
  * Outputs: o double [B][Hq][N][d] = O / l before any rounding to fp16;
- * lse double [B][Hq][N] = m + ln l.
+ * lse double [B][Hq][N] = m + ln l.  Only query blocks i0 <= i < i1 are
+ * computed (i0 = i1 = -1: all); other rows of o and lse are not written.
  * Readings: the softmax temperature of eq. threesteps multiplies the scores,
  * S = fl(fl(acc) * fl(fl(s_Q * s_K) * sm_scale)); Algorithm 1 writes the
  * accumulator update with the inverse of diag(SAS(m_old - m_new)), which
@@ -324,7 +325,7 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
  * is SAS(0) as written. */
 void or_attn_prefill(const float* q, const float* k, const float* v, int B, int Hq, int Hkv,
                      int N, int d, float sm_scale, int causal, or_opts opts, double* o,
-                     double* lse, or_trace* tr) {
+                     double* lse, or_trace* tr, int i0, int i1) {
   const int G = Hq / Hkv, nb = (N + OR_BS - 1) / OR_BS;
 #pragma omp parallel
   {
@@ -353,7 +354,7 @@ void or_attn_prefill(const float* q, const float* k, const float* v, int B, int 
             sk[j] = or_block_quant(kk + (size_t)r0 * d, (long)nr * d, k8 + (size_t)r0 * d);
             sv[j] = or_block_quant(vv + (size_t)r0 * d, (long)nr * d, v8 + (size_t)r0 * d);
           }
-        for (int i = 0; i < nb; ++i) {
+        for (int i = i0 < 0 ? 0 : i0; i < (i1 < 0 || i1 > nb ? nb : i1); ++i) {
           const int q0 = i * OR_BS, nq = (N - q0) < OR_BS ? (N - q0) : OR_BS;
           float sq = 0.0f; /* Q_i^{q1} (eq. step1bpq) */
           if (opts.quant) sq = or_block_quant(qq + (size_t)q0 * d, (long)nq * d, q8);

@@ -1,1 +1,10 @@
-"""MI355X (gfx950) TurboAttention hot path: FlashQ + SAS quantized attention."""
+"""MI355X (gfx950) TurboAttention hot path: FlashQ + SAS quantized attention.
+
+The computation lives in libturboattn.so (hand-written HIP for gfx950 behind
+the C ABI of include/turbo_attn.h); this package only marshals arguments.
+"""
+from .binding import (PagedKVCache, TurboKVCacheStruct, decode_split, decode_workspace, lib,
+                      page_bytes, turbo_attn_decode, turbo_attn_prefill, turbo_quantize_kv)
+
+__all__ = ["PagedKVCache", "TurboKVCacheStruct", "decode_split", "decode_workspace", "lib",
+           "page_bytes", "turbo_attn_decode", "turbo_attn_prefill", "turbo_quantize_kv"]

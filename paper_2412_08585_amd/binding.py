@@ -1,0 +1,188 @@
+"""Thin Python binding of libturboattn.so (argument marshalling only).
+
+The functions carry the C ABI's names and forward torch tensors as raw device
+pointers together with torch's current HIP stream.  Every computation runs in
+the library's gfx950 kernels; if the library is missing or the device is not
+gfx950 the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+HEAD_DIM = 128
+BLOCK = 64
+PAGE_TOKENS = 16
+MAX_KV_HEADS = 64
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libturboattn.so")
+
+
+class TurboKVCacheStruct(ctypes.Structure):
+    """Mirror of turbo_kv_cache (include/turbo_attn.h)."""
+    _fields_ = [("pages", ctypes.c_void_p), ("group_meta", ctypes.c_void_p),
+                ("group_scale", ctypes.c_void_p), ("num_pages", ctypes.c_int64),
+                ("num_group_slots", ctypes.c_int64), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("head_bits", ctypes.c_uint8 * MAX_KV_HEADS)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the in-tree HIP library; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2412_08585_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I, F, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        sig = {
+            "turbo_abi_version": ([], I),
+            "turbo_strerror": ([I], ctypes.c_char_p),
+            "turbo_page_bytes": ([P, I], Z),
+            "turbo_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, I, P], I),
+            "turbo_attn_prefill": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
+            "turbo_attn_decode": ([P, P, P, P, P, I, I, I, F, I, P, Z, P, P, P], I),
+            "turbo_decode_auto_split": ([I, I, I], I),
+            "turbo_decode_workspace_bytes": ([I, I, I, I, I], Z),
+        }
+        for name, (args, res) in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        msg = lib().turbo_strerror(status).decode()
+        raise RuntimeError(f"{what} failed: {msg} ({status})")
+
+
+def page_bytes(head_bits) -> int:
+    hb = np.ascontiguousarray(np.asarray(head_bits, dtype=np.uint8))
+    return int(lib().turbo_page_bytes(hb.ctypes.data_as(ctypes.c_void_p), hb.size))
+
+
+class PagedKVCache:
+    """Device storage of the compressed cache (pages, group metadata, group
+    scales) plus the host copy of the per-head bit widths."""
+
+    def __init__(self, num_pages: int, num_group_slots: int, head_bits, device="cuda"):
+        self.head_bits = np.ascontiguousarray(np.asarray(head_bits, dtype=np.uint8))
+        self.num_kv_heads = int(self.head_bits.size)
+        self.page_bytes = page_bytes(self.head_bits)
+        if self.page_bytes == 0:
+            raise ValueError("head_bits must hold 1..64 entries of 2 or 4")
+        self.pages = torch.zeros(num_pages, self.page_bytes, dtype=torch.uint8, device=device)
+        self.group_meta = torch.zeros(num_group_slots, self.num_kv_heads, 4, HEAD_DIM,
+                                      dtype=torch.int8, device=device)
+        self.group_scale = torch.zeros(num_group_slots, self.num_kv_heads, 2,
+                                       dtype=torch.float32, device=device)
+
+    def struct(self) -> TurboKVCacheStruct:
+        s = TurboKVCacheStruct()
+        s.pages = self.pages.data_ptr()
+        s.group_meta = self.group_meta.data_ptr()
+        s.group_scale = self.group_scale.data_ptr()
+        s.num_pages = self.pages.shape[0]
+        s.num_group_slots = self.group_meta.shape[0]
+        s.num_kv_heads = self.num_kv_heads
+        s.head_dim = HEAD_DIM
+        for i, b in enumerate(self.head_bits):
+            s.head_bits[i] = int(b)
+        return s
+
+
+def turbo_quantize_kv(k: torch.Tensor, v: torch.Tensor, cache: Optional[PagedKVCache] = None,
+                      block_table: Optional[torch.Tensor] = None,
+                      group_table: Optional[torch.Tensor] = None, out=None):
+    """FlashQ of K, V fp16 [B][Hkv][N][128].  Returns (k8, v8, s_k, s_v) in the
+    layouts of include/turbo_attn.h; writes the full groups into `cache`."""
+    B, Hkv, N, d = k.shape
+    nb = (N + BLOCK - 1) // BLOCK
+    dev = k.device
+    if out is None:
+        k8 = torch.empty(B, Hkv, nb * BLOCK, d, dtype=torch.int8, device=dev)
+        v8 = torch.empty(B, Hkv, nb, d, BLOCK, dtype=torch.int8, device=dev)
+        s_k = torch.empty(B, Hkv, nb, dtype=torch.float32, device=dev)
+        s_v = torch.empty(B, Hkv, nb, dtype=torch.float32, device=dev)
+    else:
+        k8, v8, s_k, s_v = out
+    cs = cache.struct() if cache is not None else None
+    mg = group_table.shape[1] if group_table is not None else 0
+    st = lib().turbo_quantize_kv(_ptr(k), _ptr(v), B, Hkv, N, d, _ptr(k8), _ptr(v8), _ptr(s_k),
+                                 _ptr(s_v), ctypes.byref(cs) if cs is not None else None,
+                                 _ptr(block_table), _ptr(group_table), mg, _stream(dev))
+    _check(st, "turbo_quantize_kv")
+    return k8, v8, s_k, s_v
+
+
+def turbo_attn_prefill(q: torch.Tensor, k8, v8, s_k, s_v, sm_scale: Optional[float] = None,
+                       causal: bool = True, return_lse: bool = False, out=None):
+    """Algorithm 1 prefill.  q fp16 [B][Hq][N][128]; k8/v8/s_k/s_v from
+    turbo_quantize_kv.  Returns o fp16 [B][Hq][N][128] (and lse fp32)."""
+    B, Hq, N, d = q.shape
+    Hkv = s_k.shape[1]
+    sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty(B, Hq, N, dtype=torch.float32, device=q.device) if return_lse else None
+    st = lib().turbo_attn_prefill(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B, Hq, Hkv,
+                                  N, d, sm, int(bool(causal)), _ptr(o), _ptr(lse),
+                                  _stream(q.device))
+    _check(st, "turbo_attn_prefill")
+    return (o, lse) if return_lse else o
+
+
+def decode_split(B: int, Hkv: int, max_groups: int, kv_split_groups: int = 0) -> int:
+    return kv_split_groups or int(lib().turbo_decode_auto_split(B, Hkv, max_groups))
+
+
+def decode_workspace(B: int, Hq: int, Hkv: int, max_groups: int, kv_split_groups: int = 0,
+                     device="cuda") -> Optional[torch.Tensor]:
+    n = int(lib().turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups, kv_split_groups))
+    if n == 0:
+        return None
+    return torch.empty(n // 4, dtype=torch.float32, device=device)
+
+
+def turbo_attn_decode(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tensor,
+                      block_table: torch.Tensor, group_table: torch.Tensor,
+                      sm_scale: Optional[float] = None, kv_split_groups: int = 0,
+                      workspace: Optional[torch.Tensor] = None, return_lse: bool = False,
+                      out=None):
+    """Algorithm 2 decode over the paged cache.  q fp16 [B][Hq][128]."""
+    B, Hq, d = q.shape
+    mg = group_table.shape[1]
+    sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
+    if workspace is None:
+        workspace = decode_workspace(B, Hq, cache.num_kv_heads, mg, kv_split_groups, q.device)
+    wbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty(B, Hq, dtype=torch.float32, device=q.device) if return_lse else None
+    cs = cache.struct()
+    st = lib().turbo_attn_decode(_ptr(q), ctypes.byref(cs), _ptr(seq_lens), _ptr(block_table),
+                                 _ptr(group_table), mg, B, Hq, sm, int(kv_split_groups),
+                                 _ptr(workspace), wbytes, _ptr(o), _ptr(lse), _stream(q.device))
+    _check(st, "turbo_attn_decode")
+    return (o, lse) if return_lse else o

@@ -1,0 +1,244 @@
+// TurboAttention prefill on gfx950 (Algorithm 1): int8 QK^T and PV on the
+// 32x32x32 i8 MFMA, SAS online softmax in fp32 on the VALU.
+//
+// One wave owns one (sequence b, query head h, 64-query block i) and runs
+// over the key blocks j (j <= i when causal).
+//
+// Register layout.  The scores are computed transposed, S^T = K Q^T, so that
+// each lane holds one query column:  for the 32x32 output block (kb, qb)
+// (32-key half kb, 32-query half qb), lane n + 32*hf, register r holds query
+// 32qb + n and key 32kb + 16hf + r.  This is obtained by feeding A-operand
+// row m of the K block with key 16*((m>>2)&1) + 4*(m>>3) + (m&3), the inverse
+// of the MFMA output row map 8(r/4) + 4hf + r%4.  Consequently the 16
+// quantized P values of a lane are, byte for byte, its B-operand for
+// O^T = V^T P^T with contraction index (hf, byte i) <-> key 16hf + i, and V^T
+// is read as 16 contiguous bytes of the channel-major int8 V block.  Row max
+// and row sum need one exchange between lanes n and n + 32.
+#include "turbo_common.h"
+
+namespace turbo {
+
+struct PrefillArgs {
+  const uint4* q;      // fp16 [B][Hq][N][128]
+  const int8_t* k8;    // [B][Hkv][nb*64][128]
+  const int8_t* v8;    // [B][Hkv][nb][128][64]
+  const float* sk;     // [B][Hkv][nb]
+  const float* sv;
+  int B, Hq, Hkv, N, nb;
+  float sm_scale;
+  int causal;
+  uint2* o;            // fp16 [B][Hq][N][128] (as 4-half units)
+  float* lse;          // [B][Hq][N] or null
+};
+
+__global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
+  __shared__ float lut[8];
+  const int lane = threadIdx.x;
+  if (lane < 8) lut[lane] = kLut[lane];
+  __syncthreads();
+
+  const int BH = a.B * a.Hq;
+  const int L = xcd_remap(blockIdx.x, BH * a.nb);
+  const int i = a.nb - 1 - L / BH;  // longest causal rows first
+  const int b = (L % BH) / a.Hq, h = L % a.Hq;
+  const int G = a.Hq / a.Hkv, kh = h / G;
+  const int n = lane & 31, hf = lane >> 5;
+  const int N = a.N;
+
+  // ---- Q_i -> int8 (eq. step1bpq), held as the QK^T B-operand ----------
+  // lane (n + 32hf), k-step ks: channels 32ks + 16hf .. +15 of query 32qb + n
+  v4i qop[2][4];
+  float sq;
+  {
+    uint4 raw[2][4][2];
+    float amax = 0.0f;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int row = 64 * i + 32 * qb + n;
+      const uint4* src = a.q + (((long)b * a.Hq + h) * N + row) * 16;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          raw[qb][ks][u] = row < N ? src[4 * ks + 2 * hf + u] : make_uint4(0, 0, 0, 0);
+          f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[qb][ks][u]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
+        }
+    }
+    amax = wave_max(amax);
+    float inv = 0.0f;
+    sq = 0.0f;
+    if (amax > 0.0f) {
+      sq = amax / kQmax;
+      inv = kQmax / amax;
+    }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        int w[4];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[qb][ks][u]);
+          int qv[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
+          w[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
+          w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
+        }
+        qop[qb][ks] = v4i{w[0], w[1], w[2], w[3]};
+      }
+  }
+
+  const long kvu = (long)b * a.Hkv + kh;
+  const int8_t* kbase = a.k8 + kvu * a.nb * 8192;
+  const int8_t* vbase = a.v8 + kvu * a.nb * 8192;
+  const float* skp = a.sk + kvu * a.nb;
+  const float* svp = a.sv + kvu * a.nb;
+
+  // A-operand row m of a 32-key half holds key kidx(m)
+  const int m = lane & 31;
+  const int kidx = 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3);
+
+  float O[4][2][16];
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) O[cb][qb][r] = 0.0f;
+  float mrow[2] = {-INFINITY, -INFINITY};
+  float lhalf[2] = {0.0f, 0.0f};
+
+  const int jend = a.causal ? i : a.nb - 1;
+  for (int j = 0; j <= jend; ++j) {
+    // ---- S^T = K_j Q_i^T (int32) -------------------------------------
+    v16i sacc[2][2];
+    {
+      v4i kop[2][4];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+          kop[kb][ks] = *reinterpret_cast<const v4i*>(
+              kbase + ((long)j * 64 + 32 * kb + kidx) * 128 + 32 * ks + 16 * hf);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          v16i acc = {};
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x32(kop[kb][ks], qop[qb][ks], acc);
+          sacc[kb][qb] = acc;
+        }
+    }
+    // ---- scores, online max, SAS ------------------------------------
+    const float c = (sq * skp[j]) * a.sm_scale;
+    float P[2][2][16];
+    float alpha[2];
+    float pmax = 0.0f;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int qrow = 64 * i + 32 * qb + n;
+      float smax = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = 64 * j + 32 * kb + 16 * hf + r;
+          const bool vis = key < N && qrow < N && (!a.causal || key <= qrow);
+          const float s = (float)sacc[kb][qb][r] * c;
+          P[kb][qb][r] = vis ? s : -INFINITY;
+          smax = fmaxf(smax, P[kb][qb][r]);
+        }
+      smax = fmaxf(smax, __shfl_xor(smax, 32));
+      const float mold = mrow[qb];
+      const float mnew = fmaxf(mold, smax);
+      float rs = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float s = P[kb][qb][r];
+          const float p = (s == -INFINITY) ? 0.0f : sas_y(mnew - s, lut);
+          P[kb][qb][r] = p;
+          rs += p;
+          pmax = fmaxf(pmax, p);
+        }
+      alpha[qb] = (mold == -INFINITY) ? 0.0f : sas_y(mnew - mold, lut);
+      lhalf[qb] = alpha[qb] * lhalf[qb] + rs;
+      mrow[qb] = mnew;
+    }
+    pmax = wave_max(pmax);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) O[cb][qb][r] *= alpha[qb];
+    if (pmax > 0.0f) {
+      // ---- Q(P~) with scale pmax/119 over the 64x64 tile -------------
+      const float inv = kQmax / pmax;
+      const float spv = (pmax / kQmax) * svp[j];
+      v4i pop[2][2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          int w[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            w[u] = pack4(rne_mul(P[kb][qb][4 * u], inv), rne_mul(P[kb][qb][4 * u + 1], inv),
+                         rne_mul(P[kb][qb][4 * u + 2], inv), rne_mul(P[kb][qb][4 * u + 3], inv));
+          pop[kb][qb] = v4i{w[0], w[1], w[2], w[3]};
+        }
+      // ---- O^T += s_P s_V V_j^T Q(P~)^T ---------------------------------
+      const int8_t* vb = vbase + (long)j * 8192;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        v4i vop[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+          vop[kb] = *reinterpret_cast<const v4i*>(vb + (32 * cb + n) * 64 + 32 * kb + 16 * hf);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          v16i acc = {};
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb) acc = mfma32x32x32(vop[kb], pop[kb][qb], acc);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) O[cb][qb][r] = __builtin_fmaf(spv, (float)acc[r], O[cb][qb][r]);
+        }
+      }
+    }
+  }
+
+  // ---- epilogue: O / l (fp16), L = m + ln l ----------------------------
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int qrow = 64 * i + 32 * qb + n;
+    const float l = lhalf[qb] + __shfl_xor(lhalf[qb], 32);
+    if (qrow >= N) continue;
+    const float rl = 1.0f / l;
+    uint2* orow = a.o + (((long)b * a.Hq + h) * N + qrow) * 32;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f16x4_t hv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][qb][4 * g + e] / l);
+        orow[(32 * cb + 8 * g + 4 * hf) / 4] = __builtin_bit_cast(uint2, hv);
+      }
+    (void)rl;
+    if (a.lse && hf == 0) a.lse[((long)b * a.Hq + h) * N + qrow] = mrow[qb] + logf(l);
+  }
+}
+
+hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
+  const int total = a.B * a.Hq * a.nb;
+  hipLaunchKernelGGL(k_attn_prefill, dim3(total), dim3(64), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace turbo

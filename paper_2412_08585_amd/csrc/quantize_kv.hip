@@ -1,0 +1,236 @@
+// FlashQ for K and V on gfx950: step 1 (symmetric int8 per 64-token block,
+// eq. step1bpq) and step 2 (asymmetric int4/int2 per 64-token channel group,
+// eq. step2bpq) with the cache writes of Algorithm 1.
+//
+// One workgroup of 256 threads handles one (sequence b, KV head h, 64-token
+// block j) for both K and V.  The int8 block is staged token-major in LDS;
+// step 2 then works channel by channel out of LDS.
+#include "turbo_common.h"
+
+namespace turbo {
+
+constexpr int kQkvThreads = 256;
+constexpr int kTileStride = 136;  // LDS row stride (bytes) of the int8 tile
+
+struct QuantArgs {
+  const uint4* k;  // fp16 [B][Hkv][N][128]
+  const uint4* v;
+  int Hkv, N, nb;
+  int8_t* k8;      // [B][Hkv][nb*64][128]
+  int8_t* v8;      // [B][Hkv][nb][128][64]
+  float* sk;       // [B][Hkv][nb]
+  float* sv;
+  // cache (pages == nullptr: no step 2)
+  uint8_t* pages;
+  int8_t* gmeta;
+  float* gscale;
+  long num_pages, num_slots;
+  int page_bytes;
+  unsigned long long int2_mask;  // bit h set: KV head h stored with 2 bits
+  const int* block_table;        // [B][4*max_groups]
+  const int* group_table;        // [B][max_groups]
+  int max_groups;
+};
+
+// Block amax over the 256 threads (each passes its own max).
+__device__ __forceinline__ float block_max(float v, float* red) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  return r;
+}
+
+// Step 1 for one 64-token block of one tensor.  Thread (ts = tid>>4,
+// cg = tid&15) holds tokens ts + 16*tk (tk = 0..3) x channels 8cg..8cg+7.
+// Writes the int8 tile into LDS (token-major) and returns the block scale.
+__device__ float quant_block(const uint4* __restrict__ x, int nr, int8_t* tile, float* red,
+                             int8_t* __restrict__ out_tokmajor) {
+  const int tid = threadIdx.x, ts = tid >> 4, cg = tid & 15;
+  float f[4][8];
+  float amax = 0.0f;
+#pragma unroll
+  for (int tk = 0; tk < 4; ++tk) {
+    const int t = ts + 16 * tk;
+    uint4 raw = make_uint4(0, 0, 0, 0);
+    if (t < nr) raw = x[t * 16 + cg];
+    f16x8_t h = __builtin_bit_cast(f16x8_t, raw);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      f[tk][e] = (float)h[e];
+      amax = fmaxf(amax, fabsf(f[tk][e]));
+    }
+  }
+  amax = block_max(amax, red);
+  float s = 0.0f, inv = 0.0f;
+  if (amax > 0.0f) {
+    s = amax / kQmax;
+    inv = kQmax / amax;
+  }
+#pragma unroll
+  for (int tk = 0; tk < 4; ++tk) {
+    const int t = ts + 16 * tk;
+    int q[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q[e] = min(119, max(-119, rne_mul(f[tk][e], inv)));
+    uint2 packed = make_uint2(pack4(q[0], q[1], q[2], q[3]), pack4(q[4], q[5], q[6], q[7]));
+    *reinterpret_cast<uint2*>(tile + t * kTileStride + 8 * cg) = packed;
+    if (out_tokmajor) *reinterpret_cast<uint2*>(out_tokmajor + t * 128 + 8 * cg) = packed;
+  }
+  return s;
+}
+
+// Step 2 for one channel group: thread (c = tid>>1, hh = tid&1) covers
+// channel c, tokens 32hh..32hh+31 of the LDS tile.  Returns the codes of its
+// 32 tokens in code[] and writes s/z to meta (hh == 0 threads).
+__device__ void step2_channel(const int8_t* tile, int bits, int8_t* meta_s, int8_t* meta_z,
+                              int* code) {
+  const int tid = threadIdx.x, c = tid >> 1, hh = tid & 1;
+  int q[32];
+  int mn = 127, mx = -128;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    q[i] = tile[(32 * hh + i) * kTileStride + c];
+    mn = min(mn, q[i]);
+    mx = max(mx, q[i]);
+  }
+  mn = min(mn, __shfl_xor(mn, 1));
+  mx = max(mx, __shfl_xor(mx, 1));
+  const int levels = (1 << bits) - 1;
+  const int s = max(1, (mx - mn + levels - 1) / levels);
+  // floor(num / (2s)) for num <= 2*238 + 80 as (num * M) >> 20 with
+  // M = 2^20 / (2s) + 1 (exact on that whole range).
+  const int M = (1 << 20) / (2 * s) + 1;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) code[i] = ((2 * (q[i] - mn) + s) * M) >> 20;
+  if (hh == 0) {
+    meta_s[c] = (int8_t)s;
+    meta_z[c] = (int8_t)mn;
+  }
+}
+
+__global__ __launch_bounds__(kQkvThreads) void k_quantize_kv(QuantArgs a) {
+  __shared__ int8_t tile[64 * kTileStride];
+  __shared__ uint8_t ctile[64 * kTileStride];  // K codes, token-major
+  __shared__ float red[4];
+
+  const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const long unit = (long)b * a.Hkv + h;
+  const int r0 = j * 64;
+  const int nr = min(64, a.N - r0);
+  const long xoff = (unit * a.N + r0) * 16;  // in uint4 (8 halves)
+
+  // cache destination of this group (full groups with valid table entries)
+  bool do_cache = a.pages != nullptr && nr == 64;
+  long page[4] = {0, 0, 0, 0};
+  long slot = 0;
+  if (do_cache) {
+    const int* bt = a.block_table + (long)b * 4 * a.max_groups + 4 * j;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      page[p] = bt[p];
+      do_cache = do_cache && page[p] >= 0 && page[p] < a.num_pages;
+    }
+    slot = a.group_table[(long)b * a.max_groups + j];
+    do_cache = do_cache && slot >= 0 && slot < a.num_slots;
+  }
+  const int bits = ((a.int2_mask >> h) & 1ull) ? 2 : 4;
+  const int head_off = 512 * (4 * h - 2 * __popcll(a.int2_mask & ((1ull << h) - 1ull)));
+  int8_t* meta = a.gmeta + (slot * a.Hkv + h) * 512;
+
+  // ---- K ----
+  float s = quant_block(a.k + xoff, nr, tile, red, a.k8 + (unit * a.nb + j) * 8192);
+  if (tid == 0) a.sk[unit * a.nb + j] = s;
+  __syncthreads();
+  if (do_cache) {
+    int code[32];
+    step2_channel(tile, bits, meta, meta + 128, code);
+    if (tid == 0) a.gscale[(slot * a.Hkv + h) * 2 + 0] = s;
+    const int c = tid >> 1, hh = tid & 1;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) ctile[(32 * hh + i) * kTileStride + c] = (uint8_t)code[i];
+    __syncthreads();
+    // token-major packing: thread (t = tid>>2, chunk = tid&3) packs 32 channels
+    const int t = tid >> 2, ch = tid & 3;
+    const uint8_t* src = ctile + t * kTileStride + 32 * ch;
+    uint8_t* dst = a.pages + page[t >> 4] * a.page_bytes + head_off + (t & 15) * 16 * bits;
+    if (bits == 4) {
+      unsigned w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        unsigned x = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x |= (unsigned)src[8 * i + e] << (4 * e);
+        w[i] = x;
+      }
+      *reinterpret_cast<uint4*>(dst + 16 * ch) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+      unsigned w[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        unsigned x = 0;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) x |= (unsigned)src[16 * i + e] << (2 * e);
+        w[i] = x;
+      }
+      *reinterpret_cast<uint2*>(dst + 8 * ch) = make_uint2(w[0], w[1]);
+    }
+  }
+  __syncthreads();
+
+  // ---- V ----
+  s = quant_block(a.v + xoff, nr, tile, red, nullptr);
+  if (tid == 0) a.sv[unit * a.nb + j] = s;
+  __syncthreads();
+  {
+    // channel-major int8 block: thread (c = tid>>1, hh) writes 32 tokens
+    const int c = tid >> 1, hh = tid & 1;
+    unsigned w[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int t = 32 * hh + 4 * i;
+      w[i] = pack4(tile[t * kTileStride + c], tile[(t + 1) * kTileStride + c],
+                   tile[(t + 2) * kTileStride + c], tile[(t + 3) * kTileStride + c]);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(a.v8 + (unit * a.nb + j) * 8192 + c * 64 + 32 * hh);
+    dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+    dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+  }
+  if (do_cache) {
+    int code[32];
+    step2_channel(tile, bits, meta + 256, meta + 384, code);
+    if (tid == 0) a.gscale[(slot * a.Hkv + h) * 2 + 1] = s;
+    // channel-major packing: tokens 32hh..32hh+31 are pages 2hh, 2hh+1
+    const int c = tid >> 1, hh = tid & 1;
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) {
+      uint8_t* dst = a.pages + page[2 * hh + pp] * a.page_bytes + head_off + 256 * bits +
+                     c * 2 * bits;
+      if (bits == 4) {
+        unsigned lo = 0, hi = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          lo |= (unsigned)code[16 * pp + e] << (4 * e);
+          hi |= (unsigned)code[16 * pp + 8 + e] << (4 * e);
+        }
+        *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+      } else {
+        unsigned x = 0;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) x |= (unsigned)code[16 * pp + e] << (2 * e);
+        *reinterpret_cast<unsigned*>(dst) = x;
+      }
+    }
+  }
+}
+
+hipError_t launch_quantize_kv(const QuantArgs& a, int B, hipStream_t stream) {
+  dim3 grid(a.nb, a.Hkv, B);
+  hipLaunchKernelGGL(k_quantize_kv, grid, dim3(kQkvThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace turbo

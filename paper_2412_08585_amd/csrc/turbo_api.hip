@@ -1,0 +1,214 @@
+// C ABI of the gfx950 TurboAttention hot path: argument checks on the host,
+// then the kernel launches on the caller's stream.  No allocation, no
+// synchronization, no exception crosses the boundary.
+#include <atomic>
+#include <cstring>
+
+#include "turbo_common.h"
+
+// The library is one translation unit: the kernel sources (each with its
+// argument struct and launcher) are included here.
+#include "quantize_kv.hip"
+#include "attn_prefill.hip"
+#include "attn_decode.hip"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+// 0 unknown, 1 gfx950, -1 other; written once per device (benign race: every
+// writer stores the same value).
+std::atomic<int> g_arch_ok[kMaxDevices];
+
+int check_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return TURBO_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return TURBO_ERR_UNSUPPORTED;
+  int st = g_arch_ok[dev].load(std::memory_order_relaxed);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return TURBO_ERR_HIP;
+    st = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    g_arch_ok[dev].store(st, std::memory_order_relaxed);
+  }
+  return st == 1 ? TURBO_OK : TURBO_ERR_UNSUPPORTED;
+}
+
+int check_cache(const turbo_kv_cache* c, int Hkv, unsigned long long* int2_mask,
+                int* page_bytes) {
+  if (!c || !c->pages || !c->group_meta || !c->group_scale) return TURBO_ERR_INVALID_ARG;
+  if (c->num_kv_heads != Hkv || c->head_dim != TURBO_HEAD_DIM) return TURBO_ERR_INVALID_ARG;
+  if (c->num_pages < 1 || c->num_group_slots < 1) return TURBO_ERR_INVALID_ARG;
+  unsigned long long mask = 0;
+  for (int h = 0; h < Hkv; ++h) {
+    if (c->head_bits[h] == 2)
+      mask |= 1ull << h;
+    else if (c->head_bits[h] != 4)
+      return TURBO_ERR_INVALID_ARG;
+  }
+  *int2_mask = mask;
+  *page_bytes = (int)turbo_page_bytes(c->head_bits, Hkv);
+  return TURBO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int turbo_abi_version(void) { return TURBO_ABI_VERSION; }
+
+const char* turbo_strerror(int status) {
+  switch (status) {
+    case TURBO_OK: return "success";
+    case TURBO_ERR_INVALID_ARG: return "invalid argument";
+    case TURBO_ERR_UNSUPPORTED: return "unsupported device (gfx950 required)";
+    case TURBO_ERR_WORKSPACE_TOO_SMALL: return "decode workspace too small";
+    case TURBO_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t turbo_page_bytes(const uint8_t* head_bits, int num_kv_heads) {
+  if (!head_bits || num_kv_heads < 1 || num_kv_heads > TURBO_MAX_KV_HEADS) return 0;
+  size_t total = 0;
+  for (int h = 0; h < num_kv_heads; ++h) {
+    if (head_bits[h] != 2 && head_bits[h] != 4) return 0;
+    total += 512u * head_bits[h];
+  }
+  return total;
+}
+
+int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d, int8_t* k8,
+                      int8_t* v8, float* s_k, float* s_v, const turbo_kv_cache* cache,
+                      const int32_t* block_table, const int32_t* group_table,
+                      int max_groups_per_seq, hipStream_t stream) {
+  if (B < 0 || N < 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || d != TURBO_HEAD_DIM)
+    return TURBO_ERR_INVALID_ARG;
+  if (B == 0 || N == 0) return TURBO_OK;
+  if (!k || !v || !k8 || !v8 || !s_k || !s_v) return TURBO_ERR_INVALID_ARG;
+  turbo::QuantArgs a{};
+  if (cache) {
+    if (!block_table || !group_table || max_groups_per_seq < N / TURBO_BLOCK)
+      return TURBO_ERR_INVALID_ARG;
+    int st = check_cache(cache, Hkv, &a.int2_mask, &a.page_bytes);
+    if (st != TURBO_OK) return st;
+    a.pages = cache->pages;
+    a.gmeta = cache->group_meta;
+    a.gscale = cache->group_scale;
+    a.num_pages = cache->num_pages;
+    a.num_slots = cache->num_group_slots;
+    a.block_table = block_table;
+    a.group_table = group_table;
+    a.max_groups = max_groups_per_seq;
+  }
+  int st = check_device();
+  if (st != TURBO_OK) return st;
+  a.k = static_cast<const uint4*>(k);
+  a.v = static_cast<const uint4*>(v);
+  a.Hkv = Hkv;
+  a.N = N;
+  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.k8 = k8;
+  a.v8 = v8;
+  a.sk = s_k;
+  a.sv = s_v;
+  return turbo::launch_quantize_kv(a, B, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
+                       const float* s_v, int B, int Hq, int Hkv, int N, int d, float sm_scale,
+                       int causal, void* o, float* lse, hipStream_t stream) {
+  if (B < 0 || N < 0 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || Hq / Hkv > TURBO_MAX_GQA ||
+      d != TURBO_HEAD_DIM || !(sm_scale > 0.0f) || sm_scale > 3.0e38f)
+    return TURBO_ERR_INVALID_ARG;
+  if (B == 0 || N == 0) return TURBO_OK;
+  if (!q || !k8 || !v8 || !s_k || !s_v || !o) return TURBO_ERR_INVALID_ARG;
+  const long tiles = (long)B * Hq * ((N + TURBO_BLOCK - 1) / TURBO_BLOCK);
+  if (tiles > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
+  int st = check_device();
+  if (st != TURBO_OK) return st;
+  turbo::PrefillArgs a{};
+  a.q = static_cast<const uint4*>(q);
+  a.k8 = k8;
+  a.v8 = v8;
+  a.sk = s_k;
+  a.sv = s_v;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.N = N;
+  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.sm_scale = sm_scale;
+  a.causal = causal ? 1 : 0;
+  a.o = static_cast<uint2*>(o);
+  a.lse = lse;
+  return turbo::launch_attn_prefill(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {
+  if (B < 1 || Hkv < 1 || max_groups_per_seq < 1) return 1;
+  // aim at >= 4096 waves (16 per CU on 256 CUs) of streaming work
+  const long units = (long)B * Hkv;
+  long nsplit = (4096 + units - 1) / units;
+  if (nsplit > max_groups_per_seq) nsplit = max_groups_per_seq;
+  if (nsplit < 1) nsplit = 1;
+  return (int)((max_groups_per_seq + nsplit - 1) / nsplit);
+}
+
+size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
+                                    int kv_split_groups) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || max_groups_per_seq < 1 || kv_split_groups < 0) return 0;
+  const int split = kv_split_groups ? kv_split_groups
+                                    : turbo_decode_auto_split(B, Hkv, max_groups_per_seq);
+  const long nsplit = (max_groups_per_seq + split - 1) / split;
+  if (nsplit <= 1) return 0;
+  return (size_t)B * Hq * nsplit * turbo::kWsStride * sizeof(float);
+}
+
+int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+                      const int32_t* block_table, const int32_t* group_table,
+                      int max_groups_per_seq, int B, int Hq, float sm_scale, int kv_split_groups,
+                      void* workspace, size_t workspace_bytes, void* o, float* lse,
+                      hipStream_t stream) {
+  if (B < 0 || Hq < 1 || max_groups_per_seq < 1 || kv_split_groups < 0 || !cache ||
+      !(sm_scale > 0.0f) || sm_scale > 3.0e38f)
+    return TURBO_ERR_INVALID_ARG;
+  const int Hkv = cache->num_kv_heads;
+  if (Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || Hq % Hkv != 0 || Hq / Hkv > TURBO_MAX_GQA)
+    return TURBO_ERR_INVALID_ARG;
+  if (B == 0) return TURBO_OK;
+  if (!q || !seq_lens || !block_table || !group_table || !o) return TURBO_ERR_INVALID_ARG;
+  turbo::DecodeArgs a{};
+  int st = check_cache(cache, Hkv, &a.int2_mask, &a.page_bytes);
+  if (st != TURBO_OK) return st;
+  const int split = kv_split_groups ? kv_split_groups
+                                    : turbo_decode_auto_split(B, Hkv, max_groups_per_seq);
+  const long nsplit = (max_groups_per_seq + split - 1) / split;
+  if ((long)B * Hkv * nsplit > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
+  const size_t need = turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups_per_seq, split);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return TURBO_ERR_WORKSPACE_TOO_SMALL;
+  st = check_device();
+  if (st != TURBO_OK) return st;
+  a.q = static_cast<const uint4*>(q);
+  a.pages = cache->pages;
+  a.gmeta = cache->group_meta;
+  a.gscale = cache->group_scale;
+  a.num_pages = cache->num_pages;
+  a.num_slots = cache->num_group_slots;
+  a.seq_lens = seq_lens;
+  a.block_table = block_table;
+  a.group_table = group_table;
+  a.max_groups = max_groups_per_seq;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.G = Hq / Hkv;
+  a.sm_scale = sm_scale;
+  a.split = split;
+  a.nsplit = (int)nsplit;
+  a.ws = static_cast<float*>(workspace);
+  a.o = static_cast<uint2*>(o);
+  a.lse = lse;
+  return turbo::launch_attn_decode(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,108 @@
+// Device-side building blocks of the gfx950 TurboAttention kernels.
+//
+// Nothing here is shared with the CPU oracle; the paper's constants are typed
+// again below as exact binary32 literals.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "turbo_attn.h"
+
+namespace turbo {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef unsigned short u16;
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+
+// Symmetric int8 divisor of Algorithms 1 and 2.
+constexpr float kQmax = 119.0f;
+// 1.5 * 2^23: adding it to a value of magnitude < 2^22 leaves the value
+// rounded to an integer (ties to even) in the low mantissa bits.
+constexpr float kMagic = 12582912.0f;
+constexpr int kMagicBits = 0x4B400000;
+
+// SAS (Sec. 4): e^{-y} ~ LUT[floor y] * POLY(y - floor y) for y = m - s in
+// [0, 6]; zero for y > 6 (n_r = -6, Sec. 5.2).  LUT[k] = e^{-k} rounded to
+// binary32; POLY coefficients as printed in Sec. 4, rounded to binary32.
+constexpr float kLut[8] = {0x1p+0f,          0x1.78b564p-2f, 0x1.152aaap-3f, 0x1.97db0cp-5f,
+                           0x1.2c155cp-6f,   0x1.b993fep-8f, 0x1.44e520p-9f, 0.0f};
+constexpr float kC3 = -0x1.a3d70ap-4f;  // -0.1025
+constexpr float kC2 = 0x1.d9b3d0p-2f;   //  0.4626
+constexpr float kC1 = -0x1.fc01a4p-1f;  // -0.9922
+constexpr float kC0 = 0x1.ffcb92p-1f;   //  0.9996
+constexpr float kNr = 6.0f;
+
+// Nearest integer (ties to even) of the exact product a*b, |a*b| < 2^22.
+__device__ __forceinline__ int rne_mul(float a, float b) {
+  return __float_as_int(__builtin_fmaf(a, b, kMagic)) - kMagicBits;
+}
+
+__device__ __forceinline__ float poly(float f) {
+  return __builtin_fmaf(__builtin_fmaf(__builtin_fmaf(kC3, f, kC2), f, kC1), f, kC0);
+}
+
+// SAS of x = -y, y >= 0, with the table in LDS (8 floats, entry 7 = 0).
+__device__ __forceinline__ float sas_y(float y, const float* lut) {
+  const float k = __builtin_floorf(y);
+  const float f = y - k;  // exact
+  const int idx = (y > kNr) ? 7 : (int)k;
+  return lut[idx] * poly(f);
+}
+
+// SAS with the table in registers (used where LDS is not set up).
+__device__ __forceinline__ float sas_y_reg(float y) {
+  const float k = __builtin_floorf(y);
+  const float f = y - k;
+  float l = 0.0f;
+  const int idx = (y > kNr) ? 7 : (int)k;
+#pragma unroll
+  for (int i = 0; i < 7; ++i) l = (idx == i) ? kLut[i] : l;
+  return l * poly(f);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
+  return v;
+}
+
+__device__ __forceinline__ int wave_max_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = max(v, __shfl_xor(v, m));
+  return v;
+}
+
+__device__ __forceinline__ int wave_min_i(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = min(v, __shfl_xor(v, m));
+  return v;
+}
+
+__device__ __forceinline__ v16i mfma32x32x32(v4i a, v4i b, v16i c) {
+  return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ v4i mfma16x16x64(v4i a, v4i b, v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+// Pack the low bytes of four ints (values -128..255) into one dword.
+__device__ __forceinline__ int pack4(int a, int b, int c, int d) {
+  return (a & 0xff) | ((b & 0xff) << 8) | ((c & 0xff) << 16) | ((int)((unsigned)d << 24));
+}
+
+// XCD-aware remap of a 1-D workgroup id: the hardware hands consecutive
+// workgroup ids to the 8 XCDs round-robin; this returns a logical index such
+// that each XCD works on a contiguous range of logical indices (so logically
+// neighbouring tiles share that XCD's L2).
+__device__ __forceinline__ int xcd_remap(int wg, int total) {
+  constexpr int kXcd = 8;
+  const int per = total / kXcd, rem = total % kXcd;
+  const int x = wg % kXcd, i = wg / kXcd;
+  return x * per + min(x, rem) + i;
+}
+
+}  // namespace turbo

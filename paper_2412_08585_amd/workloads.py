@@ -107,6 +107,20 @@ def unit_qkv(w: Workload, b: int, h: int, device="cpu", N: Optional[int] = None,
     return q.half(), k.half(), v.half()
 
 
+def unit_kv(w: Workload, b: int, h: int, device="cpu", N: Optional[int] = None,
+            outliers: bool = True):
+    """fp16 (k [N][128], v [N][128]) of sequence b, KV head h: the same draws
+    as unit_qkv (K and V come before Q in the stream)."""
+    N = w.N if N is None else N
+    g = _gen(device, seed_of(w.wid, b, h, 0))
+    ch = torch.randperm(HEAD_DIM, generator=g, device=device)[:N_OUTLIER]
+    k = torch.randn(N, HEAD_DIM, generator=g, device=device, dtype=torch.float32)
+    v = torch.randn(N, HEAD_DIM, generator=g, device=device, dtype=torch.float32)
+    if outliers:
+        k[:, ch] *= OUTLIER_GAIN
+    return k.half(), v.half()
+
+
 def prefill_inputs(w: Workload, device="cpu", N: Optional[int] = None, B: Optional[int] = None):
     """fp16 Q [B][Hq][N][128], K, V [B][Hkv][N][128] built unit by unit."""
     N = w.N if N is None else N

@@ -1,0 +1,335 @@
+"""GPU parity: the gfx950 kernels (called through the C ABI) against the CPU
+oracle on the same seeded inputs.
+
+Bar (fixed by the method's integer steps and the fp16 output):
+  * bit-exact: int8 K/V codes, block scales (bits), int4/int2 codes, integer
+    step-2 scales and zero points, group scales;
+  * fp16 O within 1e-3 of the row's largest |O| (the GPU's fp32 l and O sums
+    round in another order than the oracle's double ones; every integer of
+    the path, including Q(P~), is decided by the same binary32 operations);
+  * L = m + ln l within 1e-4 absolute.
+Full-size workloads run on the GPU in full, in the launch configuration the
+benchmark times, and are compared on sampled (sequence, KV head) units.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from tests import cache_layout
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 1e-3
+LSE_TOL = 1e-4
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def ta(dev):
+    import paper_2412_08585_amd as ta
+    ta.lib()
+    return ta
+
+
+def _cmp_o(got: torch.Tensor, want: np.ndarray, what: str):
+    g = got.float().cpu().numpy()
+    rowmax = np.maximum(np.abs(want).max(axis=-1, keepdims=True), 1e-30)
+    err = np.abs(g - want) / rowmax
+    worst = float(np.nanmax(err))
+    assert np.all(np.isfinite(g)), what
+    assert worst < O_TOL, f"{what}: max rel-to-row-max error {worst:.3e}"
+    return worst
+
+
+def _cmp_lse(got: torch.Tensor, want: np.ndarray, what: str):
+    g = got.cpu().numpy().astype(np.float64)
+    fin = np.isfinite(want)
+    assert np.array_equal(np.isfinite(g), fin), what
+    if fin.any():
+        worst = float(np.max(np.abs(g[fin] - want[fin])))
+        assert worst < LSE_TOL, f"{what}: lse error {worst:.3e}"
+
+
+def _tables(B, mg, seed):
+    rng = np.random.default_rng(seed)
+    bt = rng.permutation(B * 4 * mg).astype(np.int32).reshape(B, 4 * mg)
+    gt = rng.permutation(B * mg).astype(np.int32).reshape(B, mg)
+    return bt, gt
+
+
+def _quantize(ta, dev, k, v, bits, seed=0):
+    B, H, N, _ = k.shape
+    mg = max(1, N // 64)
+    bt, gt = _tables(B, mg, seed)
+    cache = ta.PagedKVCache(bt.size, gt.size, bits, dev)
+    btd, gtd = torch.from_numpy(bt).to(dev), torch.from_numpy(gt).to(dev)
+    outs = ta.turbo_quantize_kv(k.to(dev), v.to(dev), cache, btd, gtd)
+    torch.cuda.synchronize()
+    return outs, cache, bt, gt, btd, gtd
+
+
+def _rand(shape, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(*shape, generator=g) * scale).half()
+
+
+QUANT_CASES = [
+    # B, Hkv, N, bits
+    (1, 4, 512, [4, 4, 4, 4]),
+    (2, 3, 64 * 5 + 17, [4, 2, 4]),
+    (1, 2, 64, [2, 2]),
+    (1, 1, 17, [4]),
+    (2, 2, 64 * 3, [2, 4]),
+]
+
+
+@pytest.mark.parametrize("B,H,N,bits", QUANT_CASES)
+def test_quantize_kv_bit_exact(orc, ta, dev, B, H, N, bits):
+    _log(f"quantize_kv B={B} H={H} N={N} bits={bits}")
+    k = _rand((B, H, N, 128), 100 + N)
+    v = _rand((B, H, N, 128), 200 + N)
+    k[..., 7] *= 10
+    if N >= 128:
+        k[:, 0, 64:128] = 0  # an all-zero block: s = 0, codes 0
+    (k8, v8, sk, sv), cache, bt, gt, _, _ = _quantize(ta, dev, k, v, bits)
+    ref = orc.quantize_kv(k, v, bits)
+    nb = (N + 63) // 64
+    k8 = k8.cpu().numpy()
+    v8 = v8.cpu().numpy().transpose(0, 1, 2, 4, 3).reshape(B, H, nb * 64, 128)
+    assert np.array_equal(k8[:, :, :N], ref["k8"])
+    assert np.array_equal(v8[:, :, :N], ref["v8"])
+    assert not k8[:, :, N:].any() and not v8[:, :, N:].any()
+    assert np.array_equal(sk.cpu().numpy().view(np.int32), ref["sk"].view(np.int32))
+    assert np.array_equal(sv.cpu().numpy().view(np.int32), ref["sv"].view(np.int32))
+    ng = N // 64
+    pages = cache.pages.cpu().numpy()
+    gmeta = cache.group_meta.cpu().numpy()
+    gscale = cache.group_scale.cpu().numpy()
+    for b in range(B):
+        for h in range(H):
+            if ng == 0:
+                continue
+            u = cache_layout.read_unit(pages, gmeta, gscale, bits, bt, gt, b, h, ng)
+            for key in ("kc", "vc", "ks", "kz", "vs", "vz"):
+                assert np.array_equal(u[key], ref[key][b, h]), (b, h, key)
+            assert np.array_equal(u["sk"].view(np.int32), ref["sk"][b, h, :ng].view(np.int32))
+            assert np.array_equal(u["sv"].view(np.int32), ref["sv"][b, h, :ng].view(np.int32))
+
+
+PREFILL_CASES = [
+    # B, Hq, Hkv, N, causal
+    (1, 4, 4, 512, True),
+    (2, 8, 2, 64 * 3 + 40, True),
+    (1, 2, 1, 130, False),
+    (1, 2, 2, 1, True),
+    (1, 2, 2, 64, True),
+    (1, 16, 1, 200, True),
+    (1, 3, 3, 64 * 2 + 63, False),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,N,causal", PREFILL_CASES)
+def test_prefill_parity(orc, ta, dev, B, Hq, Hkv, N, causal):
+    _log(f"prefill B={B} Hq={Hq} Hkv={Hkv} N={N} causal={causal}")
+    q = _rand((B, Hq, N, 128), 300 + N)
+    k = _rand((B, Hkv, N, 128), 400 + N)
+    v = _rand((B, Hkv, N, 128), 500 + N)
+    k[..., 3] *= 10
+    (k8, v8, sk, sv) = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
+    o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, 1 / np.sqrt(128), causal,
+                                   return_lse=True)
+    torch.cuda.synchronize()
+    ro, rl = orc.attn_prefill(q, k, v, 1 / np.sqrt(128), causal)
+    err = _cmp_o(o, ro, "prefill O")
+    _cmp_lse(lse, rl, "prefill lse")
+    ex, _ = orc.attn_exact(q, k, v, float(np.float32(1 / np.sqrt(128))), causal)
+    g = o.float().cpu().numpy()
+    _log(f"  vs oracle {err:.2e}; rel-L2 vs exact fp64: gpu "
+         f"{np.linalg.norm(g - ex) / np.linalg.norm(ex):.3e} oracle "
+         f"{np.linalg.norm(ro - ex) / np.linalg.norm(ex):.3e}")
+
+
+def test_prefill_zero_query_block(orc, ta, dev):
+    """An all-zero query block has s_Q = 0: every score is 0 (closed form)."""
+    N = 64 * 3
+    q = _rand((1, 2, N, 128), 1)
+    q[:, :, 64:128] = 0
+    k, v = _rand((1, 2, N, 128), 2), _rand((1, 2, N, 128), 3)
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
+    o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, 1 / np.sqrt(128), True,
+                                   return_lse=True)
+    ro, rl = orc.attn_prefill(q, k, v, 1 / np.sqrt(128), True)
+    _cmp_o(o, ro, "zero block O")
+    _cmp_lse(lse, rl, "zero block lse")
+
+
+DECODE_CASES = [
+    # B, Hq, Hkv, Nc, bits, seq_lens, split
+    (3, 8, 2, 64 * 6, [4, 2], [384, 200, 0], 2),
+    (3, 8, 2, 64 * 6, [4, 2], [384, 200, 63], 0),
+    (2, 4, 4, 64 * 4, [2, 4, 4, 2], [256, 256], 1),
+    (1, 16, 1, 64 * 8, [4], [512], 3),
+    (2, 2, 1, 64 * 5, [2], [320, 128], 100),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,Nc,bits,sl,split", DECODE_CASES)
+def test_decode_parity(orc, ta, dev, B, Hq, Hkv, Nc, bits, sl, split):
+    _log(f"decode B={B} Hq={Hq} Hkv={Hkv} Nc={Nc} bits={bits} seq={sl} split={split}")
+    k = _rand((B, Hkv, Nc, 128), 600 + Nc)
+    v = _rand((B, Hkv, Nc, 128), 700 + Nc)
+    k[..., 11] *= 10
+    q = _rand((B, Hq, 128), 800 + Nc)
+    _, cache, bt, gt, btd, gtd = _quantize(ta, dev, k, v, bits, seed=Nc)
+    sld = torch.tensor(sl, dtype=torch.int32, device=dev)
+    o, lse = ta.turbo_attn_decode(q.to(dev), cache, sld, btd, gtd, 1 / np.sqrt(128), split,
+                                  return_lse=True)
+    torch.cuda.synchronize()
+    ref = orc.quantize_kv(k, v, bits)
+    used = ta.decode_split(B, Hkv, Nc // 64, split)
+    ro, rl = orc.attn_decode(q, ref, sl, 1 / np.sqrt(128), split=used)
+    _cmp_o(o, ro, "decode O")
+    _cmp_lse(lse, rl, "decode lse")
+
+
+def test_decode_rows_with_empty_groups(orc, ta, dev):
+    """Rows of one wave whose later groups all fall more than 6 below their
+    running maximum (P~ = 0 for a whole group, P scale 0) next to rows for
+    which they do not: the quantized P of the former must add nothing."""
+    B, Hq, Hkv, Nc = 1, 4, 1, 64 * 4
+    k = _rand((B, Hkv, Nc, 128), 901, 0.1)
+    k[:, :, :64] = 3.0          # group 0 aligned with +1 queries
+    v = _rand((B, Hkv, Nc, 128), 902)
+    q = torch.ones(B, Hq, 128, dtype=torch.float16)
+    q[:, 1] = -1.0              # row 1: group 0 far below the others
+    q[:, 2] = _rand((Hq, 128), 903)[2]
+    _, cache, bt, gt, btd, gtd = _quantize(ta, dev, k, v, [4], seed=5)
+    sld = torch.tensor([Nc], dtype=torch.int32, device=dev)
+    ref = orc.quantize_kv(k, v, [4])
+    for split in (1, 2):
+        o, lse = ta.turbo_attn_decode(q.to(dev), cache, sld, btd, gtd, 1 / np.sqrt(128), split,
+                                      return_lse=True)
+        torch.cuda.synchronize()
+        ro, rl = orc.attn_decode(q, ref, [Nc], 1 / np.sqrt(128), split=split)
+        _cmp_o(o, ro, f"decode empty groups split={split}")
+        _cmp_lse(lse, rl, "decode empty groups lse")
+
+
+def test_prefill_tiles_with_empty_p(orc, ta, dev):
+    """Key blocks whose every score lies more than 6 below the running
+    maximum: the tile's P scale is 0 and its PV is skipped."""
+    N = 64 * 4
+    q = torch.ones(1, 2, N, 128, dtype=torch.float16)
+    q[:, 1] = _rand((N, 128), 911)
+    k = _rand((1, 1, N, 128), 912, 0.1)
+    k[:, :, :64] = 3.0
+    v = _rand((1, 1, N, 128), 913)
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
+    o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, 1 / np.sqrt(128), True,
+                                   return_lse=True)
+    ro, rl = orc.attn_prefill(q, k, v, 1 / np.sqrt(128), True)
+    _cmp_o(o, ro, "prefill empty tiles O")
+    _cmp_lse(lse, rl, "prefill empty tiles lse")
+
+
+def test_determinism(ta, dev):
+    N = 64 * 4 + 9
+    q, k, v = _rand((2, 4, N, 128), 1), _rand((2, 2, N, 128), 2), _rand((2, 2, N, 128), 3)
+    outs = []
+    for _ in range(2):
+        k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
+        o = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv)
+        outs.append(o.cpu())
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+
+
+# ---- full-size workloads (launch configuration of the benchmark) -----------
+
+def _sample_units(w, n, seed=0):
+    rng = np.random.default_rng(seed)
+    return sorted({(int(rng.integers(w.B)), int(rng.integers(w.Hkv))) for _ in range(n)})
+
+
+@pytest.mark.parametrize("name,qblocks", [("phi3m-prefill-4k", None),
+                                          ("llama3-8b-prefill-16k", (0, 2)),
+                                          ("llama3-8b-prefill-16k", (255, 256))])
+def test_full_size_prefill(orc, ta, dev, name, qblocks):
+    from paper_2412_08585_amd import workloads as W
+    w = W.WORKLOADS[name]
+    _log(f"full-size prefill {name} qblocks={qblocks}")
+    q, k, v = W.prefill_inputs(w, device=dev)
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k, v)
+    o, lse = ta.turbo_attn_prefill(q, k8, v8, sk, sv, w.sm_scale, True, return_lse=True)
+    torch.cuda.synchronize()
+    for (b, h) in _sample_units(w, 2 if qblocks is None else 1, seed=len(name)):
+        qs = q[b:b + 1, h * w.G:(h + 1) * w.G].cpu()
+        ro, rl = orc.attn_prefill(qs, k[b:b + 1, h:h + 1].cpu(), v[b:b + 1, h:h + 1].cpu(),
+                                  w.sm_scale, True, qblocks=qblocks)
+        rows = slice(None) if qblocks is None else slice(64 * qblocks[0], 64 * qblocks[1])
+        _cmp_o(o[b:b + 1, h * w.G:(h + 1) * w.G, rows], ro[:, :, rows], f"{name} O unit {b},{h}")
+        _cmp_lse(lse[b:b + 1, h * w.G:(h + 1) * w.G, rows], rl[:, :, rows], f"{name} lse")
+        _log(f"  unit ({b},{h}) ok")
+    del q, k, v, k8, v8, o
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["phi3m-decode-8k", "long-decode-32k"])
+def test_full_size_decode(orc, ta, dev, name):
+    from paper_2412_08585_amd import workloads as W
+    w = W.WORKLOADS[name]
+    _log(f"full-size decode {name}")
+    bits = W.head_bits(w)
+    bt, gt = W.tables(w)
+    cache = ta.PagedKVCache(bt.size, gt.size, bits, dev)
+    btd, gtd = torch.from_numpy(bt).to(dev), torch.from_numpy(gt).to(dev)
+    chunk = 16
+    units = {}
+    samples = _sample_units(w, 3, seed=7)
+    for b0 in range(0, w.B, chunk):
+        nbat = min(chunk, w.B - b0)
+        k = torch.empty(nbat, w.Hkv, w.N, 128, dtype=torch.float16, device=dev)
+        v = torch.empty_like(k)
+        for bb in range(nbat):
+            for h in range(w.Hkv):
+                k[bb, h], v[bb, h] = W.unit_kv(w, b0 + bb, h, device=dev)
+                if (b0 + bb, h) in samples:
+                    units[b0 + bb, h] = (k[bb, h].cpu(), v[bb, h].cpu())
+        ta.turbo_quantize_kv(k, v, cache, btd[b0:b0 + nbat], gtd[b0:b0 + nbat])
+        del k, v
+    torch.cuda.synchronize()
+    _log("  cache built")
+    q = W.decode_query(w, device=dev)
+    sl = torch.full((w.B,), w.N, dtype=torch.int32, device=dev)
+    o, lse = ta.turbo_attn_decode(q, cache, sl, btd, gtd, w.sm_scale, 0, return_lse=True)
+    torch.cuda.synchronize()
+    split = ta.decode_split(w.B, w.Hkv, w.max_groups, 0)
+    pages = cache.pages.cpu().numpy()
+    gmeta = cache.group_meta.cpu().numpy()
+    gscale = cache.group_scale.cpu().numpy()
+    for (b, h), (ku, vu) in units.items():
+        ref = orc.quantize_kv(ku[None, None], vu[None, None], [int(bits[h])])
+        u = cache_layout.read_unit(pages, gmeta, gscale, bits, bt, gt, b, h, w.max_groups)
+        for key in ("kc", "vc", "ks", "kz", "vs", "vz"):
+            assert np.array_equal(u[key], ref[key][0, 0]), (b, h, key)
+        assert np.array_equal(u["sk"].view(np.int32), ref["sk"][0, 0].view(np.int32))
+        qs = q[b:b + 1, h * w.G:(h + 1) * w.G].cpu()
+        ro, rl = orc.attn_decode(qs, ref, [w.N], w.sm_scale, split=split)
+        _cmp_o(o[b:b + 1, h * w.G:(h + 1) * w.G], ro, f"{name} O unit {b},{h}")
+        _cmp_lse(lse[b:b + 1, h * w.G:(h + 1) * w.G], rl, f"{name} lse unit {b},{h}")
+        _log(f"  unit ({b},{h}) ok")
+    del cache
+    torch.cuda.empty_cache()

@@ -1,0 +1,165 @@
+"""Host-side checks of the C ABI library (no GPU): it loads, exports every
+function declared in include/*.h, rejects bad arguments before any launch,
+and its sizing helpers follow the documented formulas.  Also host checks of
+the integer tricks the kernels rely on and of the cache format reader."""
+import ctypes
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+
+from tests import cache_layout
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def ta():
+    import paper_2412_08585_amd as ta
+    if not os.path.exists(ta.binding.LIB_PATH):
+        from paper_2412_08585_amd import build
+        build.build()
+    return ta
+
+
+def _declared_functions():
+    names = []
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        src = open(h).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names += re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(turbo_\w+)\s*\(", src, flags=re.M)
+    return sorted(set(names))
+
+
+def test_exports_every_declared_function(ta):
+    names = _declared_functions()
+    assert {"turbo_quantize_kv", "turbo_attn_prefill", "turbo_attn_decode"} <= set(names)
+    L = ctypes.CDLL(ta.binding.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_strerror(ta):
+    L = ta.lib()
+    assert L.turbo_abi_version() == 1
+    for st in (0, -1, -2, -3, -4, 7):
+        assert L.turbo_strerror(st)
+
+
+def test_page_bytes(ta):
+    assert ta.page_bytes([4] * 10) == 10 * 2048
+    assert ta.page_bytes([4, 2, 2, 4]) == 2048 * 2 + 1024 * 2
+    assert ta.page_bytes([3]) == 0
+    assert ta.page_bytes([]) == 0
+    assert ta.page_bytes([4] * 65) == 0
+
+
+def test_invalid_arguments_rejected_before_launch(ta):
+    L = ta.lib()
+    P = ctypes.c_void_p
+    dummy = P(16)
+    # d != 128
+    assert L.turbo_quantize_kv(dummy, dummy, 1, 1, 64, 64, dummy, dummy, dummy, dummy, None, None,
+                               None, 0, None) == -1
+    # Hq % Hkv != 0
+    assert L.turbo_attn_prefill(dummy, dummy, dummy, dummy, dummy, 1, 6, 4, 64, 128, 0.1, 1, dummy,
+                                None, None) == -1
+    # GQA ratio above 16
+    assert L.turbo_attn_prefill(dummy, dummy, dummy, dummy, dummy, 1, 34, 2, 64, 128, 0.1, 1, dummy,
+                                None, None) == -1
+    # null output
+    assert L.turbo_attn_prefill(dummy, dummy, dummy, dummy, dummy, 1, 4, 4, 64, 128, 0.1, 1, None,
+                                None, None) == -1
+    # non-positive / NaN scale
+    for sm in (0.0, -1.0, float("nan")):
+        assert L.turbo_attn_prefill(dummy, dummy, dummy, dummy, dummy, 1, 4, 4, 64, 128, sm, 1,
+                                    dummy, None, None) == -1
+    # empty problem is a no-op success (no device touched)
+    assert L.turbo_attn_prefill(None, None, None, None, None, 0, 4, 4, 64, 128, 0.1, 1, None, None,
+                                None) == 0
+    assert L.turbo_quantize_kv(None, None, 1, 1, 0, 128, None, None, None, None, None, None, None, 0,
+                               None) == 0
+    # cache with a bad bit width
+    c = ta.TurboKVCacheStruct()
+    c.pages, c.group_meta, c.group_scale = 16, 16, 16
+    c.num_pages, c.num_group_slots, c.num_kv_heads, c.head_dim = 4, 1, 1, 128
+    c.head_bits[0] = 3
+    assert L.turbo_attn_decode(dummy, ctypes.byref(c), dummy, dummy, dummy, 1, 1, 1, 0.1, 1, None,
+                               0, dummy, None, None) == -1
+    c.head_bits[0] = 4
+    # workspace required for 2 chunks of 1 group each but not given
+    assert L.turbo_attn_decode(dummy, ctypes.byref(c), dummy, dummy, dummy, 2, 1, 1, 0.1, 1, None,
+                               0, dummy, None, None) == -3
+    # quantize with a cache whose head count differs from Hkv
+    assert L.turbo_quantize_kv(dummy, dummy, 1, 2, 64, 128, dummy, dummy, dummy, dummy,
+                               ctypes.byref(c), dummy, dummy, 1, None) == -1
+    # max_groups too small for N
+    assert L.turbo_quantize_kv(dummy, dummy, 1, 1, 192, 128, dummy, dummy, dummy, dummy,
+                               ctypes.byref(c), dummy, dummy, 2, None) == -1
+
+
+def test_decode_split_and_workspace(ta):
+    L = ta.lib()
+    assert L.turbo_decode_auto_split(64, 10, 128) == 19       # ceil(4096/640)=7 chunks
+    assert L.turbo_decode_auto_split(256, 8, 512) == 256      # 2 chunks
+    assert L.turbo_decode_auto_split(4096, 8, 4) == 4         # one chunk
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10) == 0
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3) == 4 * 8 * 4 * 132 * 4
+
+
+def test_step2_reciprocal_division_is_exact():
+    """The step-2 kernel divides by 2s as (num * (2^20 // (2s) + 1)) >> 20;
+    exact for every integer scale s in 1..80 and numerator up to 2*238 + s."""
+    for s in range(1, 81):
+        M = (1 << 20) // (2 * s) + 1
+        num = np.arange(0, 2 * 238 + s + 1, dtype=np.int64)
+        assert np.array_equal((num * M) >> 20, num // (2 * s)), s
+
+
+def test_rne_magic_constant():
+    """fma(a, b, 1.5*2^23) leaves round-half-even(a*b) in the low mantissa
+    bits for |a*b| < 2^22 (binary32)."""
+    magic = np.float32(12582912.0)
+    assert magic.view(np.int32) == 0x4B400000
+    x = np.array([-119.0, -2.5, -0.5, 0.5, 1.5, 2.5, 118.5, 119.0, 3.4999998], np.float64)
+    got = ((x + np.float64(magic)).astype(np.float32).view(np.int32) - 0x4B400000)
+    assert got.tolist() == np.rint(x).astype(int).tolist()
+
+
+@pytest.mark.parametrize("bits", [[4, 2, 4], [2, 2], [4]])
+def test_cache_format_round_trip(bits):
+    rng = np.random.default_rng(1)
+    H, ng, B = len(bits), 3, 2
+    off, pb = cache_layout.head_offsets(bits)
+    pages = np.zeros((B * ng * 4, pb), np.uint8)
+    gmeta = np.zeros((B * ng, H, 4, 128), np.int8)
+    gscale = np.zeros((B * ng, H, 2), np.float32)
+    bt = rng.permutation(B * ng * 4).reshape(B, ng * 4)
+    gt = rng.permutation(B * ng).reshape(B, ng)
+    units = {}
+    for b in range(B):
+        for h in range(H):
+            lv = (1 << bits[h]) - 1
+            u = dict(kc=rng.integers(0, lv + 1, (ng * 64, 128)).astype(np.uint8),
+                     vc=rng.integers(0, lv + 1, (ng * 64, 128)).astype(np.uint8),
+                     ks=rng.integers(1, 80, (ng, 128)).astype(np.uint8),
+                     kz=rng.integers(-119, 120, (ng, 128)).astype(np.int8),
+                     vs=rng.integers(1, 80, (ng, 128)).astype(np.uint8),
+                     vz=rng.integers(-119, 120, (ng, 128)).astype(np.int8),
+                     sk=rng.random(ng).astype(np.float32), sv=rng.random(ng).astype(np.float32))
+            units[b, h] = u
+            cache_layout.write_unit(pages, gmeta, gscale, bits, bt, gt, b, h, u)
+    for (b, h), u in units.items():
+        r = cache_layout.read_unit(pages, gmeta, gscale, bits, bt, gt, b, h, ng)
+        for key in u:
+            assert np.array_equal(r[key], u[key]), (b, h, key)
+    # documented byte order: int4 K byte 0 = channel 0 (low nibble), channel 1 (high)
+    u = units[0, 0]
+    first = pages[bt[0, 0], off[0]]
+    if bits[0] == 4:
+        assert first == (u["kc"][0, 0] | (u["kc"][0, 1] << 4))
+    else:
+        assert first == (u["kc"][0, 0] | (u["kc"][0, 1] << 2) | (u["kc"][0, 2] << 4)
+                         | (u["kc"][0, 3] << 6))
