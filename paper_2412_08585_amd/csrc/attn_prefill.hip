@@ -100,6 +100,34 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
   // A-operand row m of a 32-key half holds key kidx(m)
   const int m = lane & 31;
   const int kidx = 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3);
+  const int8_t* klane = kbase + (32 * 0 + kidx) * 128 + 16 * hf;
+  const int8_t* vlane = vbase + n * 64 + 16 * hf;
+
+  auto load_k = [&](v4i (&kop)[2][4], int j) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        kop[kb][ks] = *reinterpret_cast<const v4i*>(klane + ((long)j * 64 + 32 * kb) * 128 + 32 * ks);
+  };
+  auto load_v = [&](v4i (&vop)[4][2], int j) {
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        vop[cb][kb] = *reinterpret_cast<const v4i*>(vlane + (long)j * 8192 + 32 * cb * 64 + 32 * kb);
+  };
+  auto qk = [&](v16i (&S)[2][2], const v4i (&kop)[2][4]) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        v16i acc = {};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x32(kop[kb][ks], qop[qb][ks], acc);
+        S[kb][qb] = acc;
+      }
+  };
 
   float O[4][2][16];
 #pragma unroll
@@ -112,47 +140,48 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
   float lhalf[2] = {0.0f, 0.0f};
 
   const int jend = a.causal ? i : a.nb - 1;
+  // Software pipeline: while the VALU works on the softmax of tile j, the
+  // MFMA computes S for tile j+1 from K registers loaded one tile ahead; V of
+  // tile j+1 is loaded behind the PV of tile j.
+  v4i kop[2][4];
+  v4i vop[4][2];
+  v16i S[2][2];
+  load_k(kop, 0);
+  qk(S, kop);
+  load_v(vop, 0);
   for (int j = 0; j <= jend; ++j) {
-    // ---- S^T = K_j Q_i^T (int32) -------------------------------------
-    v16i sacc[2][2];
-    {
-      v4i kop[2][4];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-          kop[kb][ks] = *reinterpret_cast<const v4i*>(
-              kbase + ((long)j * 64 + 32 * kb + kidx) * 128 + 32 * ks + 16 * hf);
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          v16i acc = {};
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x32(kop[kb][ks], qop[qb][ks], acc);
-          sacc[kb][qb] = acc;
-        }
-    }
-    // ---- scores, online max, SAS ------------------------------------
+    const int jn = min(j + 1, jend);
+    load_k(kop, jn);
+    // ---- scores, online max, SAS (Algorithm 1, statistics step) --------
     const float c = (sq * skp[j]) * a.sm_scale;
+    // masking only on the diagonal tile and on tiles that reach past N
+    const bool need_mask = (a.causal && j == i) || (64 * j + 64 > N) || (64 * i + 64 > N);
     float P[2][2][16];
     float alpha[2];
     float pmax = 0.0f;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      const int qrow = 64 * i + 32 * qb + n;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) P[kb][qb][r] = (float)S[kb][qb][r] * c;
+      if (need_mask) {
+        const int qrow = 64 * i + 32 * qb + n;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = 64 * j + 32 * kb + 16 * hf + r;
+            const bool vis = key < N && qrow < N && (!a.causal || key <= qrow);
+            P[kb][qb][r] = vis ? P[kb][qb][r] : -INFINITY;
+          }
+      }
       float smax = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = 64 * j + 32 * kb + 16 * hf + r;
-          const bool vis = key < N && qrow < N && (!a.causal || key <= qrow);
-          const float s = (float)sacc[kb][qb][r] * c;
-          P[kb][qb][r] = vis ? s : -INFINITY;
-          smax = fmaxf(smax, P[kb][qb][r]);
-        }
-      smax = fmaxf(smax, __shfl_xor(smax, 32));
+        for (int r = 0; r < 16; ++r) smax = fmaxf(smax, P[kb][qb][r]);
+      smax = max_xor32(smax);
       const float mold = mrow[qb];
       const float mnew = fmaxf(mold, smax);
       float rs = 0.0f;
@@ -160,64 +189,54 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float s = P[kb][qb][r];
-          const float p = (s == -INFINITY) ? 0.0f : sas_y(mnew - s, lut);
+          const float p = sas_y(mnew - P[kb][qb][r], lut);
           P[kb][qb][r] = p;
           rs += p;
           pmax = fmaxf(pmax, p);
         }
-      alpha[qb] = (mold == -INFINITY) ? 0.0f : sas_y(mnew - mold, lut);
+      alpha[qb] = sas_y(mnew - mold, lut);  // 0 when mold = -inf
       lhalf[qb] = alpha[qb] * lhalf[qb] + rs;
       mrow[qb] = mnew;
     }
-    pmax = wave_max(pmax);
+    pmax = wave_max_fast(pmax);
+    // ---- Q(P~) with scale pmax/119 over the 64x64 tile -----------------
+    // (a tile with pmax = 0 gets inv = 0, Q(P~) = 0 and adds nothing)
+    const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
+    const float spv = (pmax / kQmax) * svp[j];
+    v4i pop[2][2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        int w[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          w[u] = pack4(rne_mul(P[kb][qb][4 * u], inv), rne_mul(P[kb][qb][4 * u + 1], inv),
+                       rne_mul(P[kb][qb][4 * u + 2], inv), rne_mul(P[kb][qb][4 * u + 3], inv));
+        pop[kb][qb] = v4i{w[0], w[1], w[2], w[3]};
+      }
+    // ---- next tile's S on the MFMA -------------------------------------
+    qk(S, kop);
+    // ---- O^T = alpha O^T + s_P s_V V_j^T Q(P~)^T -------------------------
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+      for (int qb = 0; qb < 2; ++qb) {
+        v16i acc = {};
 #pragma unroll
-        for (int r = 0; r < 16; ++r) O[cb][qb][r] *= alpha[qb];
-    if (pmax > 0.0f) {
-      // ---- Q(P~) with scale pmax/119 over the 64x64 tile -------------
-      const float inv = kQmax / pmax;
-      const float spv = (pmax / kQmax) * svp[j];
-      v4i pop[2][2];
+        for (int kb = 0; kb < 2; ++kb) acc = mfma32x32x32(vop[cb][kb], pop[kb][qb], acc);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          int w[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            w[u] = pack4(rne_mul(P[kb][qb][4 * u], inv), rne_mul(P[kb][qb][4 * u + 1], inv),
-                         rne_mul(P[kb][qb][4 * u + 2], inv), rne_mul(P[kb][qb][4 * u + 3], inv));
-          pop[kb][qb] = v4i{w[0], w[1], w[2], w[3]};
-        }
-      // ---- O^T += s_P s_V V_j^T Q(P~)^T ---------------------------------
-      const int8_t* vb = vbase + (long)j * 8192;
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        v4i vop[2];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          vop[kb] = *reinterpret_cast<const v4i*>(vb + (32 * cb + n) * 64 + 32 * kb + 16 * hf);
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          v16i acc = {};
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb) acc = mfma32x32x32(vop[kb], pop[kb][qb], acc);
-#pragma unroll
-          for (int r = 0; r < 16; ++r) O[cb][qb][r] = __builtin_fmaf(spv, (float)acc[r], O[cb][qb][r]);
-        }
+        for (int r = 0; r < 16; ++r)
+          O[cb][qb][r] = __builtin_fmaf(spv, (float)acc[r], O[cb][qb][r] * alpha[qb]);
       }
-    }
+    load_v(vop, jn);
   }
 
   // ---- epilogue: O / l (fp16), L = m + ln l ----------------------------
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int qrow = 64 * i + 32 * qb + n;
-    const float l = lhalf[qb] + __shfl_xor(lhalf[qb], 32);
+    const float l = add_xor32(lhalf[qb]);
     if (qrow >= N) continue;
     const float rl = 1.0f / l;
     uint2* orow = a.o + (((long)b * a.Hq + h) * N + qrow) * 32;
@@ -227,10 +246,9 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
       for (int g = 0; g < 4; ++g) {
         f16x4_t hv;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][qb][4 * g + e] / l);
+        for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][qb][4 * g + e] * rl);
         orow[(32 * cb + 8 * g + 4 * hf) / 4] = __builtin_bit_cast(uint2, hv);
       }
-    (void)rl;
     if (a.lse && hf == 0) a.lse[((long)b * a.Hq + h) * N + qrow] = mrow[qb] + logf(l);
   }
 }

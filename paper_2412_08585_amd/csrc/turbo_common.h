@@ -45,22 +45,59 @@ __device__ __forceinline__ float poly(float f) {
 }
 
 // SAS of x = -y, y >= 0, with the table in LDS (8 floats, entry 7 = 0).
+// Branch-free: y > 6 (x < n_r), y = +inf (a masked score) and y = NaN (a row
+// with no visible key yet) all select the zero entry.
 __device__ __forceinline__ float sas_y(float y, const float* lut) {
-  const float k = __builtin_floorf(y);
-  const float f = y - k;  // exact
-  const int idx = (y > kNr) ? 7 : (int)k;
-  return lut[idx] * poly(f);
+  const float yc = (y <= kNr) ? y : 7.0f;
+  const float k = __builtin_floorf(yc);
+  const float f = yc - k;  // exact
+  return lut[(int)k] * poly(f);
 }
 
 // SAS with the table in registers (used where LDS is not set up).
 __device__ __forceinline__ float sas_y_reg(float y) {
-  const float k = __builtin_floorf(y);
-  const float f = y - k;
+  const float yc = (y <= kNr) ? y : 7.0f;
+  const float k = __builtin_floorf(yc);
+  const float f = yc - k;
+  const int idx = (int)k;
   float l = 0.0f;
-  const int idx = (y > kNr) ? 7 : (int)k;
 #pragma unroll
   for (int i = 0; i < 7; ++i) l = (idx == i) ? kLut[i] : l;
   return l * poly(f);
+}
+
+// max(v, v of lane ^ 32): one v_permlane32_swap (gfx950) and one max.
+__device__ __forceinline__ float max_xor32(float v) {
+  const unsigned u = __float_as_uint(v);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float add_xor32(float v) {
+  const unsigned u = __float_as_uint(v);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// max(v, v of lane ^ 16) within each 32-lane half: v_permlane16_swap.
+__device__ __forceinline__ float max_xor16(float v) {
+  const unsigned u = __float_as_uint(v);
+  auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// max over the 16 lanes of a DPP row.
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xf, 0xf, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xf, 0xf, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xf, 0xf, false)));
+  return v;
+}
+
+// max over the 64 lanes of the wave (result in every lane).
+__device__ __forceinline__ float wave_max_fast(float v) {
+  return max_xor32(max_xor16(row16_max(v)));
 }
 
 __device__ __forceinline__ float wave_max(float v) {
