@@ -1,19 +1,28 @@
 // TurboAttention prefill on gfx950 (Algorithm 1): int8 QK^T and PV on the
 // 32x32x32 i8 MFMA, SAS online softmax in fp32 on the VALU.
 //
-// One wave owns one (sequence b, query head h, 64-query block i) and runs
-// over the key blocks j (j <= i when causal).
+// A workgroup of two waves owns one (sequence b, query head h, 64-query
+// block i); wave qh holds queries 64i + 32qh .. +31 and both run over the key
+// blocks j (j <= i when causal).  The P scale of Algorithm 1 covers the whole
+// 64x64 tile, so the two waves exchange their partial maxima through LDS once
+// per tile.  32 queries per wave keep a wave under 256 VGPRs (two waves per
+// SIMD, MFMA results in VGPRs).
 //
 // Register layout.  The scores are computed transposed, S^T = K Q^T, so that
-// each lane holds one query column:  for the 32x32 output block (kb, qb)
-// (32-key half kb, 32-query half qb), lane n + 32*hf, register r holds query
-// 32qb + n and key 32kb + 16hf + r.  This is obtained by feeding A-operand
-// row m of the K block with key 16*((m>>2)&1) + 4*(m>>3) + (m&3), the inverse
-// of the MFMA output row map 8(r/4) + 4hf + r%4.  Consequently the 16
-// quantized P values of a lane are, byte for byte, its B-operand for
-// O^T = V^T P^T with contraction index (hf, byte i) <-> key 16hf + i, and V^T
-// is read as 16 contiguous bytes of the channel-major int8 V block.  Row max
-// and row sum need one exchange between lanes n and n + 32.
+// each lane holds one query column:  for the 32x32 output block kb (32-key
+// half kb), lane n + 32*hf, register r holds query n and key 32kb + 16hf + r.
+// This is obtained by feeding A-operand row m of the K block with key
+// 16*((m>>2)&1) + 4*(m>>3) + (m&3), the inverse of the MFMA output row map
+// 8(r/4) + 4hf + r%4.  Consequently the 16 quantized P values of a lane are,
+// byte for byte, its B-operand for O^T = V^T P^T with contraction index
+// (hf, byte i) <-> key 16hf + i, and V^T is read as 16 contiguous bytes of
+// the channel-major int8 V block.  Row max and row sum need one exchange
+// between lanes n and n + 32 (v_permlane32_swap).
+//
+// The accumulator is kept as O = beta * Ost with a per-row factor beta, so
+// the rescale by SAS(m_old - m_new) of Algorithm 1 multiplies beta instead of
+// the 128 accumulator entries of a row; Ost is renormalized (a wave-uniform
+// rare path) when beta underflows or the factor is 0.
 #include "turbo_common.h"
 
 namespace turbo {
@@ -31,10 +40,14 @@ struct PrefillArgs {
   float* lse;          // [B][Hq][N] or null
 };
 
-__global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
+constexpr int kPrefillWaves = 2;
+
+__global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillArgs a) {
   __shared__ float lut[8];
-  const int lane = threadIdx.x;
-  if (lane < 8) lut[lane] = kLut[lane];
+  __shared__ float xmax[2][kPrefillWaves];  // per-wave P maxima, double-buffered
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, qh = tid >> 6;
+  if (tid < 8) lut[tid] = kLut[tid];
   __syncthreads();
 
   const int BH = a.B * a.Hq;
@@ -44,29 +57,30 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
   const int G = a.Hq / a.Hkv, kh = h / G;
   const int n = lane & 31, hf = lane >> 5;
   const int N = a.N;
+  const int qrow = 64 * i + 32 * qh + n;
 
-  // ---- Q_i -> int8 (eq. step1bpq), held as the QK^T B-operand ----------
-  // lane (n + 32hf), k-step ks: channels 32ks + 16hf .. +15 of query 32qb + n
-  v4i qop[2][4];
+  // ---- Q_i -> int8 (eq. step1bpq; scale over the 64-row block) ----------
+  // lane (n + 32hf), k-step ks: channels 32ks + 16hf .. +15 of query qrow
+  v4i qop[4];
   float sq;
   {
-    uint4 raw[2][4][2];
+    uint4 raw[4][2];
     float amax = 0.0f;
+    const uint4* src = a.q + (((long)b * a.Hq + h) * N + qrow) * 16;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int row = 64 * i + 32 * qb + n;
-      const uint4* src = a.q + (((long)b * a.Hq + h) * N + row) * 16;
+    for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+      for (int u = 0; u < 2; ++u) {
+        raw[ks][u] = qrow < N ? src[4 * ks + 2 * hf + u] : make_uint4(0, 0, 0, 0);
+        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[ks][u]);
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          raw[qb][ks][u] = row < N ? src[4 * ks + 2 * hf + u] : make_uint4(0, 0, 0, 0);
-          f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[qb][ks][u]);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
-        }
-    }
-    amax = wave_max(amax);
+        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
+      }
+    amax = wave_max_fast(amax);
+    if (lane == 0) xmax[0][qh] = amax;
+    __syncthreads();
+    amax = fmaxf(xmax[0][0], xmax[0][1]);
+    __syncthreads();
     float inv = 0.0f;
     sq = 0.0f;
     if (amax > 0.0f) {
@@ -74,34 +88,29 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
       inv = kQmax / amax;
     }
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int ks = 0; ks < 4; ++ks) {
+      int w[4];
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        int w[4];
+      for (int u = 0; u < 2; ++u) {
+        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[ks][u]);
+        int qv[8];
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[qb][ks][u]);
-          int qv[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
-          w[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
-          w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
-        }
-        qop[qb][ks] = v4i{w[0], w[1], w[2], w[3]};
+        for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
+        w[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
+        w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
       }
+      qop[ks] = v4i{w[0], w[1], w[2], w[3]};
+    }
   }
 
   const long kvu = (long)b * a.Hkv + kh;
-  const int8_t* kbase = a.k8 + kvu * a.nb * 8192;
-  const int8_t* vbase = a.v8 + kvu * a.nb * 8192;
   const float* skp = a.sk + kvu * a.nb;
   const float* svp = a.sv + kvu * a.nb;
-
   // A-operand row m of a 32-key half holds key kidx(m)
   const int m = lane & 31;
   const int kidx = 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3);
-  const int8_t* klane = kbase + (32 * 0 + kidx) * 128 + 16 * hf;
-  const int8_t* vlane = vbase + n * 64 + 16 * hf;
+  const int8_t* klane = a.k8 + kvu * a.nb * 8192 + kidx * 128 + 16 * hf;
+  const int8_t* vlane = a.v8 + kvu * a.nb * 8192 + n * 64 + 16 * hf;
 
   auto load_k = [&](v4i (&kop)[2][4], int j) {
 #pragma unroll
@@ -117,27 +126,22 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
       for (int kb = 0; kb < 2; ++kb)
         vop[cb][kb] = *reinterpret_cast<const v4i*>(vlane + (long)j * 8192 + 32 * cb * 64 + 32 * kb);
   };
-  auto qk = [&](v16i (&S)[2][2], const v4i (&kop)[2][4]) {
+  auto qk = [&](v16i (&S)[2], const v4i (&kop)[2][4]) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb) {
+      v16i acc = {};
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        v16i acc = {};
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x32(kop[kb][ks], qop[qb][ks], acc);
-        S[kb][qb] = acc;
-      }
+      for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x32(kop[kb][ks], qop[ks], acc);
+      S[kb] = acc;
+    }
   };
 
-  float O[4][2][16];
+  float O[4][16];
 #pragma unroll
   for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) O[cb][qb][r] = 0.0f;
-  float mrow[2] = {-INFINITY, -INFINITY};
-  float lhalf[2] = {0.0f, 0.0f};
+    for (int r = 0; r < 16; ++r) O[cb][r] = 0.0f;
+  float mrow = -INFINITY, lhalf = 0.0f, beta = 1.0f;
 
   const int jend = a.causal ? i : a.nb - 1;
   // Software pipeline: while the VALU works on the softmax of tile j, the
@@ -145,7 +149,7 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
   // tile j+1 is loaded behind the PV of tile j.
   v4i kop[2][4];
   v4i vop[4][2];
-  v16i S[2][2];
+  v16i S[2];
   load_k(kop, 0);
   qk(S, kop);
   load_v(vop, 0);
@@ -154,108 +158,107 @@ __global__ __launch_bounds__(64, 1) void k_attn_prefill(PrefillArgs a) {
     load_k(kop, jn);
     // ---- scores, online max, SAS (Algorithm 1, statistics step) --------
     const float c = (sq * skp[j]) * a.sm_scale;
+    float P[2][16];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) P[kb][r] = (float)S[kb][r] * c;
     // masking only on the diagonal tile and on tiles that reach past N
-    const bool need_mask = (a.causal && j == i) || (64 * j + 64 > N) || (64 * i + 64 > N);
-    float P[2][2][16];
-    float alpha[2];
-    float pmax = 0.0f;
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) P[kb][qb][r] = (float)S[kb][qb][r] * c;
-      if (need_mask) {
-        const int qrow = 64 * i + 32 * qb + n;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = 64 * j + 32 * kb + 16 * hf + r;
-            const bool vis = key < N && qrow < N && (!a.causal || key <= qrow);
-            P[kb][qb][r] = vis ? P[kb][qb][r] : -INFINITY;
-          }
-      }
-      float smax = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) smax = fmaxf(smax, P[kb][qb][r]);
-      smax = max_xor32(smax);
-      const float mold = mrow[qb];
-      const float mnew = fmaxf(mold, smax);
-      float rs = 0.0f;
+    if ((a.causal && j == i) || (64 * j + 64 > N) || (64 * i + 64 > N)) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = sas_y(mnew - P[kb][qb][r], lut);
-          P[kb][qb][r] = p;
-          rs += p;
-          pmax = fmaxf(pmax, p);
+          const int key = 64 * j + 32 * kb + 16 * hf + r;
+          const bool vis = key < N && qrow < N && (!a.causal || key <= qrow);
+          P[kb][r] = vis ? P[kb][r] : -INFINITY;
         }
-      alpha[qb] = sas_y(mnew - mold, lut);  // 0 when mold = -inf
-      lhalf[qb] = alpha[qb] * lhalf[qb] + rs;
-      mrow[qb] = mnew;
     }
-    pmax = wave_max_fast(pmax);
-    // ---- Q(P~) with scale pmax/119 over the 64x64 tile -----------------
-    // (a tile with pmax = 0 gets inv = 0, Q(P~) = 0 and adds nothing)
-    const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
-    const float spv = (pmax / kQmax) * svp[j];
-    v4i pop[2][2];
+    float smax = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        int w[4];
+      for (int r = 0; r < 16; ++r) smax = fmaxf(smax, P[kb][r]);
+    smax = max_xor32(smax);
+    const float mold = mrow;
+    const float mnew = fmaxf(mold, smax);
+    float rs = 0.0f, pmax = 0.0f;
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          w[u] = pack4(rne_mul(P[kb][qb][4 * u], inv), rne_mul(P[kb][qb][4 * u + 1], inv),
-                       rne_mul(P[kb][qb][4 * u + 2], inv), rne_mul(P[kb][qb][4 * u + 3], inv));
-        pop[kb][qb] = v4i{w[0], w[1], w[2], w[3]};
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = sas_y(mnew - P[kb][r], lut);
+        P[kb][r] = p;
+        rs += p;
+        pmax = fmaxf(pmax, p);
       }
+    const float alpha = sas_y(mnew - mold, lut);  // 0 when mold = -inf
+    lhalf = alpha * lhalf + rs;
+    mrow = mnew;
+    // ---- tile maximum of P~ over both waves ----------------------------
+    pmax = wave_max_fast(pmax);
+    if (lane == 0) xmax[j & 1][qh] = pmax;
+    __syncthreads();
+    pmax = fmaxf(xmax[j & 1][0], xmax[j & 1][1]);
+    // ---- Q(P~) with scale pmax/119 over the 64x64 tile -----------------
+    // (a tile with pmax = 0 gets inv = 0, Q(P~) = 0 and adds nothing)
+    const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
+    v4i pop[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      int w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        w[u] = pack4(rne_mul(P[kb][4 * u], inv), rne_mul(P[kb][4 * u + 1], inv),
+                     rne_mul(P[kb][4 * u + 2], inv), rne_mul(P[kb][4 * u + 3], inv));
+      pop[kb] = v4i{w[0], w[1], w[2], w[3]};
+    }
     // ---- next tile's S on the MFMA -------------------------------------
     qk(S, kop);
-    // ---- O^T = alpha O^T + s_P s_V V_j^T Q(P~)^T -------------------------
+    // ---- rescale factor: O = beta * Ost --------------------------------
+    float nbeta = beta * alpha;
+    if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb)
+      for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        v16i acc = {};
+        for (int r = 0; r < 16; ++r) O[cb][r] *= nbeta;
+      nbeta = 1.0f;
+    }
+    beta = nbeta;
+    const float g = ((pmax / kQmax) * svp[j]) * __builtin_amdgcn_rcpf(beta);
+    // ---- Ost += (s_P s_V / beta) V_j^T Q(P~)^T ---------------------------
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) acc = mfma32x32x32(vop[cb][kb], pop[kb][qb], acc);
+    for (int cb = 0; cb < 4; ++cb) {
+      v16i acc = {};
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          O[cb][qb][r] = __builtin_fmaf(spv, (float)acc[r], O[cb][qb][r] * alpha[qb]);
-      }
+      for (int kb = 0; kb < 2; ++kb) acc = mfma32x32x32(vop[cb][kb], pop[kb], acc);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) O[cb][r] = __builtin_fmaf(g, (float)acc[r], O[cb][r]);
+    }
     load_v(vop, jn);
   }
 
   // ---- epilogue: O / l (fp16), L = m + ln l ----------------------------
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int qrow = 64 * i + 32 * qb + n;
-    const float l = add_xor32(lhalf[qb]);
-    if (qrow >= N) continue;
-    const float rl = 1.0f / l;
+  const float l = add_xor32(lhalf);
+  if (qrow < N) {
+    const float f = beta / l;
     uint2* orow = a.o + (((long)b * a.Hq + h) * N + qrow) * 32;
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
+      for (int g4 = 0; g4 < 4; ++g4) {
         f16x4_t hv;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][qb][4 * g + e] * rl);
-        orow[(32 * cb + 8 * g + 4 * hf) / 4] = __builtin_bit_cast(uint2, hv);
+        for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][4 * g4 + e] * f);
+        orow[(32 * cb + 8 * g4 + 4 * hf) / 4] = __builtin_bit_cast(uint2, hv);
       }
-    if (a.lse && hf == 0) a.lse[((long)b * a.Hq + h) * N + qrow] = mrow[qb] + logf(l);
+    if (a.lse && hf == 0) a.lse[((long)b * a.Hq + h) * N + qrow] = mrow + logf(l);
   }
 }
 
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hq * a.nb;
-  hipLaunchKernelGGL(k_attn_prefill, dim3(total), dim3(64), 0, stream, a);
+  hipLaunchKernelGGL(k_attn_prefill, dim3(total), dim3(64 * kPrefillWaves), 0, stream, a);
   return hipGetLastError();
 }
 

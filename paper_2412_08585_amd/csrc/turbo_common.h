@@ -49,9 +49,8 @@ __device__ __forceinline__ float poly(float f) {
 // with no visible key yet) all select the zero entry.
 __device__ __forceinline__ float sas_y(float y, const float* lut) {
   const float yc = (y <= kNr) ? y : 7.0f;
-  const float k = __builtin_floorf(yc);
-  const float f = yc - k;  // exact
-  return lut[(int)k] * poly(f);
+  const float f = __builtin_amdgcn_fractf(yc);  // yc - floor(yc), exact
+  return lut[(int)__builtin_floorf(yc)] * poly(f);
 }
 
 // SAS with the table in registers (used where LDS is not set up).
