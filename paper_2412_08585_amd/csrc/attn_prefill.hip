@@ -144,20 +144,22 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
   float mrow = -INFINITY, lhalf = 0.0f, beta = 1.0f;
 
   const int jend = a.causal ? i : a.nb - 1;
-  // Software pipeline: while the VALU works on the softmax of tile j, the
-  // MFMA computes S for tile j+1 from K registers loaded one tile ahead; V of
-  // tile j+1 is loaded behind the PV of tile j.
+  // Software pipeline per tile j:  softmax of S_j on the VALU (K of tile j+1
+  // already in flight) -> tile maximum exchange -> PV_j and then S_{j+1} on
+  // the MFMA -> accumulator update on the VALU while S_{j+1} is computed.
   v4i kop[2][4];
   v4i vop[4][2];
   v16i S[2];
   load_k(kop, 0);
   qk(S, kop);
   load_v(vop, 0);
+  float skj = skp[0], svj = svp[0];
   for (int j = 0; j <= jend; ++j) {
     const int jn = min(j + 1, jend);
     load_k(kop, jn);
+    const float skn = skp[jn], svn = svp[jn];
     // ---- scores, online max, SAS (Algorithm 1, statistics step) --------
-    const float c = (sq * skp[j]) * a.sm_scale;
+    const float c = (sq * skj) * a.sm_scale;
     float P[2][16];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -200,21 +202,6 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
     if (lane == 0) xmax[j & 1][qh] = pmax;
     __syncthreads();
     pmax = fmaxf(xmax[j & 1][0], xmax[j & 1][1]);
-    // ---- Q(P~) with scale pmax/119 over the 64x64 tile -----------------
-    // (a tile with pmax = 0 gets inv = 0, Q(P~) = 0 and adds nothing)
-    const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
-    v4i pop[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      int w[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        w[u] = pack4(rne_mul(P[kb][4 * u], inv), rne_mul(P[kb][4 * u + 1], inv),
-                     rne_mul(P[kb][4 * u + 2], inv), rne_mul(P[kb][4 * u + 3], inv));
-      pop[kb] = v4i{w[0], w[1], w[2], w[3]};
-    }
-    // ---- next tile's S on the MFMA -------------------------------------
-    qk(S, kop);
     // ---- rescale factor: O = beta * Ost --------------------------------
     float nbeta = beta * alpha;
     if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
@@ -225,17 +212,38 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
       nbeta = 1.0f;
     }
     beta = nbeta;
-    const float g = ((pmax / kQmax) * svp[j]) * __builtin_amdgcn_rcpf(beta);
-    // ---- Ost += (s_P s_V / beta) V_j^T Q(P~)^T ---------------------------
+    // ---- Q(P~) with scale pmax/119 over the 64x64 tile -----------------
+    // (a tile with pmax = 0 gets inv = 0, Q(P~) = 0 and adds nothing)
+    const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
+    const float g = ((pmax / kQmax) * svj) * __builtin_amdgcn_rcpf(beta);
+    v4i pop[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      int w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        w[u] = pack_lo4(rne_bits(P[kb][4 * u], inv), rne_bits(P[kb][4 * u + 1], inv),
+                        rne_bits(P[kb][4 * u + 2], inv), rne_bits(P[kb][4 * u + 3], inv));
+      pop[kb] = v4i{w[0], w[1], w[2], w[3]};
+    }
+    // ---- PV_j, then S_{j+1}, on the MFMA -------------------------------
+    v16i acc[4];
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
-      v16i acc = {};
+      v16i t = {};
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) acc = mfma32x32x32(vop[cb][kb], pop[kb], acc);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) O[cb][r] = __builtin_fmaf(g, (float)acc[r], O[cb][r]);
+      for (int kb = 0; kb < 2; ++kb) t = mfma32x32x32(vop[cb][kb], pop[kb], t);
+      acc[cb] = t;
     }
+    qk(S, kop);
+    // ---- Ost += (s_P s_V / beta) V_j^T Q(P~)^T ---------------------------
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) O[cb][r] = __builtin_fmaf(g, (float)acc[cb][r], O[cb][r]);
     load_v(vop, jn);
+    skj = skn;
+    svj = svn;
   }
 
   // ---- epilogue: O / l (fp16), L = m + ln l ----------------------------

@@ -47,10 +47,29 @@ __device__ __forceinline__ float poly(float f) {
 // SAS of x = -y, y >= 0, with the table in LDS (8 floats, entry 7 = 0).
 // Branch-free: y > 6 (x < n_r), y = +inf (a masked score) and y = NaN (a row
 // with no visible key yet) all select the zero entry.
+__device__ __forceinline__ int cvt_flr_i32(float x) {
+  int r;
+  asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+
 __device__ __forceinline__ float sas_y(float y, const float* lut) {
   const float yc = (y <= kNr) ? y : 7.0f;
   const float f = __builtin_amdgcn_fractf(yc);  // yc - floor(yc), exact
-  return lut[(int)__builtin_floorf(yc)] * poly(f);
+  return lut[cvt_flr_i32(yc)] * poly(f);
+}
+
+// Bits of fma(a, b, 1.5*2^23): the low byte is round-half-even(a*b) when
+// 0 <= a*b < 256 (codes of Q(P~) and the like).
+__device__ __forceinline__ int rne_bits(float a, float b) {
+  return __float_as_int(__builtin_fmaf(a, b, kMagic));
+}
+
+// Low bytes of four dwords packed into one (two v_perm_b32).
+__device__ __forceinline__ int pack_lo4(int x0, int x1, int x2, int x3) {
+  const int t01 = (int)__builtin_amdgcn_perm((unsigned)x1, (unsigned)x0, 0x0c0c0400u);
+  const int t23 = (int)__builtin_amdgcn_perm((unsigned)x3, (unsigned)x2, 0x04000c0cu);
+  return t01 | t23;
 }
 
 // SAS with the table in registers (used where LDS is not set up).
