@@ -3,25 +3,34 @@
 // k_decode_combine).
 //
 // One wave owns one (sequence b, KV head kh, chunk s) and all G query heads
-// of kh.  Contractions run on the 16x16x64 i8 MFMA; the G query rows are the
-// N columns (G <= 16).
+// of kh (padded to GP = 1, 2, 4, 8 or 16 rows).  Per 64-token group:
 //
-// Layouts.  Lane = n + 16*g4 (n = lane & 15, g4 = lane >> 4).
-//  * QK^T is computed transposed, S^T = K q^T.  A-operand row m of m-block mb
-//    holds token 16*(m>>2) + 4*mb + (m&3) of the 64-token group, so that the
-//    MFMA output of lane (n, g4), register r of m-block mb is the score of
-//    query row n against token 16*g4 + 4*mb + r.  The 16 quantized P values
-//    of a lane are then, in order, the scores of its row against the tokens
-//    of page g4 -- exactly the B-operand of O^T = V^T P^T when the V^T
-//    A-operand of lane (c, g4) is the 16 codes of channel c in page g4, which
-//    is one contiguous 8-byte (int4) / 4-byte (int2) run of the
-//    channel-major page.
-//  * K is expanded to int8 in registers (code * s^int + z^int, Sec. 2.3);
-//    the contraction index of k-step ks, byte i is channel 32*g4 + 16*ks + i.
-//  * V is contracted on its raw codes and corrected per channel with the
-//    exact integer identity sum_t p_t (c_t s + z) = s sum_t p_t c_t +
-//    z sum_t p_t (eq. integer_inference of Sec. 2.3), so the int32 PV
-//    accumulator equals the one over the int8-expanded V.
+//  * QK^T on the raw codes.  With w_c = q_c * s_c split exactly as
+//    w = 128*hi + lo (lo in 0..127, hi in -75..74, both int8), the int32
+//    accumulator of Algorithm 2, sum_c q_c (code_c s_c + z_c), equals
+//    128 * sum hi*code + sum lo*code + sum_c q_c z_c  (eq. integer_inference
+//    of Sec. 2.3 applied to the step-2 dequantization code*s + z).  Two
+//    16x16x64 i8 MFMAs per k-step contract the unpacked 4/2-bit codes with
+//    hi and lo; the zero-point term enters as the initial accumulator.  The
+//    codes are only unpacked (mask/shift), never multiplied.
+//    S^T = K q^T: A-operand row m of m-block mb holds token
+//    16*(m>>2) + 4*mb + (m&3), so lane (n + 16*g4), register r of m-block mb
+//    is the score of query row n and token 16*g4 + 4*mb + r.
+//  * The GP x 64 scores go through LDS to a compact layout (lane L: row
+//    L / (64/GP), GP consecutive tokens) where the SAS online softmax of
+//    Algorithm 2 runs on useful values only; row reductions are DPP /
+//    permlane within the row's 64/GP lanes.
+//  * Q(P~) bytes return through LDS as the A-operand of O = P V (16x16x64
+//    MFMA, K index = the tokens of page kg in the order the V codes unpack
+//    to); the B-operand is the 16 codes of a channel in page kg, one
+//    contiguous 8-byte (int4) / 4-byte (int2) run of the channel-major page.
+//    PV is taken on the raw V codes and corrected per channel with
+//    s * acc + z * sum(Q(P~)) (same identity), which equals the int32
+//    accumulator over the int8-expanded V.  The GP x 128 result goes through
+//    LDS to the compact layout (lane L: row L / (64/GP), 2*GP channels) for
+//    the accumulator update.
+//  * The accumulator is kept as O = beta * Ost (per-row beta) so the
+//    rescale by SAS(m_old - m_new) touches one value per row.
 #include "turbo_common.h"
 
 namespace turbo {
@@ -50,85 +59,89 @@ struct DecodeArgs {
 constexpr int kWsStride = 132;  // m, l, two pad words, O[128] (16-byte aligned)
 constexpr int kWsO = 4;
 
-__device__ __forceinline__ int byte_of(const unsigned* w, int idx) {
-  return (int)((w[idx >> 2] >> (8 * (idx & 3))) & 0xffu);
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+
+// Reductions over the 64/GP consecutive lanes of a compact row (every lane
+// of the row receives the result).
+template <int LPR>
+__device__ __forceinline__ float row_max(float v) {
+  if (LPR >= 2) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false)));
+  if (LPR >= 4) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xf, 0xf, false)));
+  if (LPR >= 8) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false)));
+  if (LPR >= 16) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false)));
+  if (LPR >= 32) v = max_xor16(v);
+  if (LPR >= 64) v = max_xor32(v);
+  return v;
 }
 
-__device__ __forceinline__ int sbyte_of(const unsigned* w, int idx) {
-  return (int)(int8_t)((w[idx >> 2] >> (8 * (idx & 3))) & 0xffu);
-}
-
-__global__ __launch_bounds__(64, 1) void k_attn_decode(DecodeArgs a) {
-  __shared__ float lut[8];
-  const int lane = threadIdx.x;
-  if (lane < 8) lut[lane] = kLut[lane];
-  __syncthreads();
-
-  const int s = blockIdx.x % a.nsplit;
-  const int kh = (blockIdx.x / a.nsplit) % a.Hkv;
-  const int b = blockIdx.x / (a.nsplit * a.Hkv);
-  const int n = lane & 15, g4 = lane >> 4;
-  const int G = a.G;
-  const bool rowok = n < G;
-  const int h = kh * G + n;
-
-  int ng = a.seq_lens[b] / 64;
-  ng = min(max(ng, 0), a.max_groups);
-  const int g0 = s * a.split;
-  const int g1 = min(ng, g0 + a.split);
-
-  const int bits = ((a.int2_mask >> kh) & 1ull) ? 2 : 4;
-  const int head_off = 512 * (4 * kh - 2 * __popcll(a.int2_mask & ((1ull << kh) - 1ull)));
-
-  // ---- q -> int8 per (b, query head) (Algorithm 2; eq. step1bpq) ---------
-  v4i qop[2];
-  float sq = 0.0f;
-  {
-    uint4 raw[2][2];
-    float amax = 0.0f;
-    const uint4* src = a.q + ((long)b * a.Hq + (rowok ? h : 0)) * 16;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        raw[ks][u] = rowok ? src[4 * g4 + 2 * ks + u] : make_uint4(0, 0, 0, 0);
-        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[ks][u]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
-      }
-    amax = fmaxf(amax, __shfl_xor(amax, 16));
-    amax = fmaxf(amax, __shfl_xor(amax, 32));
-    float inv = 0.0f;
-    if (amax > 0.0f) {
-      sq = amax / kQmax;
-      inv = kQmax / amax;
-    }
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      int w[4];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[ks][u]);
-        int qv[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
-        w[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
-        w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
-      }
-      qop[ks] = v4i{w[0], w[1], w[2], w[3]};
-    }
+template <int LPR>
+__device__ __forceinline__ float row_sum(float v) {
+  if (LPR >= 2) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false));
+  if (LPR >= 4) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xf, 0xf, false));
+  if (LPR >= 8) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false));
+  if (LPR >= 16) v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false));
+  if (LPR >= 32) {
+    const unsigned u = __float_as_uint(v);
+    auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
   }
+  if (LPR >= 64) v = add_xor32(v);
+  return v;
+}
 
-  float O[8][4];
+// Position of page token j in the order the V codes unpack to (see the PV
+// step): int4 gives tokens {0,2,4,6},{1,3,5,7},{8,..},{9,..}; int2 gives
+// {0,4,8,12},{1,5,9,13},...
+template <int BITS>
+__device__ __forceinline__ int vpos(int j) {
+  if (BITS == 4) return (j & 8) + ((j & 1) << 2) + ((j & 7) >> 1);
+  return 4 * (j & 3) + (j >> 2);
+}
+
+template <int GP>
+struct DecodeLds {
+  float lut[8];
+  float sq[16];
+  int sbuf[GP][64];             // scores, row-major
+  unsigned char pbuf[GP][64];   // Q(P~), per page in V-unpack order
+  int obuf[GP][128];            // PV accumulators
+};
+
+template <int GP, int BITS>
+__device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>& L, int b, int kh,
+                                              int g0, int g1, int head_off, const int (&q8w)[8],
+                                              float& mrow, float& lpart, float& beta,
+                                              float (&O)[2 * GP], float sq_row) {
+  constexpr int LPR = 64 / GP;  // lanes per compact row
+  constexpr int CPL = 2 * GP;   // accumulator channels per lane
+  constexpr int d = BITS == 4 ? 2 : 4;
+  const int lane = threadIdx.x;
+  const int n = lane & 15, g4 = lane >> 4;
+  const int rr = lane / LPR, cc = lane % LPR;
+  const int m = lane & 15;
+
+  // 16-bit (q_ca, q_cb) pairs in the order the K codes unpack to: B-operand
+  // dword j of k-step ks covers channels c0 + {0, d, 2d, 3d}; pair xy = 0 is
+  // (c0, c0+d), xy = 1 is (c0+2d, c0+3d).
+  unsigned qpair[2][4][2];
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb)
+  for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) O[cb][r] = 0.0f;
-  float mrow = -INFINITY, lpart = 0.0f;
+    for (int j = 0; j < 4; ++j) {
+      const int c0 = BITS == 4 ? 16 * ks + 8 * (j >> 1) + (j & 1) : 16 * ks + j;
+#pragma unroll
+      for (int xy = 0; xy < 2; ++xy) {
+        const int ca = c0 + 2 * d * xy, cb = ca + d;
+        const int qa = (int)(int8_t)(q8w[ca >> 2] >> (8 * (ca & 3)));
+        const int qb = (int)(int8_t)(q8w[cb >> 2] >> (8 * (cb & 3)));
+        qpair[ks][j][xy] = ((unsigned)qa & 0xffffu) | ((unsigned)qb << 16);
+      }
+    }
 
   const int* bt = a.block_table + (long)b * 4 * a.max_groups;
   const int* gt = a.group_table + (long)b * a.max_groups;
-  const int m = lane & 15;
 
   for (int g = g0; g < g1; ++g) {
     long pg[4];
@@ -146,176 +159,313 @@ __global__ __launch_bounds__(64, 1) void k_attn_decode(DecodeArgs a) {
     const float skg = a.gscale[(slot * a.Hkv + kh) * 2 + 0];
     const float svg = a.gscale[(slot * a.Hkv + kh) * 2 + 1];
 
-    // K scale/zero of this lane's 32 channels 32g4 .. 32g4+31
-    unsigned ksw[8], kzw[8];
-    {
-      const uint4* ms = reinterpret_cast<const uint4*>(meta + 32 * g4);
-      const uint4* mz = reinterpret_cast<const uint4*>(meta + 128 + 32 * g4);
-      uint4 t0 = ms[0], t1 = ms[1], z0 = mz[0], z1 = mz[1];
-      ksw[0] = t0.x; ksw[1] = t0.y; ksw[2] = t0.z; ksw[3] = t0.w;
-      ksw[4] = t1.x; ksw[5] = t1.y; ksw[6] = t1.z; ksw[7] = t1.w;
-      kzw[0] = z0.x; kzw[1] = z0.y; kzw[2] = z0.z; kzw[3] = z0.w;
-      kzw[4] = z1.x; kzw[5] = z1.y; kzw[6] = z1.z; kzw[7] = z1.w;
-    }
-
-    // ---- S^T = K^{q1} q^T ---------------------------------------------
-    v4i sacc[4];
+    // ---- K codes of this lane: A-operand rows of the 4 m-blocks ---------
+    unsigned kraw[4][BITS];  // int4: 4 dwords (32 channels); int2: 2 dwords
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) {
       const uint8_t* krow = a.pages + pg[m >> 2] * a.page_bytes + head_off +
-                            (4 * mb + (m & 3)) * 16 * bits;
-      int kv[32];  // int8 values of channels 32g4 + e
-      if (bits == 4) {
-        uint4 x = *reinterpret_cast<const uint4*>(krow + 16 * g4);
-        unsigned xw[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-        for (int e = 0; e < 32; ++e) {
-          const int code = (int)((xw[e >> 3] >> (4 * (e & 7))) & 15u);
-          kv[e] = code * byte_of(ksw, e) + sbyte_of(kzw, e);
-        }
+                            (4 * mb + (m & 3)) * 16 * BITS + 4 * BITS * g4;
+      if (BITS == 4) {
+        const uint4 x = *reinterpret_cast<const uint4*>(krow);
+        kraw[mb][0] = x.x; kraw[mb][1] = x.y; kraw[mb][2] = x.z; kraw[mb][3] = x.w;
       } else {
-        uint2 x = *reinterpret_cast<const uint2*>(krow + 8 * g4);
-        unsigned xw[2] = {x.x, x.y};
-#pragma unroll
-        for (int e = 0; e < 32; ++e) {
-          const int code = (int)((xw[e >> 4] >> (2 * (e & 15))) & 3u);
-          kv[e] = code * byte_of(ksw, e) + sbyte_of(kzw, e);
-        }
+        const uint2 x = *reinterpret_cast<const uint2*>(krow);
+        kraw[mb][0] = x.x; kraw[mb][1] = x.y;
       }
-      v4i acc = {};
+    }
+    // ---- hi/lo B-operands from w = q * s^int (this lane's 32 channels) --
+    unsigned ks4[8], kz4[8];
+    {
+      const uint4* ms = reinterpret_cast<const uint4*>(meta + 32 * g4);
+      const uint4* mz = reinterpret_cast<const uint4*>(meta + 128 + 32 * g4);
+      const uint4 t0 = ms[0], t1 = ms[1], z0 = mz[0], z1 = mz[1];
+      ks4[0] = t0.x; ks4[1] = t0.y; ks4[2] = t0.z; ks4[3] = t0.w;
+      ks4[4] = t1.x; ks4[5] = t1.y; ks4[6] = t1.z; ks4[7] = t1.w;
+      kz4[0] = z0.x; kz4[1] = z0.y; kz4[2] = z0.z; kz4[3] = z0.w;
+      kz4[4] = z1.x; kz4[5] = z1.y; kz4[6] = z1.z; kz4[7] = z1.w;
+    }
+    v4i bhi[2], blo[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      int hw[4], lw[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c0 = BITS == 4 ? 16 * ks + 8 * (j >> 1) + (j & 1) : 16 * ks + j;
+        unsigned hx[2], lx[2];
+#pragma unroll
+        for (int xy = 0; xy < 2; ++xy) {
+          const int ca = c0 + 2 * d * xy, cb = ca + d;
+          // bytes [s_ca, 0, s_cb, 0]: the 16-bit pair (s_ca, s_cb)
+          const unsigned selb = (cb >> 2) == (ca >> 2) ? (unsigned)(cb & 3) : 4u + (cb & 3);
+          const unsigned sel = (unsigned)(ca & 3) | (0x0cu << 8) | (selb << 16) | (0x0cu << 24);
+          const unsigned spair = __builtin_amdgcn_perm(ks4[cb >> 2], ks4[ca >> 2], sel);
+          const u16x2 w =
+              __builtin_bit_cast(u16x2, qpair[ks][j][xy]) * __builtin_bit_cast(u16x2, spair);
+          hx[xy] = __builtin_bit_cast(unsigned, __builtin_bit_cast(s16x2, w) >> (short)7);
+          lx[xy] = __builtin_bit_cast(unsigned, w) & 0x007F007Fu;
+        }
+        hw[j] = (int)__builtin_amdgcn_perm(hx[1], hx[0], 0x06040200u);
+        lw[j] = (int)__builtin_amdgcn_perm(lx[1], lx[0], 0x06040200u);
+      }
+      bhi[ks] = v4i{hw[0], hw[1], hw[2], hw[3]};
+      blo[ks] = v4i{lw[0], lw[1], lw[2], lw[3]};
+    }
+    // zero-point term sum_c q_c z_c over the lane's channels, then over g4
+    int bias = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) bias = __builtin_amdgcn_sdot4(q8w[i], (int)kz4[i], bias, false);
+    bias = (int)add_xor32((float)bias);  // exact: |bias| < 2^24
+    {
+      const unsigned u = (unsigned)bias;
+      auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+      bias = (int)r[0] + (int)r[1];
+    }
+    // ---- S^T = K^{q1} q^T on the MFMA, scores to LDS -------------------
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      v4i kop[2];
+      if (BITS == 4) {
+        unsigned u[8];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          u[2 * w] = kraw[mb][w] & 0x0F0F0F0Fu;
+          u[2 * w + 1] = (kraw[mb][w] >> 4) & 0x0F0F0F0Fu;
+        }
+        kop[0] = v4i{(int)u[0], (int)u[1], (int)u[2], (int)u[3]};
+        kop[1] = v4i{(int)u[4], (int)u[5], (int)u[6], (int)u[7]};
+      } else {
+#pragma unroll
+        for (int w = 0; w < 2; ++w)
+          kop[w] = v4i{(int)(kraw[mb][w] & 0x03030303u), (int)((kraw[mb][w] >> 2) & 0x03030303u),
+                       (int)((kraw[mb][w] >> 4) & 0x03030303u),
+                       (int)((kraw[mb][w] >> 6) & 0x03030303u)};
+      }
+      v4i lo = v4i{bias, bias, bias, bias};
+      v4i hi = {};
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        v4i kop = v4i{pack4(kv[16 * ks + 0], kv[16 * ks + 1], kv[16 * ks + 2], kv[16 * ks + 3]),
-                      pack4(kv[16 * ks + 4], kv[16 * ks + 5], kv[16 * ks + 6], kv[16 * ks + 7]),
-                      pack4(kv[16 * ks + 8], kv[16 * ks + 9], kv[16 * ks + 10], kv[16 * ks + 11]),
-                      pack4(kv[16 * ks + 12], kv[16 * ks + 13], kv[16 * ks + 14], kv[16 * ks + 15])};
-        acc = mfma16x16x64(kop, qop[ks], acc);
+        lo = mfma16x16x64(kop[ks], blo[ks], lo);
+        hi = mfma16x16x64(kop[ks], bhi[ks], hi);
       }
-      sacc[mb] = acc;
+      if (n < GP) {
+        const int4 sv = make_int4((hi[0] << 7) + lo[0], (hi[1] << 7) + lo[1], (hi[2] << 7) + lo[2],
+                                  (hi[3] << 7) + lo[3]);
+        *reinterpret_cast<int4*>(&L.sbuf[n][16 * g4 + 4 * mb]) = sv;
+      }
     }
-
-    // ---- scores, online max, SAS (one row per lane column n) ----------
-    const float c = (sq * skg) * a.sm_scale;
-    float P[4][4];
-    float smax = -INFINITY;
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        P[mb][r] = (float)sacc[mb][r] * c;
-        smax = fmaxf(smax, P[mb][r]);
-      }
-    smax = fmaxf(smax, __shfl_xor(smax, 16));
-    smax = fmaxf(smax, __shfl_xor(smax, 32));
-    const float mnew = fmaxf(mrow, smax);
-    float rs = 0.0f, pmax = 0.0f;
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = sas_y(mnew - P[mb][r], lut);
-        P[mb][r] = p;
-        rs += p;
-        pmax = fmaxf(pmax, p);
-      }
-    const float alpha = (mrow == -INFINITY) ? 0.0f : sas_y(mnew - mrow, lut);
-    lpart = alpha * lpart + rs;
-    mrow = mnew;
-    pmax = fmaxf(pmax, __shfl_xor(pmax, 16));
-    pmax = fmaxf(pmax, __shfl_xor(pmax, 32));
-#pragma unroll
-    for (int cb = 0; cb < 8; ++cb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) O[cb][r] *= alpha;
+    __syncthreads();
+    // ---- compact softmax: lane (rr, cc) holds tokens cc*GP .. +GP-1 -------
+    float gsc;  // s_P s_V / beta of the row
+    int psum;   // sum of the row's Q(P~)
     {
-      // ---- Q(P~) with the row's scale pmax/119 over the group ----------
-      // pmax differs between the rows of the wave and is 0 for a row whose
-      // whole group lies more than 6 below its running maximum; such a row
-      // gets Q(P~) = 0 and adds nothing (no branch: the shuffles and the
-      // MFMA below need every lane).
-      const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
-      const float spv = (pmax / kQmax) * svg;
-      int qpw[4];
-      int psum = 0;
+      int si[GP];
+      if (GP >= 4) {
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        int qv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          qv[r] = rne_mul(P[mb][r], inv);
-          psum += qv[r];
+        for (int e = 0; e < GP; e += 4) {
+          const int4 t = *reinterpret_cast<const int4*>(&L.sbuf[rr][cc * GP + e]);
+          si[e] = t.x; si[e + 1] = t.y; si[e + 2] = t.z; si[e + 3] = t.w;
         }
-        qpw[mb] = pack4(qv[0], qv[1], qv[2], qv[3]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < GP; ++e) si[e] = L.sbuf[rr][cc * GP + e];
       }
-      psum += __shfl_xor(psum, 16);
-      psum += __shfl_xor(psum, 32);
-      const v4i pop = v4i{qpw[0], qpw[1], qpw[2], qpw[3]};
-      // ---- O^T += s_P s_V (s V^T_codes P^T + z sum P) --------------------
-      const uint8_t* vreg = a.pages + pg[g4] * a.page_bytes + head_off + 256 * bits;
+      const float c = (sq_row * skg) * a.sm_scale;
+      float p[GP];
+      float smax = -INFINITY;
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) {
-        const int ch = 16 * cb + n;  // A-operand row (channel) of this lane
-        int w[4];
-        if (bits == 4) {
-          uint2 x = *reinterpret_cast<const uint2*>(vreg + ch * 8);
-          unsigned xw[2] = {x.x, x.y};
+      for (int e = 0; e < GP; ++e) {
+        p[e] = (float)si[e] * c;
+        smax = fmaxf(smax, p[e]);
+      }
+      smax = row_max<LPR>(smax);
+      const float mnew = fmaxf(mrow, smax);
+      float rs = 0.0f, pmax = 0.0f;
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const unsigned src = xw[u >> 1] >> (16 * (u & 1));
-            w[u] = (int)((src & 15u) | (((src >> 4) & 15u) << 8) | (((src >> 8) & 15u) << 16) |
-                         (((src >> 12) & 15u) << 24));
-          }
-        } else {
-          const unsigned x = *reinterpret_cast<const unsigned*>(vreg + ch * 4);
+      for (int e = 0; e < GP; ++e) {
+        p[e] = sas_y(mnew - p[e], L.lut);
+        rs += p[e];
+        pmax = fmaxf(pmax, p[e]);
+      }
+      const float alpha = sas_y(mnew - mrow, L.lut);  // 0 when mrow = -inf
+      lpart = alpha * lpart + rs;
+      mrow = mnew;
+      pmax = row_max<LPR>(pmax);
+      // rescale: O = beta * Ost
+      float nbeta = beta * alpha;
+      if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const unsigned src = x >> (8 * u);
-            w[u] = (int)((src & 3u) | (((src >> 2) & 3u) << 8) | (((src >> 4) & 3u) << 16) |
-                         (((src >> 6) & 3u) << 24));
+        for (int e = 0; e < CPL; ++e) O[e] *= nbeta;
+        nbeta = 1.0f;
+      }
+      beta = nbeta;
+      // Q(P~) with the row's scale pmax/119 (a row whose group lies wholly
+      // below the threshold has pmax = 0: inv = 0, Q(P~) = 0, adds nothing)
+      const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
+      int ps = 0;
+#pragma unroll
+      for (int e = 0; e < GP; ++e) {
+        const int code = rne_bits(p[e], inv) & 0xff;
+        ps += code;
+        const int t = cc * GP + e;  // token of the group
+        L.pbuf[rr][16 * (t >> 4) + vpos<BITS>(t & 15)] = (unsigned char)code;
+      }
+      psum = (int)row_sum<LPR>((float)ps);  // exact: < 2^24
+      gsc = ((pmax / kQmax) * svg) * __builtin_amdgcn_rcpf(beta);
+    }
+    __syncthreads();
+    // ---- O = Q(P~) V on the raw codes (A = P rows, B = V codes) ---------
+    const v4i pop = n < GP ? *reinterpret_cast<const v4i*>(&L.pbuf[n < GP ? n : 0][16 * g4])
+                           : v4i{0, 0, 0, 0};
+    const uint8_t* vreg = a.pages + pg[g4] * a.page_bytes + head_off + 256 * BITS;
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      const int ch = 16 * cb + n;  // B-operand column (channel) of this lane
+      v4i vop;
+      if (BITS == 4) {
+        const uint2 x = *reinterpret_cast<const uint2*>(vreg + ch * 8);
+        vop = v4i{(int)(x.x & 0x0F0F0F0Fu), (int)((x.x >> 4) & 0x0F0F0F0Fu),
+                  (int)(x.y & 0x0F0F0F0Fu), (int)((x.y >> 4) & 0x0F0F0F0Fu)};
+      } else {
+        const unsigned x = *reinterpret_cast<const unsigned*>(vreg + ch * 4);
+        vop = v4i{(int)(x & 0x03030303u), (int)((x >> 2) & 0x03030303u),
+                  (int)((x >> 4) & 0x03030303u), (int)((x >> 6) & 0x03030303u)};
+      }
+      v4i acc = {};
+      acc = mfma16x16x64(pop, vop, acc);
+      // lane (n, g4), register r <-> row 4*g4 + r, channel 16*cb + n
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (4 * g4 + r < GP) L.obuf[4 * g4 + r < GP ? 4 * g4 + r : 0][16 * cb + n] = acc[r];
+    }
+    __syncthreads();
+    // ---- accumulator update in the compact layout -----------------------
+    {
+      const int c0 = cc * CPL;
+      int acc[CPL];
+      unsigned vsw, vzw;  // CPL <= 4: bytes of one dword
+      if (CPL >= 4) {
+#pragma unroll
+        for (int e = 0; e < CPL; e += 4) {
+          const int4 t = *reinterpret_cast<const int4*>(&L.obuf[rr][c0 + e]);
+          acc[e] = t.x; acc[e + 1] = t.y; acc[e + 2] = t.z; acc[e + 3] = t.w;
+        }
+      } else {
+        const int2 t = *reinterpret_cast<const int2*>(&L.obuf[rr][c0]);
+        acc[0] = t.x; acc[CPL > 1 ? 1 : 0] = t.y;
+      }
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) {
+        if ((e & 3) == 0) {
+          if (CPL >= 4) {
+            vsw = *reinterpret_cast<const unsigned*>(meta + 256 + c0 + e);
+            vzw = *reinterpret_cast<const unsigned*>(meta + 384 + c0 + e);
+          } else {
+            vsw = *reinterpret_cast<const unsigned short*>(meta + 256 + c0);
+            vzw = *reinterpret_cast<const unsigned short*>(meta + 384 + c0);
           }
         }
-        v4i acc = {};
-        acc = mfma16x16x64(v4i{w[0], w[1], w[2], w[3]}, pop, acc);
-        // output: lane (n, g4), register r <-> channel 16cb + 4g4 + r, row n
-        const unsigned vs4 = *reinterpret_cast<const unsigned*>(meta + 256 + 16 * cb + 4 * g4);
-        const unsigned vz4 = *reinterpret_cast<const unsigned*>(meta + 384 + 16 * cb + 4 * g4);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int sv_c = (int)((vs4 >> (8 * r)) & 0xffu);
-          const int zv_c = (int)(int8_t)((vz4 >> (8 * r)) & 0xffu);
-          const int pv = sv_c * acc[r] + zv_c * psum;
-          O[cb][r] = __builtin_fmaf(spv, (float)pv, O[cb][r]);
-        }
+        const int s_c = (int)((vsw >> (8 * (e & 3))) & 0xffu);
+        const int z_c = (int)(int8_t)((vzw >> (8 * (e & 3))) & 0xffu);
+        const int pv = s_c * acc[e] + z_c * psum;  // exact int32 PV of Algorithm 2
+        O[e] = __builtin_fmaf(gsc, (float)pv, O[e]);
       }
     }
   }
+}
 
-  // ---- epilogue -----------------------------------------------------------
-  float l = lpart + __shfl_xor(lpart, 16);
-  l += __shfl_xor(l, 32);
-  if (!rowok) return;
-  if (a.nsplit == 1) {
-    uint2* orow = a.o + ((long)b * a.Hq + h) * 32;
-    const bool empty = g1 <= g0;
+template <int GP>
+__global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
+  __shared__ DecodeLds<GP> L;
+  constexpr int LPR = 64 / GP;
+  constexpr int CPL = 2 * GP;
+  const int lane = threadIdx.x;
+  if (lane < 8) L.lut[lane] = kLut[lane];
+
+  const int s = blockIdx.x % a.nsplit;
+  const int kh = (blockIdx.x / a.nsplit) % a.Hkv;
+  const int b = blockIdx.x / (a.nsplit * a.Hkv);
+  const int n = lane & 15, g4 = lane >> 4;
+  const int rr = lane / LPR, cc = lane % LPR;
+  const int G = a.G;
+
+  int ng = a.seq_lens[b] / 64;
+  ng = min(max(ng, 0), a.max_groups);
+  const int g0 = s * a.split;
+  const int g1 = min(ng, g0 + a.split);
+
+  const int bits = ((a.int2_mask >> kh) & 1ull) ? 2 : 4;
+  const int head_off = 512 * (4 * kh - 2 * __popcll(a.int2_mask & ((1ull << kh) - 1ull)));
+
+  // ---- q -> int8 per (b, query head) (Algorithm 2; eq. step1bpq) ---------
+  // lane (n, g4) holds channels 32*g4 .. 32*g4+31 of row n (zero if n >= G)
+  int q8w[8];
+  {
+    const bool rowok = n < G;
+    uint4 raw[4];
+    float amax = 0.0f;
+    const uint4* src = a.q + ((long)b * a.Hq + kh * G + (rowok ? n : 0)) * 16;
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) {
-      f16x4_t hv;
+    for (int u = 0; u < 4; ++u) {
+      raw[u] = rowok ? src[4 * g4 + u] : make_uint4(0, 0, 0, 0);
+      f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[u]);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) hv[r] = empty ? (_Float16)0.0f : (_Float16)(O[cb][r] / l);
-      orow[(16 * cb + 4 * g4) / 4] = __builtin_bit_cast(uint2, hv);
+      for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
     }
-    if (a.lse && g4 == 0) a.lse[(long)b * a.Hq + h] = empty ? -INFINITY : mrow + logf(l);
+    amax = max_xor16(amax);
+    amax = max_xor32(amax);
+    float inv = 0.0f, sq = 0.0f;
+    if (amax > 0.0f) {
+      sq = amax / kQmax;
+      inv = kQmax / amax;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[u]);
+      int qv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
+      q8w[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
+      q8w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
+    }
+    if (g4 == 0) L.sq[n] = sq;
+  }
+  __syncthreads();
+  const float sq_row = L.sq[rr];
+
+  float O[CPL];
+#pragma unroll
+  for (int e = 0; e < CPL; ++e) O[e] = 0.0f;
+  float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
+  if (bits == 4)
+    decode_groups<GP, 4>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row);
+  else
+    decode_groups<GP, 2>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row);
+
+  // ---- epilogue: lane (rr, cc) holds channels cc*CPL .. of row rr --------
+  const float l = row_sum<LPR>(lpart);
+  if (rr >= G) return;
+  const int h = kh * G + rr;
+  const int c0 = cc * CPL;
+  if (a.nsplit == 1) {
+    const bool empty = g1 <= g0;
+    const float f = beta / l;
+    _Float16* orow = reinterpret_cast<_Float16*>(a.o) + ((long)b * a.Hq + h) * 128 + c0;
+#pragma unroll
+    for (int e = 0; e < CPL; e += 2) {
+      _Float16 h2[2] = {empty ? (_Float16)0.0f : (_Float16)(O[e] * f),
+                        empty ? (_Float16)0.0f : (_Float16)(O[e + 1] * f)};
+      *reinterpret_cast<unsigned*>(orow + e) = __builtin_bit_cast(unsigned, h2);
+    }
+    if (a.lse && cc == 0) a.lse[(long)b * a.Hq + h] = empty ? -INFINITY : mrow + logf(l);
   } else {
     if (g1 <= g0) return;  // chunk beyond this sequence: never read by the merge
     float* w = a.ws + (((long)b * a.Hq + h) * a.nsplit + s) * kWsStride;
-    if (g4 == 0) {
+    if (cc == 0) {
       w[0] = mrow;
       w[1] = l;
     }
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb)
-      *reinterpret_cast<float4*>(w + kWsO + 16 * cb + 4 * g4) =
-          make_float4(O[cb][0], O[cb][1], O[cb][2], O[cb][3]);
+    for (int e = 0; e < CPL; ++e) w[kWsO + c0 + e] = O[e] * beta;
   }
 }
 
@@ -360,7 +510,14 @@ __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
 
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hkv * a.nsplit;
-  hipLaunchKernelGGL(k_attn_decode, dim3(total), dim3(64), 0, stream, a);
+  const int gp = a.G <= 1 ? 1 : a.G <= 2 ? 2 : a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
+  switch (gp) {
+    case 1: hipLaunchKernelGGL(k_attn_decode<1>, dim3(total), dim3(64), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(k_attn_decode<2>, dim3(total), dim3(64), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL(k_attn_decode<4>, dim3(total), dim3(64), 0, stream, a); break;
+    case 8: hipLaunchKernelGGL(k_attn_decode<8>, dim3(total), dim3(64), 0, stream, a); break;
+    default: hipLaunchKernelGGL(k_attn_decode<16>, dim3(total), dim3(64), 0, stream, a); break;
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsplit == 1) return e;
   hipLaunchKernelGGL(k_decode_combine, dim3(a.B * a.Hq), dim3(64), 0, stream, a);
