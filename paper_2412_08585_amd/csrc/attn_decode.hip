@@ -106,21 +106,90 @@ struct DecodeLds {
   float sq[16];
   int sbuf[GP][64];             // scores, row-major
   unsigned char pbuf[GP][64];   // Q(P~), per page in V-unpack order
-  int obuf[GP][128];            // PV accumulators
+  int obuf[128][GP];            // PV accumulators, channel-major
+  float4 rowv[GP];              // per row: g = s_P s_V / beta, sum Q(P~), renorm, -
 };
+
+// Everything one group needs from memory, loaded one group ahead.
+template <int BITS>
+struct GroupData {
+  bool ok;
+  const uint8_t* krow;          // K codes of this lane's A-operand rows (page m>>2)
+  const uint8_t* vreg;          // V codes of page g4
+  const int8_t* meta;
+  float skg, svg;
+  unsigned kraw[4][BITS];       // K codes of the 4 A-operand rows (32 channels each)
+  unsigned ks4[8], kz4[8];      // K scale / zero of the lane's 32 channels
+  unsigned vraw[8][BITS / 2];   // V codes of channel 16*cb + n in page g4
+  unsigned vsz;                 // V scale (low 16 bits) / zero (high) of channels 2L, 2L+1
+};
+
+template <int BITS>
+__device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head_off,
+                                           const int* bt, const int* gt, int g,
+                                           GroupData<BITS>& D) {
+  const int lane = threadIdx.x;
+  const int n = lane & 15, g4 = lane >> 4, m = lane & 15;
+  const long p0 = bt[4 * g], p1 = bt[4 * g + 1], p2 = bt[4 * g + 2], p3 = bt[4 * g + 3];
+  bool ok = p0 >= 0 && p0 < a.num_pages && p1 >= 0 && p1 < a.num_pages && p2 >= 0 &&
+            p2 < a.num_pages && p3 >= 0 && p3 < a.num_pages;
+  const long slot = gt[g];
+  ok = ok && slot >= 0 && slot < a.num_slots;
+  D.ok = ok;
+  if (!ok) return;  // caller error: this group is not read
+  D.meta = a.gmeta + (slot * a.Hkv + kh) * 512;
+  D.skg = a.gscale[(slot * a.Hkv + kh) * 2 + 0];
+  D.svg = a.gscale[(slot * a.Hkv + kh) * 2 + 1];
+  // lane-dependent page choice by selects (no dynamic indexing of an array)
+  const int pk = m >> 2;
+  const long pgk = pk == 0 ? p0 : pk == 1 ? p1 : pk == 2 ? p2 : p3;
+  const long pgv = g4 == 0 ? p0 : g4 == 1 ? p1 : g4 == 2 ? p2 : p3;
+  D.krow = a.pages + pgk * a.page_bytes + head_off + (m & 3) * 16 * BITS + 4 * BITS * g4;
+  D.vreg = a.pages + pgv * a.page_bytes + head_off + 256 * BITS;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+    const uint8_t* krow = D.krow + 4 * mb * 16 * BITS;
+    if (BITS == 4) {
+      const uint4 x = *reinterpret_cast<const uint4*>(krow);
+      D.kraw[mb][0] = x.x; D.kraw[mb][1] = x.y; D.kraw[mb][2] = x.z; D.kraw[mb][3] = x.w;
+    } else {
+      const uint2 x = *reinterpret_cast<const uint2*>(krow);
+      D.kraw[mb][0] = x.x; D.kraw[mb][1] = x.y;
+    }
+  }
+  {
+    const uint4* ms = reinterpret_cast<const uint4*>(D.meta + 32 * g4);
+    const uint4* mz = reinterpret_cast<const uint4*>(D.meta + 128 + 32 * g4);
+    const uint4 t0 = ms[0], t1 = ms[1], z0 = mz[0], z1 = mz[1];
+    D.ks4[0] = t0.x; D.ks4[1] = t0.y; D.ks4[2] = t0.z; D.ks4[3] = t0.w;
+    D.ks4[4] = t1.x; D.ks4[5] = t1.y; D.ks4[6] = t1.z; D.ks4[7] = t1.w;
+    D.kz4[0] = z0.x; D.kz4[1] = z0.y; D.kz4[2] = z0.z; D.kz4[3] = z0.w;
+    D.kz4[4] = z1.x; D.kz4[5] = z1.y; D.kz4[6] = z1.z; D.kz4[7] = z1.w;
+  }
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) {
+    const int ch = 16 * cb + n;
+    if (BITS == 4) {
+      const uint2 x = *reinterpret_cast<const uint2*>(D.vreg + ch * 8);
+      D.vraw[cb][0] = x.x; D.vraw[cb][1] = x.y;
+    } else {
+      D.vraw[cb][0] = *reinterpret_cast<const unsigned*>(D.vreg + ch * 4);
+    }
+  }
+  D.vsz = (unsigned)*reinterpret_cast<const unsigned short*>(D.meta + 256 + 2 * lane) |
+          ((unsigned)*reinterpret_cast<const unsigned short*>(D.meta + 384 + 2 * lane) << 16);
+}
 
 template <int GP, int BITS>
 __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>& L, int b, int kh,
                                               int g0, int g1, int head_off, const int (&q8w)[8],
                                               float& mrow, float& lpart, float& beta,
-                                              float (&O)[2 * GP], float sq_row) {
-  constexpr int LPR = 64 / GP;  // lanes per compact row
-  constexpr int CPL = 2 * GP;   // accumulator channels per lane
+                                              float (&O)[GP][2], float sq_row) {
+  constexpr int LPR = 64 / GP;  // lanes per compact softmax row
   constexpr int d = BITS == 4 ? 2 : 4;
   const int lane = threadIdx.x;
   const int n = lane & 15, g4 = lane >> 4;
   const int rr = lane / LPR, cc = lane % LPR;
-  const int m = lane & 15;
 
   // 16-bit (q_ca, q_cb) pairs in the order the K codes unpack to: B-operand
   // dword j of k-step ks covers channels c0 + {0, d, 2d, 3d}; pair xy = 0 is
@@ -143,233 +212,205 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   const int* bt = a.block_table + (long)b * 4 * a.max_groups;
   const int* gt = a.group_table + (long)b * a.max_groups;
 
+  GroupData<BITS> cur, nxt;
+  if (g0 < g1) load_group<BITS>(a, kh, head_off, bt, gt, g0, cur);
   for (int g = g0; g < g1; ++g) {
-    long pg[4];
-    bool ok = true;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      pg[p] = bt[4 * g + p];
-      ok = ok && pg[p] >= 0 && pg[p] < a.num_pages;
-    }
-    const long slot = gt[g];
-    ok = ok && slot >= 0 && slot < a.num_slots;
-    if (!ok) continue;  // caller error: this group is not read
-
-    const int8_t* meta = a.gmeta + (slot * a.Hkv + kh) * 512;
-    const float skg = a.gscale[(slot * a.Hkv + kh) * 2 + 0];
-    const float svg = a.gscale[(slot * a.Hkv + kh) * 2 + 1];
-
-    // ---- K codes of this lane: A-operand rows of the 4 m-blocks ---------
-    unsigned kraw[4][BITS];  // int4: 4 dwords (32 channels); int2: 2 dwords
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      const uint8_t* krow = a.pages + pg[m >> 2] * a.page_bytes + head_off +
-                            (4 * mb + (m & 3)) * 16 * BITS + 4 * BITS * g4;
-      if (BITS == 4) {
-        const uint4 x = *reinterpret_cast<const uint4*>(krow);
-        kraw[mb][0] = x.x; kraw[mb][1] = x.y; kraw[mb][2] = x.z; kraw[mb][3] = x.w;
-      } else {
-        const uint2 x = *reinterpret_cast<const uint2*>(krow);
-        kraw[mb][0] = x.x; kraw[mb][1] = x.y;
-      }
-    }
-    // ---- hi/lo B-operands from w = q * s^int (this lane's 32 channels) --
-    unsigned ks4[8], kz4[8];
-    {
-      const uint4* ms = reinterpret_cast<const uint4*>(meta + 32 * g4);
-      const uint4* mz = reinterpret_cast<const uint4*>(meta + 128 + 32 * g4);
-      const uint4 t0 = ms[0], t1 = ms[1], z0 = mz[0], z1 = mz[1];
-      ks4[0] = t0.x; ks4[1] = t0.y; ks4[2] = t0.z; ks4[3] = t0.w;
-      ks4[4] = t1.x; ks4[5] = t1.y; ks4[6] = t1.z; ks4[7] = t1.w;
-      kz4[0] = z0.x; kz4[1] = z0.y; kz4[2] = z0.z; kz4[3] = z0.w;
-      kz4[4] = z1.x; kz4[5] = z1.y; kz4[6] = z1.z; kz4[7] = z1.w;
-    }
-    v4i bhi[2], blo[2];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      int hw[4], lw[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int c0 = BITS == 4 ? 16 * ks + 8 * (j >> 1) + (j & 1) : 16 * ks + j;
-        unsigned hx[2], lx[2];
-#pragma unroll
-        for (int xy = 0; xy < 2; ++xy) {
-          const int ca = c0 + 2 * d * xy, cb = ca + d;
-          // bytes [s_ca, 0, s_cb, 0]: the 16-bit pair (s_ca, s_cb)
-          const unsigned selb = (cb >> 2) == (ca >> 2) ? (unsigned)(cb & 3) : 4u + (cb & 3);
-          const unsigned sel = (unsigned)(ca & 3) | (0x0cu << 8) | (selb << 16) | (0x0cu << 24);
-          const unsigned spair = __builtin_amdgcn_perm(ks4[cb >> 2], ks4[ca >> 2], sel);
-          const u16x2 w =
-              __builtin_bit_cast(u16x2, qpair[ks][j][xy]) * __builtin_bit_cast(u16x2, spair);
-          hx[xy] = __builtin_bit_cast(unsigned, __builtin_bit_cast(s16x2, w) >> (short)7);
-          lx[xy] = __builtin_bit_cast(unsigned, w) & 0x007F007Fu;
-        }
-        hw[j] = (int)__builtin_amdgcn_perm(hx[1], hx[0], 0x06040200u);
-        lw[j] = (int)__builtin_amdgcn_perm(lx[1], lx[0], 0x06040200u);
-      }
-      bhi[ks] = v4i{hw[0], hw[1], hw[2], hw[3]};
-      blo[ks] = v4i{lw[0], lw[1], lw[2], lw[3]};
-    }
-    // zero-point term sum_c q_c z_c over the lane's channels, then over g4
-    int bias = 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) bias = __builtin_amdgcn_sdot4(q8w[i], (int)kz4[i], bias, false);
-    bias = (int)add_xor32((float)bias);  // exact: |bias| < 2^24
-    {
-      const unsigned u = (unsigned)bias;
-      auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-      bias = (int)r[0] + (int)r[1];
-    }
-    // ---- S^T = K^{q1} q^T on the MFMA, scores to LDS -------------------
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      v4i kop[2];
-      if (BITS == 4) {
-        unsigned u[8];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          u[2 * w] = kraw[mb][w] & 0x0F0F0F0Fu;
-          u[2 * w + 1] = (kraw[mb][w] >> 4) & 0x0F0F0F0Fu;
-        }
-        kop[0] = v4i{(int)u[0], (int)u[1], (int)u[2], (int)u[3]};
-        kop[1] = v4i{(int)u[4], (int)u[5], (int)u[6], (int)u[7]};
-      } else {
-#pragma unroll
-        for (int w = 0; w < 2; ++w)
-          kop[w] = v4i{(int)(kraw[mb][w] & 0x03030303u), (int)((kraw[mb][w] >> 2) & 0x03030303u),
-                       (int)((kraw[mb][w] >> 4) & 0x03030303u),
-                       (int)((kraw[mb][w] >> 6) & 0x03030303u)};
-      }
-      v4i lo = v4i{bias, bias, bias, bias};
-      v4i hi = {};
+    if (g + 1 < g1) load_group<BITS>(a, kh, head_off, bt, gt, g + 1, nxt);
+    if (cur.ok) {
+      // ---- hi/lo B-operands from w = q * s^int (this lane's 32 channels)
+      v4i bhi[2], blo[2];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        lo = mfma16x16x64(kop[ks], blo[ks], lo);
-        hi = mfma16x16x64(kop[ks], bhi[ks], hi);
+        int hw[4], lw[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c0 = BITS == 4 ? 16 * ks + 8 * (j >> 1) + (j & 1) : 16 * ks + j;
+          unsigned hx[2], lx[2];
+#pragma unroll
+          for (int xy = 0; xy < 2; ++xy) {
+            const int ca = c0 + 2 * d * xy, cb = ca + d;
+            // bytes [s_ca, 0, s_cb, 0]: the 16-bit pair (s_ca, s_cb)
+            const unsigned selb = (cb >> 2) == (ca >> 2) ? (unsigned)(cb & 3) : 4u + (cb & 3);
+            const unsigned sel = (unsigned)(ca & 3) | (0x0cu << 8) | (selb << 16) | (0x0cu << 24);
+            const unsigned spair = __builtin_amdgcn_perm(cur.ks4[cb >> 2], cur.ks4[ca >> 2], sel);
+            const u16x2 w =
+                __builtin_bit_cast(u16x2, qpair[ks][j][xy]) * __builtin_bit_cast(u16x2, spair);
+            hx[xy] = __builtin_bit_cast(unsigned, __builtin_bit_cast(s16x2, w) >> (short)7);
+            lx[xy] = __builtin_bit_cast(unsigned, w) & 0x007F007Fu;
+          }
+          hw[j] = (int)__builtin_amdgcn_perm(hx[1], hx[0], 0x06040200u);
+          lw[j] = (int)__builtin_amdgcn_perm(lx[1], lx[0], 0x06040200u);
+        }
+        bhi[ks] = v4i{hw[0], hw[1], hw[2], hw[3]};
+        blo[ks] = v4i{lw[0], lw[1], lw[2], lw[3]};
+      }
+      // zero-point term sum_c q_c z_c over the lane's channels, then over g4
+      int bias = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) bias = __builtin_amdgcn_sdot4(q8w[i], (int)cur.kz4[i], bias, false);
+      bias = (int)add_xor32((float)bias);  // exact: |bias| < 2^24
+      {
+        const unsigned u = (unsigned)bias;
+        auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        bias = (int)r[0] + (int)r[1];
+      }
+      // ---- S^T = K^{q1} q^T on the MFMA, scores to LDS -----------------
+      int4 sv[4];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        v4i kop[2];
+        if (BITS == 4) {
+          unsigned u[8];
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            u[2 * w] = cur.kraw[mb][w] & 0x0F0F0F0Fu;
+            u[2 * w + 1] = (cur.kraw[mb][w] >> 4) & 0x0F0F0F0Fu;
+          }
+          kop[0] = v4i{(int)u[0], (int)u[1], (int)u[2], (int)u[3]};
+          kop[1] = v4i{(int)u[4], (int)u[5], (int)u[6], (int)u[7]};
+        } else {
+#pragma unroll
+          for (int w = 0; w < 2; ++w)
+            kop[w] = v4i{(int)(cur.kraw[mb][w] & 0x03030303u),
+                         (int)((cur.kraw[mb][w] >> 2) & 0x03030303u),
+                         (int)((cur.kraw[mb][w] >> 4) & 0x03030303u),
+                         (int)((cur.kraw[mb][w] >> 6) & 0x03030303u)};
+        }
+        v4i lo = v4i{bias, bias, bias, bias};
+        v4i hi = {};
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          lo = mfma16x16x64(kop[ks], blo[ks], lo);
+          hi = mfma16x16x64(kop[ks], bhi[ks], hi);
+        }
+        sv[mb] = make_int4((hi[0] << 7) + lo[0], (hi[1] << 7) + lo[1], (hi[2] << 7) + lo[2],
+                           (hi[3] << 7) + lo[3]);
       }
       if (n < GP) {
-        const int4 sv = make_int4((hi[0] << 7) + lo[0], (hi[1] << 7) + lo[1], (hi[2] << 7) + lo[2],
-                                  (hi[3] << 7) + lo[3]);
-        *reinterpret_cast<int4*>(&L.sbuf[n][16 * g4 + 4 * mb]) = sv;
-      }
-    }
-    __syncthreads();
-    // ---- compact softmax: lane (rr, cc) holds tokens cc*GP .. +GP-1 -------
-    float gsc;  // s_P s_V / beta of the row
-    int psum;   // sum of the row's Q(P~)
-    {
-      int si[GP];
-      if (GP >= 4) {
 #pragma unroll
-        for (int e = 0; e < GP; e += 4) {
-          const int4 t = *reinterpret_cast<const int4*>(&L.sbuf[rr][cc * GP + e]);
-          si[e] = t.x; si[e + 1] = t.y; si[e + 2] = t.z; si[e + 3] = t.w;
+        for (int mb = 0; mb < 4; ++mb)
+          *reinterpret_cast<int4*>(&L.sbuf[n < GP ? n : 0][16 * g4 + 4 * mb]) = sv[mb];
+      }
+      __syncthreads();
+      // ---- compact softmax: lane (rr, cc) holds tokens cc*GP .. +GP-1 -----
+      bool renorm;
+      {
+        int si[GP];
+        if (GP >= 4) {
+#pragma unroll
+          for (int e = 0; e < GP; e += 4) {
+            const int4 t = *reinterpret_cast<const int4*>(&L.sbuf[rr][cc * GP + e]);
+            si[e] = t.x; si[e + 1] = t.y; si[e + 2] = t.z; si[e + 3] = t.w;
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < GP; ++e) si[e] = L.sbuf[rr][cc * GP + e];
         }
-      } else {
+        const float c = (sq_row * cur.skg) * a.sm_scale;
+        float p[GP];
+        float smax = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < GP; ++e) si[e] = L.sbuf[rr][cc * GP + e];
-      }
-      const float c = (sq_row * skg) * a.sm_scale;
-      float p[GP];
-      float smax = -INFINITY;
-#pragma unroll
-      for (int e = 0; e < GP; ++e) {
-        p[e] = (float)si[e] * c;
-        smax = fmaxf(smax, p[e]);
-      }
-      smax = row_max<LPR>(smax);
-      const float mnew = fmaxf(mrow, smax);
-      float rs = 0.0f, pmax = 0.0f;
-#pragma unroll
-      for (int e = 0; e < GP; ++e) {
-        p[e] = sas_y(mnew - p[e], L.lut);
-        rs += p[e];
-        pmax = fmaxf(pmax, p[e]);
-      }
-      const float alpha = sas_y(mnew - mrow, L.lut);  // 0 when mrow = -inf
-      lpart = alpha * lpart + rs;
-      mrow = mnew;
-      pmax = row_max<LPR>(pmax);
-      // rescale: O = beta * Ost
-      float nbeta = beta * alpha;
-      if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
-#pragma unroll
-        for (int e = 0; e < CPL; ++e) O[e] *= nbeta;
-        nbeta = 1.0f;
-      }
-      beta = nbeta;
-      // Q(P~) with the row's scale pmax/119 (a row whose group lies wholly
-      // below the threshold has pmax = 0: inv = 0, Q(P~) = 0, adds nothing)
-      const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
-      int ps = 0;
-#pragma unroll
-      for (int e = 0; e < GP; ++e) {
-        const int code = rne_bits(p[e], inv) & 0xff;
-        ps += code;
-        const int t = cc * GP + e;  // token of the group
-        L.pbuf[rr][16 * (t >> 4) + vpos<BITS>(t & 15)] = (unsigned char)code;
-      }
-      psum = (int)row_sum<LPR>((float)ps);  // exact: < 2^24
-      gsc = ((pmax / kQmax) * svg) * __builtin_amdgcn_rcpf(beta);
-    }
-    __syncthreads();
-    // ---- O = Q(P~) V on the raw codes (A = P rows, B = V codes) ---------
-    const v4i pop = n < GP ? *reinterpret_cast<const v4i*>(&L.pbuf[n < GP ? n : 0][16 * g4])
-                           : v4i{0, 0, 0, 0};
-    const uint8_t* vreg = a.pages + pg[g4] * a.page_bytes + head_off + 256 * BITS;
-#pragma unroll
-    for (int cb = 0; cb < 8; ++cb) {
-      const int ch = 16 * cb + n;  // B-operand column (channel) of this lane
-      v4i vop;
-      if (BITS == 4) {
-        const uint2 x = *reinterpret_cast<const uint2*>(vreg + ch * 8);
-        vop = v4i{(int)(x.x & 0x0F0F0F0Fu), (int)((x.x >> 4) & 0x0F0F0F0Fu),
-                  (int)(x.y & 0x0F0F0F0Fu), (int)((x.y >> 4) & 0x0F0F0F0Fu)};
-      } else {
-        const unsigned x = *reinterpret_cast<const unsigned*>(vreg + ch * 4);
-        vop = v4i{(int)(x & 0x03030303u), (int)((x >> 2) & 0x03030303u),
-                  (int)((x >> 4) & 0x03030303u), (int)((x >> 6) & 0x03030303u)};
-      }
-      v4i acc = {};
-      acc = mfma16x16x64(pop, vop, acc);
-      // lane (n, g4), register r <-> row 4*g4 + r, channel 16*cb + n
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (4 * g4 + r < GP) L.obuf[4 * g4 + r < GP ? 4 * g4 + r : 0][16 * cb + n] = acc[r];
-    }
-    __syncthreads();
-    // ---- accumulator update in the compact layout -----------------------
-    {
-      const int c0 = cc * CPL;
-      int acc[CPL];
-      unsigned vsw, vzw;  // CPL <= 4: bytes of one dword
-      if (CPL >= 4) {
-#pragma unroll
-        for (int e = 0; e < CPL; e += 4) {
-          const int4 t = *reinterpret_cast<const int4*>(&L.obuf[rr][c0 + e]);
-          acc[e] = t.x; acc[e + 1] = t.y; acc[e + 2] = t.z; acc[e + 3] = t.w;
+        for (int e = 0; e < GP; ++e) {
+          p[e] = (float)si[e] * c;
+          smax = fmaxf(smax, p[e]);
         }
-      } else {
-        const int2 t = *reinterpret_cast<const int2*>(&L.obuf[rr][c0]);
-        acc[0] = t.x; acc[CPL > 1 ? 1 : 0] = t.y;
-      }
+        smax = row_max<LPR>(smax);
+        const float mnew = fmaxf(mrow, smax);
+        float rs = 0.0f, pmax = 0.0f;
 #pragma unroll
-      for (int e = 0; e < CPL; ++e) {
-        if ((e & 3) == 0) {
-          if (CPL >= 4) {
-            vsw = *reinterpret_cast<const unsigned*>(meta + 256 + c0 + e);
-            vzw = *reinterpret_cast<const unsigned*>(meta + 384 + c0 + e);
+        for (int e = 0; e < GP; ++e) {
+          p[e] = sas_y(mnew - p[e], L.lut);
+          rs += p[e];
+          pmax = fmaxf(pmax, p[e]);
+        }
+        const float alpha = sas_y(mnew - mrow, L.lut);  // 0 when mrow = -inf
+        lpart = alpha * lpart + rs;
+        mrow = mnew;
+        pmax = row_max<LPR>(pmax);
+        // rescale: O = beta * Ost; renormalize when beta underflows / is 0
+        float nbeta = beta * alpha;
+        renorm = __builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0;
+        const float rf = renorm ? nbeta : 1.0f;
+        if (renorm) nbeta = 1.0f;
+        beta = nbeta;
+        // Q(P~) with the row's scale pmax/119 (a row whose group lies wholly
+        // below the threshold has pmax = 0: inv = 0, Q(P~) = 0, adds nothing)
+        const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
+        int ps = 0;
+#pragma unroll
+        for (int e = 0; e < GP; ++e) {
+          const int code = rne_bits(p[e], inv) & 0xff;
+          ps += code;
+          const int t = cc * GP + e;  // token of the group
+          L.pbuf[rr][16 * (t >> 4) + vpos<BITS>(t & 15)] = (unsigned char)code;
+        }
+        const int psum = (int)row_sum<LPR>((float)ps);  // exact: < 2^24
+        const float gsc = ((pmax / kQmax) * cur.svg) * __builtin_amdgcn_rcpf(beta);
+        if (cc == 0) L.rowv[rr] = make_float4(gsc, __int_as_float(psum), rf, 0.0f);
+      }
+      __syncthreads();
+      // ---- O = Q(P~) V on the raw codes (A = P rows, B = V codes) -------
+      const v4i pop = n < GP ? *reinterpret_cast<const v4i*>(&L.pbuf[n < GP ? n : 0][16 * g4])
+                             : v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) {
+        v4i vop;
+        if (BITS == 4) {
+          const unsigned x0 = cur.vraw[cb][0], x1 = cur.vraw[cb][BITS / 2 - 1];
+          vop = v4i{(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
+                    (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+        } else {
+          const unsigned x = cur.vraw[cb][0];
+          vop = v4i{(int)(x & 0x03030303u), (int)((x >> 2) & 0x03030303u),
+                    (int)((x >> 4) & 0x03030303u), (int)((x >> 6) & 0x03030303u)};
+        }
+        v4i acc = {};
+        acc = mfma16x16x64(pop, vop, acc);
+        // lane (n, g4), register r <-> row 4*g4 + r, channel 16*cb + n
+        if (GP >= 4) {
+          if (4 * g4 < GP)
+            *reinterpret_cast<int4*>(&L.obuf[16 * cb + n][4 * g4 < GP ? 4 * g4 : 0]) =
+                make_int4(acc[0], acc[1], acc[2], acc[3]);
+        } else if (g4 == 0) {
+#pragma unroll
+          for (int r = 0; r < GP; ++r) L.obuf[16 * cb + n][r] = acc[r];
+        }
+      }
+      __syncthreads();
+      // ---- accumulator update: lane L owns channels 2L, 2L+1 of all rows --
+      {
+        int acc[2][GP];
+#pragma unroll
+        for (int c2 = 0; c2 < 2; ++c2) {
+          if (GP >= 4) {
+#pragma unroll
+            for (int r = 0; r < GP; r += 4) {
+              const int4 t = *reinterpret_cast<const int4*>(&L.obuf[2 * lane + c2][r]);
+              acc[c2][r] = t.x; acc[c2][r + 1] = t.y; acc[c2][r + 2] = t.z; acc[c2][r + 3] = t.w;
+            }
           } else {
-            vsw = *reinterpret_cast<const unsigned short*>(meta + 256 + c0);
-            vzw = *reinterpret_cast<const unsigned short*>(meta + 384 + c0);
+#pragma unroll
+            for (int r = 0; r < GP; ++r) acc[c2][r] = L.obuf[2 * lane + c2][r];
           }
         }
-        const int s_c = (int)((vsw >> (8 * (e & 3))) & 0xffu);
-        const int z_c = (int)(int8_t)((vzw >> (8 * (e & 3))) & 0xffu);
-        const int pv = s_c * acc[e] + z_c * psum;  // exact int32 PV of Algorithm 2
-        O[e] = __builtin_fmaf(gsc, (float)pv, O[e]);
+        const int s0 = (int)(cur.vsz & 0xffu), s1 = (int)((cur.vsz >> 8) & 0xffu);
+        const int z0 = (int)(int8_t)((cur.vsz >> 16) & 0xffu);
+        const int z1 = (int)(int8_t)((cur.vsz >> 24) & 0xffu);
+#pragma unroll
+        for (int r = 0; r < GP; ++r) {
+          const float4 rv = L.rowv[r];
+          const int psum = __float_as_int(rv.y);
+          if (renorm) {
+            O[r][0] *= rv.z;
+            O[r][1] *= rv.z;
+          }
+          // exact int32 PV of Algorithm 2: s * sum P*code + z * sum P
+          O[r][0] = __builtin_fmaf(rv.x, (float)(s0 * acc[0][r] + z0 * psum), O[r][0]);
+          O[r][1] = __builtin_fmaf(rv.x, (float)(s1 * acc[1][r] + z1 * psum), O[r][1]);
+        }
       }
     }
+    cur = nxt;
   }
 }
 
@@ -377,7 +418,6 @@ template <int GP>
 __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
   __shared__ DecodeLds<GP> L;
   constexpr int LPR = 64 / GP;
-  constexpr int CPL = 2 * GP;
   const int lane = threadIdx.x;
   if (lane < 8) L.lut[lane] = kLut[lane];
 
@@ -432,40 +472,48 @@ __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
   __syncthreads();
   const float sq_row = L.sq[rr];
 
-  float O[CPL];
+  float O[GP][2];
 #pragma unroll
-  for (int e = 0; e < CPL; ++e) O[e] = 0.0f;
+  for (int r = 0; r < GP; ++r) O[r][0] = O[r][1] = 0.0f;
   float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
   if (bits == 4)
     decode_groups<GP, 4>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row);
   else
     decode_groups<GP, 2>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row);
 
-  // ---- epilogue: lane (rr, cc) holds channels cc*CPL .. of row rr --------
+  // ---- epilogue: per-row (m, l, beta) from the softmax lanes -------------
   const float l = row_sum<LPR>(lpart);
-  if (rr >= G) return;
-  const int h = kh * G + rr;
-  const int c0 = cc * CPL;
+  __syncthreads();
+  if (cc == 0) L.rowv[rr] = make_float4(mrow, l, beta, 0.0f);
+  __syncthreads();
+  const bool empty = g1 <= g0;
   if (a.nsplit == 1) {
-    const bool empty = g1 <= g0;
-    const float f = beta / l;
-    _Float16* orow = reinterpret_cast<_Float16*>(a.o) + ((long)b * a.Hq + h) * 128 + c0;
 #pragma unroll
-    for (int e = 0; e < CPL; e += 2) {
-      _Float16 h2[2] = {empty ? (_Float16)0.0f : (_Float16)(O[e] * f),
-                        empty ? (_Float16)0.0f : (_Float16)(O[e + 1] * f)};
-      *reinterpret_cast<unsigned*>(orow + e) = __builtin_bit_cast(unsigned, h2);
+    for (int r = 0; r < GP; ++r) {
+      if (r >= G) break;
+      const float4 rv = L.rowv[r];
+      const float f = rv.z / rv.y;
+      _Float16 h2[2] = {empty ? (_Float16)0.0f : (_Float16)(O[r][0] * f),
+                        empty ? (_Float16)0.0f : (_Float16)(O[r][1] * f)};
+      reinterpret_cast<unsigned*>(a.o)[((long)b * a.Hq + kh * G + r) * 64 + lane] =
+          __builtin_bit_cast(unsigned, h2);
     }
-    if (a.lse && cc == 0) a.lse[(long)b * a.Hq + h] = empty ? -INFINITY : mrow + logf(l);
+    if (a.lse && cc == 0 && rr < G)
+      a.lse[(long)b * a.Hq + kh * G + rr] = empty ? -INFINITY : mrow + logf(l);
   } else {
-    if (g1 <= g0) return;  // chunk beyond this sequence: never read by the merge
-    float* w = a.ws + (((long)b * a.Hq + h) * a.nsplit + s) * kWsStride;
-    if (cc == 0) {
+    if (empty) return;  // chunk beyond this sequence: never read by the merge
+#pragma unroll
+    for (int r = 0; r < GP; ++r) {
+      if (r >= G) break;
+      const float be = L.rowv[r].z;
+      float* w = a.ws + (((long)b * a.Hq + kh * G + r) * a.nsplit + s) * kWsStride;
+      *reinterpret_cast<float2*>(w + kWsO + 2 * lane) = make_float2(O[r][0] * be, O[r][1] * be);
+    }
+    if (cc == 0 && rr < G) {
+      float* w = a.ws + (((long)b * a.Hq + kh * G + rr) * a.nsplit + s) * kWsStride;
       w[0] = mrow;
       w[1] = l;
     }
-#pragma unroll
-    for (int e = 0; e < CPL; ++e) w[kWsO + c0 + e] = O[e] * beta;
   }
 }
 
