@@ -32,6 +32,29 @@ PEAK_INT8_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, 8 TB/s
 
 
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary (profiles/traffic.txt), or None if the kernel's sources changed
+    since the counters were taken."""
+    import hashlib
+    srcs = {"k_attn_prefill": ["paper_2412_08585_amd/csrc/attn_prefill.hip",
+                               "paper_2412_08585_amd/csrc/turbo_common.h",
+                               "paper_2412_08585_amd/build.py"]}.get(kernel)
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    if not srcs or not os.path.exists(path):
+        return None
+    m = hashlib.sha256()
+    for f in srcs:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            m.update(fh.read())
+    digest = m.hexdigest()[:16]
+    for line in open(path):
+        parts = line.split()
+        if len(parts) == 4 and parts[0] == kernel and parts[1] == workload and parts[2] == digest:
+            return float(parts[3])
+    return None
+
+
 def decode_bytes_per_token(bits: int) -> float:
     """Compressed K+V bytes read per cached token and KV head: codes plus the
     per-channel integer scale/zero (4 x 128 B per 64-token group) plus the
@@ -47,8 +70,10 @@ def parse():
     ap.add_argument("--workload", default="phi3m-prefill-4k")
     ap.add_argument("--kernel-iters", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["quantize", "prefill", "decode"], default=None,
-                    help="launch only this kernel --steps times (for profiler passes)")
+    ap.add_argument("--only", choices=["quantize", "prefill", "decode", "copy"], default=None,
+                    help="launch only this kernel --steps times (for profiler passes); "
+                         "'copy' runs a plain 1 GiB device copy (calibration of the HBM "
+                         "byte counters)")
     return ap.parse_args()
 
 
@@ -65,6 +90,16 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only == "copy":
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": "copy", "bytes_read": src.numel() * 4,
+                          "bytes_written": dst.numel() * 4,
+                          "launches": args.warmup + args.steps}))
+        return
     w = W.WORKLOADS[args.workload]
     if w.kind == "decode":
         return bench_decode(args, w)
@@ -182,7 +217,7 @@ def main():
         "roofline": {"kernel": "k_attn_prefill", "bound": "mfma",
                      "achieved": round(prefill_tops, 2), "peak": PEAK_INT8_TOPS,
                      "unit": "TOP/s", "frac": round(prefill_tops / PEAK_INT8_TOPS, 4),
-                     "traffic": None,
+                     "traffic": measured_traffic("k_attn_prefill", w.name),
                      "per_launch_ops": prefill_ops},
     }
 
