@@ -42,6 +42,20 @@ struct PrefillArgs {
 
 constexpr int kPrefillWaves = 2;
 
+// Logical work-group order L: longest causal query blocks first, and within
+// a query block the G query heads of one KV head next to each other.  The
+// dispatcher hands work-group x to XCD x % 8, so XCD k is given the units
+// k, k + 8, k + 16, ... of G consecutive L: every XCD receives the same mix
+// of row lengths (a contiguous split would leave one XCD with all the long
+// rows) and the G heads reading the same K/V tiles run together on one
+// XCD's L2.  Falls back to L = x (still interleaved) when 8G does not divide
+// the grid.
+__device__ __forceinline__ int prefill_order(int x, int total, int G) {
+  if (total % (8 * G) != 0) return x;
+  const int k = x % 8, n = x / 8;
+  return (8 * (n / G) + k) * G + n % G;
+}
+
 __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillArgs a) {
   __shared__ float lut[8];
   __shared__ float xmax[2][kPrefillWaves];  // per-wave P maxima, double-buffered
@@ -51,7 +65,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
   __syncthreads();
 
   const int BH = a.B * a.Hq;
-  const int L = xcd_remap(blockIdx.x, BH * a.nb);
+  const int L = prefill_order(blockIdx.x, BH * a.nb, a.Hq / a.Hkv);
   const int i = a.nb - 1 - L / BH;  // longest causal rows first
   const int b = (L % BH) / a.Hq, h = L % a.Hq;
   const int G = a.Hq / a.Hkv, kh = h / G;

@@ -149,15 +149,4 @@ __device__ __forceinline__ int pack4(int a, int b, int c, int d) {
   return (a & 0xff) | ((b & 0xff) << 8) | ((c & 0xff) << 16) | ((int)((unsigned)d << 24));
 }
 
-// XCD-aware remap of a 1-D workgroup id: the hardware hands consecutive
-// workgroup ids to the 8 XCDs round-robin; this returns a logical index such
-// that each XCD works on a contiguous range of logical indices (so logically
-// neighbouring tiles share that XCD's L2).
-__device__ __forceinline__ int xcd_remap(int wg, int total) {
-  constexpr int kXcd = 8;
-  const int per = total / kXcd, rem = total % kXcd;
-  const int x = wg % kXcd, i = wg / kXcd;
-  return x * per + min(x, rem) + i;
-}
-
 }  // namespace turbo
