@@ -196,7 +196,8 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
  *                 is out of range is skipped (its memory is never read).
  * B, Hq           Hq % Hkv == 0, Hq / Hkv <= 16.
  * kv_split_groups groups per chunk, >= 1; 0 selects
- *                 turbo_decode_auto_split(B, Hq / Hkv ... ) (see below).
+ *                 turbo_decode_auto_split(B, Hkv, max_groups_per_seq) with
+ *                 Hkv = cache->num_kv_heads (see below).
  * workspace       device scratch of at least turbo_decode_workspace_bytes()
  *                 bytes (may be NULL when that is 0).
  * o               fp16 [B][Hq][128];  lse fp32 [B][Hq] or NULL.
@@ -208,13 +209,18 @@ int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t*
                       hipStream_t stream);
 
 /* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
- * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq. */
+ * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq.  It
+ * minimizes ceil(B*Hkv*chunks / 2048) * (chunk length + 2), the number of
+ * rounds of resident decode waves (two per SIMD on 256 CUs) times a wave's
+ * run time in group steps, preferring longer chunks on ties.  Since the
+ * chunked result merges SAS-weighted partial states, the output depends on
+ * the chunk length; pass an explicit kv_split_groups for results that do not
+ * depend on the batch shape. */
 int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq);
 
 /* Workspace bytes turbo_attn_decode needs for these arguments (0 when every
- * sequence fits one chunk).  kv_split_groups = 0 means the automatic value
- * for Hkv = Hq (an upper bound for any Hkv dividing Hq is obtained by
- * passing the explicit split). */
+ * sequence fits one chunk).  kv_split_groups = 0 means
+ * turbo_decode_auto_split(B, Hkv, max_groups_per_seq). */
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
                                     int kv_split_groups);
 

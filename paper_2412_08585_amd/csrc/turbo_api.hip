@@ -146,12 +146,26 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
 
 int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {
   if (B < 1 || Hkv < 1 || max_groups_per_seq < 1) return 1;
-  // aim at >= 4096 waves (16 per CU on 256 CUs) of streaming work
-  const long units = (long)B * Hkv;
-  long nsplit = (4096 + units - 1) / units;
-  if (nsplit > max_groups_per_seq) nsplit = max_groups_per_seq;
-  if (nsplit < 1) nsplit = 1;
-  return (int)((max_groups_per_seq + nsplit - 1) / nsplit);
+  // One wave per (sequence, KV head, chunk); every decode kernel variant holds
+  // two waves per SIMD, 2048 on the 256 CUs of gfx950.  A wave's run time is
+  // set by its per-group latency chain rather than by its bytes (int2 and int4
+  // chunks take the same time), about (groups + 2) group steps with the
+  // prologue and epilogue.  So take the chunk length minimizing
+  //   ceil(waves / 2048) * (chunk + 2),
+  // the longest chunk on ties (fewer partial states to merge).
+  constexpr long kSlots = 2048;
+  const long units = (long)B * Hkv, G = max_groups_per_seq;
+  long best_split = G, best_cost = -1;
+  for (long split = G; split >= 1; --split) {
+    const long n = (G + split - 1) / split;
+    const long rounds = (units * n + kSlots - 1) / kSlots;
+    const long cost = rounds * (split + 2);
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best_split = split;
+    }
+  }
+  return (int)best_split;
 }
 
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,

@@ -102,9 +102,23 @@ def test_invalid_arguments_rejected_before_launch(ta):
 
 def test_decode_split_and_workspace(ta):
     L = ta.lib()
-    assert L.turbo_decode_auto_split(64, 10, 128) == 19       # ceil(4096/640)=7 chunks
-    assert L.turbo_decode_auto_split(256, 8, 512) == 256      # 2 chunks
-    assert L.turbo_decode_auto_split(4096, 8, 4) == 4         # one chunk
+    # chunk minimizing ceil(waves / 2048) * (chunk + 2), longest on ties
+    assert L.turbo_decode_auto_split(64, 10, 128) == 43       # 3 chunks: 1920 waves, one round
+    assert L.turbo_decode_auto_split(256, 8, 512) == 512      # 2048 waves unsplit, one round
+    assert L.turbo_decode_auto_split(4096, 8, 4) == 4         # one chunk (16 rounds either way)
+    assert L.turbo_decode_auto_split(4, 10, 64) == 2          # 32 chunks: 1280 waves
+    assert L.turbo_decode_auto_split(1, 1, 1) == 1
+
+    def brute(B, Hkv, G):
+        best = None
+        for split in range(G, 0, -1):
+            n = -(-G // split)
+            cost = -(-(B * Hkv * n) // 2048) * (split + 2)
+            if best is None or cost < best[0]:
+                best = (cost, split)
+        return best[1]
+    for B, Hkv, G in [(1, 8, 256), (8, 8, 128), (32, 4, 300), (128, 16, 64), (3, 5, 7)]:
+        assert L.turbo_decode_auto_split(B, Hkv, G) == brute(B, Hkv, G)
     assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10) == 0
     assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3) == 4 * 8 * 4 * 132 * 4
 
