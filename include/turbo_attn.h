@@ -52,6 +52,15 @@ extern "C" {
 #define TURBO_MAX_KV_HEADS 64
 #define TURBO_MAX_GQA 16         /* max query heads per KV head */
 
+/* Layout of the tile trace written by the *_trace test hooks (bytes): */
+#define TURBO_TRACE_Q8 0         /* int8  [64][128]  Q^{q1} rows of the block  */
+#define TURBO_TRACE_S 8192       /* int32 [64][64]   QK^T accumulators         */
+#define TURBO_TRACE_P 24576      /* int8  [64][64]   Q(P~) codes               */
+#define TURBO_TRACE_PV 28672     /* int32 [64][128]  PV accumulators           */
+#define TURBO_TRACE_SQ 61440     /* fp32             s_Q                       */
+#define TURBO_TRACE_PMAX 61444   /* fp32             max P~ behind the P scale */
+#define TURBO_TRACE_BYTES 61448
+
 typedef enum turbo_status {
   TURBO_OK = 0,
   TURBO_ERR_INVALID_ARG = -1,         /* null pointer, bad shape, bad bits */
@@ -171,6 +180,26 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
                        int causal, void* o, float* lse, hipStream_t stream);
 
 /*
+ * Test hook (not part of the method): turbo_attn_prefill with the integers of
+ * one (sequence tb, query head th, query block ti, key block tj) tile written
+ * to `trace` (device, TURBO_TRACE_BYTES, layout above).  The same kernel runs;
+ * the selected tile additionally stores
+ *   Q8[r][c]   int8 Q code of query 64*ti + r, channel c (rows past N are 0);
+ *   S[r][t]    int32 sum_c Q8[r][c] * K8[64*tj + t][c] for every (r, t) of
+ *              the tile, masked entries included (they are excluded from the
+ *              softmax, not from the product);
+ *   P[r][t]    Q(P~) code (0 where masked);
+ *   PV[r][c]   int32 sum_t P[r][t] * V8[64*tj + t][c];
+ *   SQ, PMAX   s_Q of the block and the tile maximum of P~.
+ * Nothing is written when tj is not processed for ti (tj > ti when causal).
+ * INVALID_ARG also when trace is NULL or an index is out of range.
+ */
+int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
+                             const float* s_k, const float* s_v, int B, int Hq, int Hkv, int N,
+                             int d, float sm_scale, int causal, void* o, float* lse, int tb,
+                             int th, int ti, int tj, void* trace, hipStream_t stream);
+
+/*
  * turbo_attn_decode — Algorithm 2 (TurboAttention decode): the new query of
  * each sequence is quantized to int8 per (b, query head); every cached
  * 64-token group is expanded from int4/int2 to int8 in the kernel with
@@ -207,6 +236,25 @@ int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t*
                       int max_groups_per_seq, int B, int Hq, float sm_scale, int kv_split_groups,
                       void* workspace, size_t workspace_bytes, void* o, float* lse,
                       hipStream_t stream);
+
+/*
+ * Test hook (not part of the method): turbo_attn_decode with the integers of
+ * group tg of (sequence tb, query head th) written to `trace` (device,
+ * TURBO_TRACE_BYTES, layout above; row 0 of each array is used):
+ *   Q8[0][c]   int8 code of the query;
+ *   S[0][t]    int32 sum_c Q8[c] * K^{q1}[t][c] with K^{q1} = code*s^int + z^int;
+ *   P[0][t]    Q(P~) code of token t;
+ *   PV[0][c]   int32 sum_t P[t] * V^{q1}[t][c];
+ *   SQ, PMAX   s_Q and the group's maximum of P~.
+ * Nothing is written when group tg is not attended (tg >= seq_len/64 or a
+ * table entry out of range).  INVALID_ARG also when trace is NULL or an index
+ * is out of range.
+ */
+int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+                            const int32_t* block_table, const int32_t* group_table,
+                            int max_groups_per_seq, int B, int Hq, float sm_scale,
+                            int kv_split_groups, void* workspace, size_t workspace_bytes, void* o,
+                            float* lse, int tb, int th, int tg, void* trace, hipStream_t stream);
 
 /* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
  * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq.  It

@@ -18,6 +18,9 @@ HEAD_DIM = 128
 BLOCK = 64
 PAGE_TOKENS = 16
 MAX_KV_HEADS = 64
+# tile trace layout of the *_trace test hooks (include/turbo_attn.h)
+TRACE_Q8, TRACE_S, TRACE_P, TRACE_PV, TRACE_SQ, TRACE_PMAX, TRACE_BYTES = (
+    0, 8192, 24576, 28672, 61440, 61444, 61448)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libturboattn.so")
@@ -50,6 +53,10 @@ def lib() -> ctypes.CDLL:
             "turbo_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, I, P], I),
             "turbo_attn_prefill": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
             "turbo_attn_decode": ([P, P, P, P, P, I, I, I, F, I, P, Z, P, P, P], I),
+            "turbo_attn_prefill_trace": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, I, I, I, I, P,
+                                          P], I),
+            "turbo_attn_decode_trace": ([P, P, P, P, P, I, I, I, F, I, P, Z, P, P, I, I, I, P, P],
+                                        I),
             "turbo_decode_auto_split": ([I, I, I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I], Z),
         }
@@ -154,6 +161,38 @@ def turbo_attn_prefill(q: torch.Tensor, k8, v8, s_k, s_v, sm_scale: Optional[flo
     return (o, lse) if return_lse else o
 
 
+def _trace_buffer(device) -> torch.Tensor:
+    return torch.zeros(TRACE_BYTES, dtype=torch.uint8, device=device)
+
+
+def _trace_dict(buf: torch.Tensor) -> dict:
+    h = buf.cpu().numpy()
+    return dict(q8=h[TRACE_Q8:TRACE_S].view(np.int8).reshape(64, HEAD_DIM).copy(),
+                sacc=h[TRACE_S:TRACE_P].view(np.int32).reshape(64, 64).copy(),
+                qp=h[TRACE_P:TRACE_PV].view(np.int8).reshape(64, 64).copy(),
+                pvacc=h[TRACE_PV:TRACE_SQ].view(np.int32).reshape(64, HEAD_DIM).copy(),
+                sq=h[TRACE_SQ:TRACE_PMAX].view(np.float32)[0],
+                pmax=h[TRACE_PMAX:TRACE_BYTES].view(np.float32)[0])
+
+
+def turbo_attn_prefill_trace(q: torch.Tensor, k8, v8, s_k, s_v, tile, sm_scale=None,
+                             causal: bool = True):
+    """Test hook: turbo_attn_prefill that also returns the integers of tile
+    (b, h, i, j) as a dict of numpy arrays (q8, sacc, qp, pvacc, sq, pmax)."""
+    B, Hq, N, d = q.shape
+    Hkv = s_k.shape[1]
+    sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
+    o = torch.empty_like(q)
+    buf = _trace_buffer(q.device)
+    b, h, i, j = tile
+    st = lib().turbo_attn_prefill_trace(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B, Hq,
+                                        Hkv, N, d, sm, int(bool(causal)), _ptr(o), None, b, h, i,
+                                        j, _ptr(buf), _stream(q.device))
+    _check(st, "turbo_attn_prefill_trace")
+    torch.cuda.synchronize(q.device)
+    return o, _trace_dict(buf)
+
+
 def decode_split(B: int, Hkv: int, max_groups: int, kv_split_groups: int = 0) -> int:
     return kv_split_groups or int(lib().turbo_decode_auto_split(B, Hkv, max_groups))
 
@@ -186,3 +225,26 @@ def turbo_attn_decode(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tens
                                  _ptr(workspace), wbytes, _ptr(o), _ptr(lse), _stream(q.device))
     _check(st, "turbo_attn_decode")
     return (o, lse) if return_lse else o
+
+
+def turbo_attn_decode_trace(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tensor,
+                            block_table: torch.Tensor, group_table: torch.Tensor, sel,
+                            sm_scale: Optional[float] = None, kv_split_groups: int = 0):
+    """Test hook: turbo_attn_decode that also returns the integers of group g
+    of (sequence b, query head h), sel = (b, h, g); row 0 of each array."""
+    B, Hq, d = q.shape
+    mg = group_table.shape[1]
+    sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
+    workspace = decode_workspace(B, Hq, cache.num_kv_heads, mg, kv_split_groups, q.device)
+    wbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    o = torch.empty_like(q)
+    buf = _trace_buffer(q.device)
+    cs = cache.struct()
+    b, h, g = sel
+    st = lib().turbo_attn_decode_trace(_ptr(q), ctypes.byref(cs), _ptr(seq_lens),
+                                       _ptr(block_table), _ptr(group_table), mg, B, Hq, sm,
+                                       int(kv_split_groups), _ptr(workspace), wbytes, _ptr(o),
+                                       None, b, h, g, _ptr(buf), _stream(q.device))
+    _check(st, "turbo_attn_decode_trace")
+    torch.cuda.synchronize(q.device)
+    return o, _trace_dict(buf)

@@ -54,6 +54,8 @@ struct DecodeArgs {
   float* ws;                 // [B][Hq][nsplit][132] when nsplit > 1: m, l, -, -, O[128]
   uint2* o;                  // fp16 [B][Hq][128]
   float* lse;                // [B][Hq] or null
+  unsigned char* trace;      // test hook: integers of (sequence tr_b, query head tr_h, group tr_g)
+  int tr_b, tr_h, tr_g;
 };
 
 constexpr int kWsStride = 132;  // m, l, two pad words, O[128] (16-byte aligned)
@@ -180,11 +182,11 @@ __device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head
           ((unsigned)*reinterpret_cast<const unsigned short*>(D.meta + 384 + 2 * lane) << 16);
 }
 
-template <int GP, int BITS>
+template <int GP, int BITS, bool kTrace>
 __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>& L, int b, int kh,
                                               int g0, int g1, int head_off, const int (&q8w)[8],
                                               float& mrow, float& lpart, float& beta,
-                                              float (&O)[GP][2], float sq_row) {
+                                              float (&O)[GP][2], float sq_row, int trow) {
   constexpr int LPR = 64 / GP;  // lanes per compact softmax row
   constexpr int d = BITS == 4 ? 2 : 4;
   const int lane = threadIdx.x;
@@ -291,6 +293,12 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         for (int mb = 0; mb < 4; ++mb)
           *reinterpret_cast<int4*>(&L.sbuf[n < GP ? n : 0][16 * g4 + 4 * mb]) = sv[mb];
       }
+      const bool trace_g = kTrace && trow >= 0 && g == a.tr_g;  // wave-uniform
+      if (trace_g && n == trow) {
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+          reinterpret_cast<int4*>(a.trace + TURBO_TRACE_S)[4 * g4 + mb] = sv[mb];
+      }
       __syncthreads();
       // ---- compact softmax: lane (rr, cc) holds tokens cc*GP .. +GP-1 -----
       bool renorm;
@@ -343,7 +351,10 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
           ps += code;
           const int t = cc * GP + e;  // token of the group
           L.pbuf[rr][16 * (t >> 4) + vpos<BITS>(t & 15)] = (unsigned char)code;
+          if (trace_g && rr == trow) a.trace[TURBO_TRACE_P + t] = (unsigned char)code;
         }
+        if (trace_g && rr == trow && cc == 0)
+          *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
         const int psum = (int)row_sum<LPR>((float)ps);  // exact: < 2^24
         const float gsc = ((pmax / kQmax) * cur.svg) * __builtin_amdgcn_rcpf(beta);
         if (cc == 0) L.rowv[rr] = make_float4(gsc, __int_as_float(psum), rf, 0.0f);
@@ -407,6 +418,9 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
           // exact int32 PV of Algorithm 2: s * sum P*code + z * sum P
           O[r][0] = __builtin_fmaf(rv.x, (float)(s0 * acc[0][r] + z0 * psum), O[r][0]);
           O[r][1] = __builtin_fmaf(rv.x, (float)(s1 * acc[1][r] + z1 * psum), O[r][1]);
+          if (trace_g && r == trow)
+            reinterpret_cast<int2*>(a.trace + TURBO_TRACE_PV)[lane] =
+                make_int2(s0 * acc[0][r] + z0 * psum, s1 * acc[1][r] + z1 * psum);
         }
       }
     }
@@ -414,7 +428,9 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   }
 }
 
-template <int GP>
+// kTrace = true only for the test hook that also stores one group's integers
+// (the production instances carry no trace code).
+template <int GP, bool kTrace>
 __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
   __shared__ DecodeLds<GP> L;
   constexpr int LPR = 64 / GP;
@@ -469,6 +485,14 @@ __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
     }
     if (g4 == 0) L.sq[n] = sq;
   }
+  // traced row of this wave (-1: none); the wave whose chunk holds group tr_g
+  const int trow = kTrace && b == a.tr_b && kh == a.tr_h / G && g0 <= a.tr_g && a.tr_g < g1
+                       ? a.tr_h % G : -1;
+  if (trow >= 0 && n == trow) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) reinterpret_cast<int*>(a.trace + TURBO_TRACE_Q8)[8 * g4 + i] = q8w[i];
+    if (g4 == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = L.sq[n];
+  }
   __syncthreads();
   const float sq_row = L.sq[rr];
 
@@ -477,9 +501,9 @@ __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
   for (int r = 0; r < GP; ++r) O[r][0] = O[r][1] = 0.0f;
   float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
   if (bits == 4)
-    decode_groups<GP, 4>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row);
+    decode_groups<GP, 4, kTrace>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row, trow);
   else
-    decode_groups<GP, 2>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row);
+    decode_groups<GP, 2, kTrace>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row, trow);
 
   // ---- epilogue: per-row (m, l, beta) from the softmax lanes -------------
   const float l = row_sum<LPR>(lpart);
@@ -559,12 +583,22 @@ __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hkv * a.nsplit;
   const int gp = a.G <= 1 ? 1 : a.G <= 2 ? 2 : a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
-  switch (gp) {
-    case 1: hipLaunchKernelGGL(k_attn_decode<1>, dim3(total), dim3(64), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL(k_attn_decode<2>, dim3(total), dim3(64), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL(k_attn_decode<4>, dim3(total), dim3(64), 0, stream, a); break;
-    case 8: hipLaunchKernelGGL(k_attn_decode<8>, dim3(total), dim3(64), 0, stream, a); break;
-    default: hipLaunchKernelGGL(k_attn_decode<16>, dim3(total), dim3(64), 0, stream, a); break;
+  if (a.trace) {
+    switch (gp) {
+      case 1: hipLaunchKernelGGL((k_attn_decode<1, true>), dim3(total), dim3(64), 0, stream, a); break;
+      case 2: hipLaunchKernelGGL((k_attn_decode<2, true>), dim3(total), dim3(64), 0, stream, a); break;
+      case 4: hipLaunchKernelGGL((k_attn_decode<4, true>), dim3(total), dim3(64), 0, stream, a); break;
+      case 8: hipLaunchKernelGGL((k_attn_decode<8, true>), dim3(total), dim3(64), 0, stream, a); break;
+      default: hipLaunchKernelGGL((k_attn_decode<16, true>), dim3(total), dim3(64), 0, stream, a); break;
+    }
+  } else {
+    switch (gp) {
+      case 1: hipLaunchKernelGGL((k_attn_decode<1, false>), dim3(total), dim3(64), 0, stream, a); break;
+      case 2: hipLaunchKernelGGL((k_attn_decode<2, false>), dim3(total), dim3(64), 0, stream, a); break;
+      case 4: hipLaunchKernelGGL((k_attn_decode<4, false>), dim3(total), dim3(64), 0, stream, a); break;
+      case 8: hipLaunchKernelGGL((k_attn_decode<8, false>), dim3(total), dim3(64), 0, stream, a); break;
+      default: hipLaunchKernelGGL((k_attn_decode<16, false>), dim3(total), dim3(64), 0, stream, a); break;
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsplit == 1) return e;

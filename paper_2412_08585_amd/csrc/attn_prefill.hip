@@ -38,6 +38,8 @@ struct PrefillArgs {
   int causal;
   uint2* o;            // fp16 [B][Hq][N][128] (as 4-half units)
   float* lse;          // [B][Hq][N] or null
+  unsigned char* trace;  // test hook: integers of tile (logical index tr_L, key block tr_j)
+  int tr_L, tr_j;
 };
 
 constexpr int kPrefillWaves = 2;
@@ -56,6 +58,9 @@ __device__ __forceinline__ int prefill_order(int x, int total, int G) {
   return (8 * (n / G) + k) * G + n % G;
 }
 
+// kTrace = true only for the test hook that also stores one tile's integers
+// (the production instance carries no trace code).
+template <bool kTrace>
 __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillArgs a) {
   __shared__ float lut[8];
   __shared__ float xmax[2][kPrefillWaves];  // per-wave P maxima, double-buffered
@@ -116,6 +121,15 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
       qop[ks] = v4i{w[0], w[1], w[2], w[3]};
     }
   }
+  // wave-uniform; a key block the loop never reaches traces nothing
+  const bool traced = kTrace && L == a.tr_L && a.tr_j <= (a.causal ? i : a.nb - 1);
+  if (traced) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_Q8 + (32 * qh + n) * 128 + 32 * ks + 16 * hf) =
+          qop[ks];
+    if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = sq;
+  }
 
   const long kvu = (long)b * a.Hkv + kh;
   const float* skp = a.sk + kvu * a.nb;
@@ -172,6 +186,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
     const int jn = min(j + 1, jend);
     load_k(kop, jn);
     const float skn = skp[jn], svn = svp[jn];
+    const bool trace_tile = traced && j == a.tr_j;
+    if (trace_tile) {
+      int* ts = reinterpret_cast<int*>(a.trace + TURBO_TRACE_S) + (32 * qh + n) * 64 + 16 * hf;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ts[32 * kb + r] = S[kb][r];
+    }
     // ---- scores, online max, SAS (Algorithm 1, statistics step) --------
     const float c = (sq * skj) * a.sm_scale;
     float P[2][16];
@@ -240,6 +262,13 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
                         rne_bits(P[kb][4 * u + 2], inv), rne_bits(P[kb][4 * u + 3], inv));
       pop[kb] = v4i{w[0], w[1], w[2], w[3]};
     }
+    if (trace_tile) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_P + (32 * qh + n) * 64 + 32 * kb + 16 * hf) =
+            pop[kb];
+      if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
+    }
     // ---- PV_j, then S_{j+1}, on the MFMA -------------------------------
     v16i acc[4];
 #pragma unroll
@@ -250,6 +279,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
       acc[cb] = t;
     }
     qk(S, kop);
+    if (trace_tile) {
+      // register r of channel block cb <-> channel 32cb + 8(r/4) + 4hf + r%4
+      int* tp = reinterpret_cast<int*>(a.trace + TURBO_TRACE_PV) + (32 * qh + n) * 128;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tp[32 * cb + 8 * (r >> 2) + 4 * hf + (r & 3)] = acc[cb][r];
+    }
     // ---- Ost += (s_P s_V / beta) V_j^T Q(P~)^T ---------------------------
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
@@ -280,7 +317,10 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
 
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hq * a.nb;
-  hipLaunchKernelGGL(k_attn_prefill, dim3(total), dim3(64 * kPrefillWaves), 0, stream, a);
+  if (a.trace)
+    hipLaunchKernelGGL(k_attn_prefill<true>, dim3(total), dim3(64 * kPrefillWaves), 0, stream, a);
+  else
+    hipLaunchKernelGGL(k_attn_prefill<false>, dim3(total), dim3(64 * kPrefillWaves), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -114,9 +114,10 @@ int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d
   return turbo::launch_quantize_kv(a, B, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
 }
 
-int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
-                       const float* s_v, int B, int Hq, int Hkv, int N, int d, float sm_scale,
-                       int causal, void* o, float* lse, hipStream_t stream) {
+static int attn_prefill_impl(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
+                             const float* s_v, int B, int Hq, int Hkv, int N, int d,
+                             float sm_scale, int causal, void* o, float* lse,
+                             unsigned char* trace, int tr_L, int tr_j, hipStream_t stream) {
   if (B < 0 || N < 0 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || Hq / Hkv > TURBO_MAX_GQA ||
       d != TURBO_HEAD_DIM || !(sm_scale > 0.0f) || sm_scale > 3.0e38f)
     return TURBO_ERR_INVALID_ARG;
@@ -141,7 +142,31 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
   a.causal = causal ? 1 : 0;
   a.o = static_cast<uint2*>(o);
   a.lse = lse;
+  a.trace = trace;
+  a.tr_L = tr_L;
+  a.tr_j = tr_j;
   return turbo::launch_attn_prefill(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
+                       const float* s_v, int B, int Hq, int Hkv, int N, int d, float sm_scale,
+                       int causal, void* o, float* lse, hipStream_t stream) {
+  return attn_prefill_impl(q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale, causal, o, lse,
+                           nullptr, -1, -1, stream);
+}
+
+int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
+                             const float* s_k, const float* s_v, int B, int Hq, int Hkv, int N,
+                             int d, float sm_scale, int causal, void* o, float* lse, int tb,
+                             int th, int ti, int tj, void* trace, hipStream_t stream) {
+  const int nb = N > 0 ? (N + TURBO_BLOCK - 1) / TURBO_BLOCK : 0;
+  if (!trace || tb < 0 || tb >= B || th < 0 || th >= Hq || ti < 0 || ti >= nb || tj < 0 ||
+      tj >= nb)
+    return TURBO_ERR_INVALID_ARG;
+  // logical work index of (tb, th, ti): longest query blocks first
+  const int tr_L = (nb - 1 - ti) * B * Hq + tb * Hq + th;
+  return attn_prefill_impl(q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale, causal, o, lse,
+                           static_cast<unsigned char*>(trace), tr_L, tj, stream);
 }
 
 int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {
@@ -178,11 +203,12 @@ size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_s
   return (size_t)B * Hq * nsplit * turbo::kWsStride * sizeof(float);
 }
 
-int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
-                      const int32_t* block_table, const int32_t* group_table,
-                      int max_groups_per_seq, int B, int Hq, float sm_scale, int kv_split_groups,
-                      void* workspace, size_t workspace_bytes, void* o, float* lse,
-                      hipStream_t stream) {
+static int attn_decode_impl(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+                            const int32_t* block_table, const int32_t* group_table,
+                            int max_groups_per_seq, int B, int Hq, float sm_scale,
+                            int kv_split_groups, void* workspace, size_t workspace_bytes, void* o,
+                            float* lse, unsigned char* trace, int tb, int th, int tg,
+                            hipStream_t stream) {
   if (B < 0 || Hq < 1 || max_groups_per_seq < 1 || kv_split_groups < 0 || !cache ||
       !(sm_scale > 0.0f) || sm_scale > 3.0e38f)
     return TURBO_ERR_INVALID_ARG;
@@ -222,7 +248,33 @@ int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t*
   a.ws = static_cast<float*>(workspace);
   a.o = static_cast<uint2*>(o);
   a.lse = lse;
+  a.trace = trace;
+  a.tr_b = tb;
+  a.tr_h = th;
+  a.tr_g = tg;
   return turbo::launch_attn_decode(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+                      const int32_t* block_table, const int32_t* group_table,
+                      int max_groups_per_seq, int B, int Hq, float sm_scale, int kv_split_groups,
+                      void* workspace, size_t workspace_bytes, void* o, float* lse,
+                      hipStream_t stream) {
+  return attn_decode_impl(q, cache, seq_lens, block_table, group_table, max_groups_per_seq, B, Hq,
+                          sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse, nullptr,
+                          -1, -1, -1, stream);
+}
+
+int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+                            const int32_t* block_table, const int32_t* group_table,
+                            int max_groups_per_seq, int B, int Hq, float sm_scale,
+                            int kv_split_groups, void* workspace, size_t workspace_bytes, void* o,
+                            float* lse, int tb, int th, int tg, void* trace, hipStream_t stream) {
+  if (!trace || tb < 0 || tb >= B || th < 0 || th >= Hq || tg < 0 || tg >= max_groups_per_seq)
+    return TURBO_ERR_INVALID_ARG;
+  return attn_decode_impl(q, cache, seq_lens, block_table, group_table, max_groups_per_seq, B, Hq,
+                          sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse,
+                          static_cast<unsigned char*>(trace), tb, th, tg, stream);
 }
 
 }  // extern "C"

@@ -100,6 +100,42 @@ def test_invalid_arguments_rejected_before_launch(ta):
                                ctypes.byref(c), dummy, dummy, 2, None) == -1
 
 
+def test_trace_hooks_reject_bad_arguments(ta):
+    """The *_trace test hooks check the trace buffer and the selected tile or
+    group before any launch."""
+    L = ta.lib()
+    P = ctypes.c_void_p
+    dummy = P(16)
+    pre = (dummy, dummy, dummy, dummy, dummy, 1, 4, 4, 130, 128, 0.1, 1, dummy, None)
+    assert L.turbo_attn_prefill_trace(*pre, 0, 0, 0, 0, None, None) == -1     # no buffer
+    for tile in [(1, 0, 0, 0), (0, 4, 0, 0), (0, 0, 3, 0), (0, 0, 0, 3), (-1, 0, 0, 0)]:
+        assert L.turbo_attn_prefill_trace(*pre, *tile, dummy, None) == -1
+    bad = (dummy, dummy, dummy, dummy, dummy, 1, 6, 4, 130, 128, 0.1, 1, dummy, None)
+    assert L.turbo_attn_prefill_trace(*bad, 0, 0, 0, 0, dummy, None) == -1     # Hq % Hkv
+    c = ta.TurboKVCacheStruct()
+    c.pages, c.group_meta, c.group_scale = 16, 16, 16
+    c.num_pages, c.num_group_slots, c.num_kv_heads, c.head_dim = 4, 1, 1, 128
+    c.head_bits[0] = 4
+    dec = (dummy, ctypes.byref(c), dummy, dummy, dummy, 2, 1, 1, 0.1, 1, None, 0, dummy, None)
+    assert L.turbo_attn_decode_trace(*dec, 0, 0, 0, None, None) == -1
+    for sel in [(1, 0, 0), (0, 1, 0), (0, 0, 2), (0, 0, -1)]:
+        assert L.turbo_attn_decode_trace(*dec, *sel, dummy, None) == -1
+
+
+def test_trace_layout_matches_header(ta):
+    src = open(os.path.join(ROOT, "include", "turbo_attn.h")).read()
+    vals = {m[0]: int(m[1]) for m in re.findall(r"#define (TURBO_TRACE_\w+) (\d+)", src)}
+    b = ta.binding
+    assert (vals["TURBO_TRACE_Q8"], vals["TURBO_TRACE_S"], vals["TURBO_TRACE_P"],
+            vals["TURBO_TRACE_PV"], vals["TURBO_TRACE_SQ"], vals["TURBO_TRACE_PMAX"],
+            vals["TURBO_TRACE_BYTES"]) == (b.TRACE_Q8, b.TRACE_S, b.TRACE_P, b.TRACE_PV,
+                                           b.TRACE_SQ, b.TRACE_PMAX, b.TRACE_BYTES)
+    # contiguous: int8 64x128, int32 64x64, int8 64x64, int32 64x128, two floats
+    assert b.TRACE_S == 64 * 128 and b.TRACE_P == b.TRACE_S + 4 * 64 * 64
+    assert b.TRACE_PV == b.TRACE_P + 64 * 64 and b.TRACE_SQ == b.TRACE_PV + 4 * 64 * 128
+    assert b.TRACE_BYTES == b.TRACE_SQ + 8
+
+
 def test_decode_split_and_workspace(ta):
     L = ta.lib()
     # chunk minimizing ceil(waves / 2048) * (chunk + 2), longest on ties
