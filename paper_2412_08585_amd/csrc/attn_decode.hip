@@ -123,34 +123,46 @@ struct GroupData {
   unsigned kraw[4][BITS];       // K codes of the 4 A-operand rows (32 channels each)
   unsigned ks4[8], kz4[8];      // K scale / zero of the lane's 32 channels
   unsigned vraw[8][BITS / 2];   // V codes of channel 16*cb + n in page g4
-  unsigned vsz;                 // V scale (low 16 bits) / zero (high) of channels 2L, 2L+1
+  unsigned vs4, vz4;            // V scales / zeros of channels 2L&~3 .. +3 (aligned dwords);
+                                // kept as loaded: arithmetic on them here would make the
+                                // loop wait for the prefetch of the next group
 };
 
 template <int BITS>
 __device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head_off,
-                                           const int* bt, const int* gt, int g,
+                                           const int* bt, const int* gt, int g, bool live,
                                            GroupData<BITS>& D) {
   const int lane = threadIdx.x;
   const int n = lane & 15, g4 = lane >> 4, m = lane & 15;
+  g = live ? g : 0;
   const long p0 = bt[4 * g], p1 = bt[4 * g + 1], p2 = bt[4 * g + 2], p3 = bt[4 * g + 3];
-  bool ok = p0 >= 0 && p0 < a.num_pages && p1 >= 0 && p1 < a.num_pages && p2 >= 0 &&
+  bool ok = live && p0 >= 0 && p0 < a.num_pages && p1 >= 0 && p1 < a.num_pages && p2 >= 0 &&
             p2 < a.num_pages && p3 >= 0 && p3 < a.num_pages;
   const long slot = gt[g];
   ok = ok && slot >= 0 && slot < a.num_slots;
   D.ok = ok;
-  if (!ok) return;  // caller error: this group is not read
-  D.meta = a.gmeta + (slot * a.Hkv + kh) * 512;
-  D.skg = a.gscale[(slot * a.Hkv + kh) * 2 + 0];
-  D.svg = a.gscale[(slot * a.Hkv + kh) * 2 + 1];
+  // The loads are issued on every path, so that the number of memory
+  // operations in flight is the same whatever the tables hold (and the wait
+  // counts before each use stay exact): a group that is not live (past the
+  // chunk) or has an out-of-range entry (a caller error; it is skipped) reads
+  // the first bytes of q instead.
+  const uint8_t* dummy = reinterpret_cast<const uint8_t*>(a.q);
+  D.meta = ok ? a.gmeta + (slot * a.Hkv + kh) * 512 : reinterpret_cast<const int8_t*>(dummy);
+  const float* gs = ok ? a.gscale + (slot * a.Hkv + kh) * 2 : reinterpret_cast<const float*>(dummy);
+  D.skg = gs[0];
+  D.svg = gs[1];
   // lane-dependent page choice by selects (no dynamic indexing of an array)
   const int pk = m >> 2;
   const long pgk = pk == 0 ? p0 : pk == 1 ? p1 : pk == 2 ? p2 : p3;
   const long pgv = g4 == 0 ? p0 : g4 == 1 ? p1 : g4 == 2 ? p2 : p3;
-  D.krow = a.pages + pgk * a.page_bytes + head_off + (m & 3) * 16 * BITS + 4 * BITS * g4;
-  D.vreg = a.pages + pgv * a.page_bytes + head_off + 256 * BITS;
+  D.krow = ok ? a.pages + pgk * a.page_bytes + head_off + (m & 3) * 16 * BITS + 4 * BITS * g4
+              : dummy;
+  D.vreg = ok ? a.pages + pgv * a.page_bytes + head_off + 256 * BITS : dummy;
+  const int kstep = ok ? 4 * 16 * BITS : 0, vstep = ok ? 2 * BITS : 0;  // V: 16 codes per channel
+  const int mstep = ok ? 1 : 0;
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
-    const uint8_t* krow = D.krow + 4 * mb * 16 * BITS;
+    const uint8_t* krow = D.krow + mb * kstep;
     if (BITS == 4) {
       const uint4 x = *reinterpret_cast<const uint4*>(krow);
       D.kraw[mb][0] = x.x; D.kraw[mb][1] = x.y; D.kraw[mb][2] = x.z; D.kraw[mb][3] = x.w;
@@ -160,9 +172,9 @@ __device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head
     }
   }
   {
-    const uint4* ms = reinterpret_cast<const uint4*>(D.meta + 32 * g4);
-    const uint4* mz = reinterpret_cast<const uint4*>(D.meta + 128 + 32 * g4);
-    const uint4 t0 = ms[0], t1 = ms[1], z0 = mz[0], z1 = mz[1];
+    const uint4* ms = reinterpret_cast<const uint4*>(D.meta + (32 * g4) * mstep);
+    const uint4* mz = reinterpret_cast<const uint4*>(D.meta + (128 + 32 * g4) * mstep);
+    const uint4 t0 = ms[0], t1 = ms[mstep], z0 = mz[0], z1 = mz[mstep];
     D.ks4[0] = t0.x; D.ks4[1] = t0.y; D.ks4[2] = t0.z; D.ks4[3] = t0.w;
     D.ks4[4] = t1.x; D.ks4[5] = t1.y; D.ks4[6] = t1.z; D.ks4[7] = t1.w;
     D.kz4[0] = z0.x; D.kz4[1] = z0.y; D.kz4[2] = z0.z; D.kz4[3] = z0.w;
@@ -172,14 +184,14 @@ __device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head
   for (int cb = 0; cb < 8; ++cb) {
     const int ch = 16 * cb + n;
     if (BITS == 4) {
-      const uint2 x = *reinterpret_cast<const uint2*>(D.vreg + ch * 8);
+      const uint2 x = *reinterpret_cast<const uint2*>(D.vreg + ch * vstep);
       D.vraw[cb][0] = x.x; D.vraw[cb][1] = x.y;
     } else {
-      D.vraw[cb][0] = *reinterpret_cast<const unsigned*>(D.vreg + ch * 4);
+      D.vraw[cb][0] = *reinterpret_cast<const unsigned*>(D.vreg + ch * vstep);
     }
   }
-  D.vsz = (unsigned)*reinterpret_cast<const unsigned short*>(D.meta + 256 + 2 * lane) |
-          ((unsigned)*reinterpret_cast<const unsigned short*>(D.meta + 384 + 2 * lane) << 16);
+  D.vs4 = *reinterpret_cast<const unsigned*>(D.meta + (256 + 4 * (lane >> 1)) * mstep);
+  D.vz4 = *reinterpret_cast<const unsigned*>(D.meta + (384 + 4 * (lane >> 1)) * mstep);
 }
 
 template <int GP, int BITS, bool kTrace>
@@ -214,10 +226,13 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   const int* bt = a.block_table + (long)b * 4 * a.max_groups;
   const int* gt = a.group_table + (long)b * a.max_groups;
 
-  GroupData<BITS> cur, nxt;
-  if (g0 < g1) load_group<BITS>(a, kh, head_off, bt, gt, g0, cur);
-  for (int g = g0; g < g1; ++g) {
-    if (g + 1 < g1) load_group<BITS>(a, kh, head_off, bt, gt, g + 1, nxt);
+  // Two prefetch buffers used alternately (a copy cur = nxt between groups
+  // would be a register move that waits for the prefetch to land).  Every
+  // prefetch is issued on every path so that the wait before each use covers
+  // exactly the loads that use needs.
+  GroupData<BITS> A, Bd;
+  load_group<BITS>(a, kh, head_off, bt, gt, g0, g0 < g1, A);
+  auto process = [&](const GroupData<BITS>& cur, int g) {
     if (cur.ok) {
       // ---- hi/lo B-operands from w = q * s^int (this lane's 32 channels)
       v4i bhi[2], blo[2];
@@ -404,9 +419,10 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
             for (int r = 0; r < GP; ++r) acc[c2][r] = L.obuf[2 * lane + c2][r];
           }
         }
-        const int s0 = (int)(cur.vsz & 0xffu), s1 = (int)((cur.vsz >> 8) & 0xffu);
-        const int z0 = (int)(int8_t)((cur.vsz >> 16) & 0xffu);
-        const int z1 = (int)(int8_t)((cur.vsz >> 24) & 0xffu);
+        const int sh = 16 * (lane & 1);  // channels 2L, 2L+1 within the dword
+        const int s0 = (int)((cur.vs4 >> sh) & 0xffu), s1 = (int)((cur.vs4 >> (sh + 8)) & 0xffu);
+        const int z0 = (int)(int8_t)((cur.vz4 >> sh) & 0xffu);
+        const int z1 = (int)(int8_t)((cur.vz4 >> (sh + 8)) & 0xffu);
 #pragma unroll
         for (int r = 0; r < GP; ++r) {
           const float4 rv = L.rowv[r];
@@ -424,7 +440,12 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         }
       }
     }
-    cur = nxt;
+  };
+  for (int g = g0; g < g1; g += 2) {
+    load_group<BITS>(a, kh, head_off, bt, gt, g + 1, g + 1 < g1, Bd);
+    process(A, g);
+    load_group<BITS>(a, kh, head_off, bt, gt, g + 2, g + 2 < g1, A);
+    if (g + 1 < g1) process(Bd, g + 1);
   }
 }
 

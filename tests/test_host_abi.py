@@ -136,6 +136,32 @@ def test_trace_layout_matches_header(ta):
     assert b.TRACE_BYTES == b.TRACE_SQ + 8
 
 
+def test_decode_load_addresses_stay_in_their_regions():
+    """Host replica of the decode prefetch addresses (load_group in
+    attn_decode.hip): every byte a lane reads lies in its KV head's region of a
+    16-token page (K codes in the first half, V codes in the second) or in the
+    group's 512-byte metadata, and the lanes together cover each region once."""
+    for bits in (4, 2):
+        kbytes, vbytes = (16, 8) if bits == 4 else (8, 4)
+        kstep, vstep = 4 * 16 * bits, 2 * bits
+        kseen, vseen = set(), set()
+        for lane in range(64):
+            n, g4, m = lane & 15, lane >> 4, lane & 15
+            for mb in range(4):
+                o = (m & 3) * 16 * bits + 4 * bits * g4 + mb * kstep
+                assert 0 <= o and o + kbytes <= 256 * bits
+                kseen |= set(range(o, o + kbytes))
+            for cb in range(8):
+                o = 256 * bits + (16 * cb + n) * vstep
+                assert o + vbytes <= 512 * bits
+                vseen |= set(range(o, o + vbytes))
+            for o, w in [(32 * g4, 16), (32 * g4 + 16, 16), (128 + 32 * g4, 16),
+                         (144 + 32 * g4, 16), (256 + 4 * (lane >> 1), 4), (384 + 4 * (lane >> 1), 4)]:
+                assert o + w <= 512 and o % w == 0
+        assert kseen == set(range(256 * bits))
+        assert vseen == set(range(256 * bits, 512 * bits))
+
+
 def test_decode_split_and_workspace(ta):
     L = ta.lib()
     # chunk minimizing ceil(waves / 2048) * (chunk + 2), longest on ties
