@@ -566,6 +566,7 @@ __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
 // 2*lane, 2*lane + 1.
 __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
   __shared__ float lut[8];
+  __shared__ float cwt[64], cl[64];  // merge weights and l of up to 64 chunks
   const int lane = threadIdx.x;
   if (lane < 8) lut[lane] = kLut[lane];
   __syncthreads();
@@ -582,15 +583,41 @@ __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
     o1 = w[kWsO + 1 + 2 * lane] / l;
     L = w[0] + logf(l);
   } else if (ns > 1) {
+    // m* over the chunks, lane s reading chunk s (and s + 64, ...)
     float mstar = -INFINITY;
-    for (int s = 0; s < ns; ++s) mstar = fmaxf(mstar, w[s * kWsStride]);
+    for (int s = lane; s < ns; s += 64) mstar = fmaxf(mstar, w[(long)s * kWsStride]);
+    mstar = wave_max(mstar);
+    // ascending accumulation of w_s l_s and w_s O_s; the weights of 64 chunks
+    // at a time go through LDS and four chunks' O loads are in flight at once
     float den = 0.0f, n0 = 0.0f, n1 = 0.0f;
-    for (int s = 0; s < ns; ++s) {
-      const float* ws = w + s * kWsStride;
-      const float wt = sas_y(mstar - ws[0], lut);
-      den = __builtin_fmaf(wt, ws[1], den);
-      n0 = __builtin_fmaf(wt, ws[kWsO + 2 * lane], n0);
-      n1 = __builtin_fmaf(wt, ws[kWsO + 1 + 2 * lane], n1);
+    for (int s0 = 0; s0 < ns; s0 += 64) {
+      const int cnt = min(64, ns - s0);
+      __syncthreads();
+      if (lane < cnt) {
+        const float* ws = w + (long)(s0 + lane) * kWsStride;
+        cwt[lane] = sas_y(mstar - ws[0], lut);
+        cl[lane] = ws[1];
+      }
+      __syncthreads();
+      const float* wo = w + (long)s0 * kWsStride + kWsO + 2 * lane;
+      int t = 0;
+      for (; t + 4 <= cnt; t += 4) {
+        float2 x[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) x[u] = *reinterpret_cast<const float2*>(wo + (t + u) * kWsStride);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          den = __builtin_fmaf(cwt[t + u], cl[t + u], den);
+          n0 = __builtin_fmaf(cwt[t + u], x[u].x, n0);
+          n1 = __builtin_fmaf(cwt[t + u], x[u].y, n1);
+        }
+      }
+      for (; t < cnt; ++t) {
+        const float2 x = *reinterpret_cast<const float2*>(wo + t * kWsStride);
+        den = __builtin_fmaf(cwt[t], cl[t], den);
+        n0 = __builtin_fmaf(cwt[t], x.x, n0);
+        n1 = __builtin_fmaf(cwt[t], x.y, n1);
+      }
     }
     o0 = n0 / den;
     o1 = n1 / den;
