@@ -57,6 +57,8 @@ def lib():
         I, F, L, D = ctypes.c_int, ctypes.c_float, ctypes.c_long, ctypes.c_double
         sig = {
             "or_num_threads": ([], I),
+            "or_head_priority": ([P, I, I, I, I, P], None),
+            "or_int2_heads": ([P, I, I, P], None),
             "or_lut": ([I], F),
             "or_poly": ([F], F),
             "or_sas_y": ([F], F),
@@ -242,3 +244,23 @@ def attn_exact(q, k, v, sm_scale: float, causal: bool = True):
     lib().or_attn_exact(_p(q), _p(k), _p(v), B, Hq, Hkv, Nq, Nk, d, float(sm_scale), int(causal),
                         _p(o), _p(lse))
     return o, lse
+
+
+def head_priority(k):
+    """Sec. 3.2 priority gap x std of each KV head; k [B][Hkv][N][d] (fp16
+    values).  Returns float64 [Hkv]."""
+    k = _f32(k)
+    B, Hkv, N, d = k.shape
+    out = np.empty(Hkv, np.float64)
+    lib().or_head_priority(_p(k), B, Hkv, N, d, _p(out))
+    return out
+
+
+def int2_heads(prio, n_int2: int):
+    """Sec. 3.2 strategy: uint8 [Hkv] of 2 for the n_int2 lowest priorities
+    (ties by head index), 4 otherwise."""
+    p = np.ascontiguousarray(np.asarray(prio, dtype=np.float64))
+    bits = np.empty(p.size, np.uint8)
+    lib().or_int2_heads(_p(p), p.size, int(n_int2), _p(bits))
+    return bits
+

@@ -569,6 +569,55 @@ void or_attn_exact(const float* q, const float* k, const float* v, int B, int Hq
 }
 
 /* ---- vector helpers for the Python wrapper ---------------------------- */
+/* ---- Sec. 3.2: head-wise mixed precision ------------------------------ */
+/* Priority of KV head h (Sec. 3.2, the priority equation):
+ *   gap_c   = max - min of channel c over every token of every sequence;
+ *   gap^(h) = max - min over all channels (and tokens) of the head;
+ *   std^(h) = standard deviation of the channel-wise gaps gap_c
+ *             (population form: the mean of squared deviations);
+ *   priority^(h) = gap^(h) * std^(h).
+ * Readings: the statistics are taken on K, the tensor whose heads carry the
+ * large-magnitude channels of Fig. 3 (V shows no outlier pattern), over the
+ * whole prefill batch of one layer (the bit widths are per layer and head).
+ * k: float [B][Hkv][N][d] (fp16 values).  Computed in double. */
+void or_head_priority(const float* k, int B, int Hkv, int N, int d, double* prio) {
+  double* gap = malloc(sizeof(double) * (size_t)d);
+  for (int h = 0; h < Hkv; ++h) {
+    double gmax = -INFINITY, gmin = INFINITY;
+    for (int c = 0; c < d; ++c) {
+      double cmax = -INFINITY, cmin = INFINITY;
+      for (int b = 0; b < B; ++b)
+        for (int t = 0; t < N; ++t) {
+          const double x = k[(((size_t)b * Hkv + h) * N + t) * d + c];
+          cmax = x > cmax ? x : cmax;
+          cmin = x < cmin ? x : cmin;
+        }
+      gap[c] = cmax - cmin;
+      gmax = cmax > gmax ? cmax : gmax;
+      gmin = cmin < gmin ? cmin : gmin;
+    }
+    double mean = 0.0;
+    for (int c = 0; c < d; ++c) mean += gap[c];
+    mean /= d;
+    double var = 0.0;
+    for (int c = 0; c < d; ++c) var += (gap[c] - mean) * (gap[c] - mean);
+    var /= d;
+    prio[h] = (gmax - gmin) * sqrt(var);
+  }
+  free(gap);
+}
+
+/* Sec. 3.2 quantization strategy: the n_int2 heads of lowest priority (rank
+ * <= n_h) get 2 bits, the others 4.  Equal priorities rank by head index. */
+void or_int2_heads(const double* prio, int Hkv, int n_int2, uint8_t* bits) {
+  for (int h = 0; h < Hkv; ++h) {
+    int rank = 0; /* number of heads ranked before h */
+    for (int g = 0; g < Hkv; ++g)
+      if (prio[g] < prio[h] || (prio[g] == prio[h] && g < h)) ++rank;
+    bits[h] = rank < n_int2 ? 2 : 4;
+  }
+}
+
 void or_sas_y_vec(const float* y, long n, float* out) {
   for (long i = 0; i < n; ++i) out[i] = or_sas_y(y[i]);
 }
