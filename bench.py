@@ -176,6 +176,10 @@ def main():
     ms_q = time_kernel(run_quant, args.kernel_iters)
     ms_p = time_kernel(run_prefill, args.kernel_iters)
     ms_d = time_kernel(run_decode, args.kernel_iters)
+    prio = torch.empty(Hkv, dtype=torch.float32, device=dev)
+    ms_h = time_kernel(lambda: ta.binding.lib().turbo_head_priority(
+        ta.binding._ptr(k), B, Hkv, N, d, ta.binding._ptr(prio), ta.binding._stream(dev)),
+        args.kernel_iters)
 
     # ---- algorithmic work -------------------------------------------------------
     prefill_ops = 2.0 * d * N * (N + 1) * B * Hq          # QK^T + PV over causal pairs
@@ -207,6 +211,8 @@ def main():
         "kernels": {
             "quantize_kv": {"ms": round(ms_q, 4), "GB/s": round(quant_bytes / ms_q / 1e6, 1),
                             "frac_hbm": round(quant_bytes / ms_q / 1e6 / PEAK_HBM_GBS, 4)},
+            "head_priority": {"ms": round(ms_h, 4), "GB/s": round(B * Hkv * N * d * 2 / ms_h / 1e6, 1),
+                              "note": "Sec. 3.2 bit choice from the prefill K; not in the step"},
             "attn_prefill": {"ms": round(ms_p, 4), "TOPS": round(prefill_tops, 2),
                              "frac_int8_mfma": round(prefill_tops / PEAK_INT8_TOPS, 4)},
             "attn_decode": {"ms": round(ms_d, 4),

@@ -256,6 +256,27 @@ int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache, const in
                             int kv_split_groups, void* workspace, size_t workspace_bytes, void* o,
                             float* lse, int tb, int th, int tg, void* trace, hipStream_t stream);
 
+/*
+ * turbo_head_priority — head-wise mixed precision (Sec. 3.2, the priority
+ * equation): for each KV head h of the prefill keys k (fp16 [B][Hkv][N][128],
+ * all B sequences and N tokens of one layer),
+ *   gap_c = max - min of channel c,  gap = max - min over all channels,
+ *   std   = population standard deviation of the 128 gap_c,
+ *   priority[h] = gap * std   (device fp32 [Hkv], written on `stream`).
+ * INVALID_ARG for B == 0 or N == 0 (no statistics), null pointers, d != 128.
+ */
+int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, float* priority,
+                        hipStream_t stream);
+
+/*
+ * turbo_int2_heads — the quantization strategy of Sec. 3.2 on the host:
+ * head_bits[h] = 2 for the n_int2 heads of lowest priority (equal priorities
+ * rank by head index), 4 for the others.  priority and head_bits are host
+ * arrays of Hkv entries (the result feeds turbo_kv_cache.head_bits and
+ * turbo_page_bytes).  INVALID_ARG for a NaN priority or n_int2 outside 0..Hkv.
+ */
+int turbo_int2_heads(const float* priority, int Hkv, int n_int2, uint8_t* head_bits);
+
 /* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
  * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq.  It
  * minimizes ceil(B*Hkv*chunks / 2048) * (chunk length + 2), the number of

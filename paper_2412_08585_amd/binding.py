@@ -57,6 +57,8 @@ def lib() -> ctypes.CDLL:
                                           P], I),
             "turbo_attn_decode_trace": ([P, P, P, P, P, I, I, I, F, I, P, Z, P, P, I, I, I, P, P],
                                         I),
+            "turbo_head_priority": ([P, I, I, I, I, P, P], I),
+            "turbo_int2_heads": ([P, I, I, P], I),
             "turbo_decode_auto_split": ([I, I, I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I], Z),
         }
@@ -248,3 +250,24 @@ def turbo_attn_decode_trace(q: torch.Tensor, cache: PagedKVCache, seq_lens: torc
     _check(st, "turbo_attn_decode_trace")
     torch.cuda.synchronize(q.device)
     return o, _trace_dict(buf)
+
+
+def turbo_head_priority(k: torch.Tensor) -> torch.Tensor:
+    """Sec. 3.2 priority (gap x std) of each KV head of the prefill keys
+    k fp16 [B][Hkv][N][128]; returns fp32 [Hkv] on k's device."""
+    B, Hkv, N, d = k.shape
+    out = torch.empty(Hkv, dtype=torch.float32, device=k.device)
+    _check(lib().turbo_head_priority(_ptr(k), B, Hkv, N, d, _ptr(out), _stream(k.device)),
+           "turbo_head_priority")
+    return out
+
+
+def turbo_int2_heads(priority, n_int2: int) -> np.ndarray:
+    """Sec. 3.2 strategy: uint8 [Hkv] bit widths, 2 for the n_int2 lowest
+    priorities (host)."""
+    p = np.ascontiguousarray(np.asarray(priority, dtype=np.float32))
+    bits = np.empty(p.size, np.uint8)
+    _check(lib().turbo_int2_heads(p.ctypes.data_as(ctypes.c_void_p), p.size, int(n_int2),
+                                  bits.ctypes.data_as(ctypes.c_void_p)), "turbo_int2_heads")
+    return bits
+

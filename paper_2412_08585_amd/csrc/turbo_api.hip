@@ -11,6 +11,7 @@
 #include "quantize_kv.hip"
 #include "attn_prefill.hip"
 #include "attn_decode.hip"
+#include "head_priority.hip"
 
 namespace {
 
@@ -275,6 +276,38 @@ int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache, const in
   return attn_decode_impl(q, cache, seq_lens, block_table, group_table, max_groups_per_seq, B, Hq,
                           sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse,
                           static_cast<unsigned char*>(trace), tb, th, tg, stream);
+}
+
+int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, float* priority,
+                        hipStream_t stream) {
+  if (B < 0 || N < 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || d != TURBO_HEAD_DIM)
+    return TURBO_ERR_INVALID_ARG;
+  if (!k || !priority || B == 0 || N == 0) return TURBO_ERR_INVALID_ARG;
+  if ((long)B * Hkv * N > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
+  int st = check_device();
+  if (st != TURBO_OK) return st;
+  turbo::PriorityArgs a{};
+  a.k = static_cast<const uint2*>(k);
+  a.B = B;
+  a.Hkv = Hkv;
+  a.N = N;
+  a.priority = priority;
+  return turbo::launch_head_priority(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_int2_heads(const float* priority, int Hkv, int n_int2, uint8_t* head_bits) {
+  if (!priority || !head_bits || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || n_int2 < 0 ||
+      n_int2 > Hkv)
+    return TURBO_ERR_INVALID_ARG;
+  for (int h = 0; h < Hkv; ++h)
+    if (!(priority[h] == priority[h])) return TURBO_ERR_INVALID_ARG;  // NaN
+  for (int h = 0; h < Hkv; ++h) {
+    int rank = 0;  // heads ranked before h: lower priority, or equal and lower index
+    for (int g = 0; g < Hkv; ++g)
+      if (priority[g] < priority[h] || (priority[g] == priority[h] && g < h)) ++rank;
+    head_bits[h] = rank < n_int2 ? 2 : 4;
+  }
+  return TURBO_OK;
 }
 
 }  // extern "C"

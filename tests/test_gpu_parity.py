@@ -333,3 +333,43 @@ def test_full_size_decode(orc, ta, dev, name):
         _log(f"  unit ({b},{h}) ok")
     del cache
     torch.cuda.empty_cache()
+
+
+# ---- head-wise mixed precision (Sec. 3.2) ------------------------------------
+
+PRIORITY_CASES = [
+    # B, Hkv, N, outlier heads
+    (2, 8, 200, [1, 4, 6, 7]),
+    (1, 3, 1, [2]),
+    (3, 10, 64 * 5 + 13, [0, 3, 5, 8, 9]),
+]
+
+
+@pytest.mark.parametrize("B,Hkv,N,outliers", PRIORITY_CASES)
+def test_head_priority_parity(orc, ta, dev, B, Hkv, N, outliers):
+    _log(f"head priority B={B} Hkv={Hkv} N={N}")
+    k = _rand((B, Hkv, N, 128), 1900 + N)
+    rng = np.random.default_rng(N)
+    for h in outliers:
+        k[:, h, :, torch.from_numpy(rng.choice(128, 4, replace=False))] *= 10
+    p = ta.turbo_head_priority(k.to(dev)).cpu().numpy()
+    ref = orc.head_priority(k)
+    np.testing.assert_allclose(p, ref, rtol=1e-5, atol=0)
+    n2 = Hkv - len(outliers)
+    bits = ta.turbo_int2_heads(p, n2)
+    assert np.array_equal(bits, orc.int2_heads(ref, n2))
+    if N > 1:
+        assert [int(b) for b in bits] == [4 if h in outliers else 2 for h in range(Hkv)]
+
+
+def test_head_priority_full_size(orc, ta, dev):
+    """The Phi-3-medium prefill keys (4 x 4096 tokens per KV head)."""
+    from paper_2412_08585_amd import workloads as W
+    w = W.WORKLOADS["phi3m-prefill-4k"]
+    _, k, _ = W.prefill_inputs(w, device=dev)
+    p = ta.turbo_head_priority(k).cpu().numpy()
+    ref = orc.head_priority(k.cpu())
+    np.testing.assert_allclose(p, ref, rtol=1e-5, atol=0)
+    assert np.array_equal(ta.turbo_int2_heads(p, w.Hkv // 2), orc.int2_heads(ref, w.Hkv // 2))
+    del k
+    torch.cuda.empty_cache()

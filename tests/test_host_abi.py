@@ -162,6 +162,28 @@ def test_decode_load_addresses_stay_in_their_regions():
         assert vseen == set(range(256 * bits, 512 * bits))
 
 
+def test_int2_heads_rule_matches_the_oracle(ta, orc):
+    rng = np.random.default_rng(3)
+    for Hkv in (1, 2, 8, 10, 64):
+        p = rng.random(Hkv).astype(np.float32)
+        p[rng.integers(Hkv)] = p[0]                        # a tie
+        for n in sorted({0, Hkv // 2, Hkv}):
+            assert np.array_equal(ta.turbo_int2_heads(p, n), orc.int2_heads(p.astype(np.float64), n))
+    L = ta.lib()
+    P = ctypes.c_void_p
+    out = np.empty(4, np.uint8)
+    nan = np.array([1.0, np.nan, 2.0, 3.0], np.float32)
+    assert L.turbo_int2_heads(nan.ctypes.data_as(P), 4, 2, out.ctypes.data_as(P)) == -1
+    ok = np.ones(4, np.float32)
+    assert L.turbo_int2_heads(ok.ctypes.data_as(P), 4, 5, out.ctypes.data_as(P)) == -1
+    assert L.turbo_int2_heads(None, 4, 2, out.ctypes.data_as(P)) == -1
+    # head priority: empty input and bad shapes are rejected before any launch
+    dummy = P(16)
+    assert L.turbo_head_priority(dummy, 0, 4, 64, 128, dummy, None) == -1
+    assert L.turbo_head_priority(dummy, 1, 4, 64, 64, dummy, None) == -1
+    assert L.turbo_head_priority(None, 1, 4, 64, 128, dummy, None) == -1
+
+
 def test_decode_split_and_workspace(ta):
     L = ta.lib()
     # chunk minimizing ceil(waves / 2048) * (chunk + 2), longest on ties
