@@ -70,7 +70,10 @@ def lib():
             "or_sas_softmax_rows": ([P, I, I, P], None),
             "or_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P], None),
             "or_attn_prefill": ([P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P, I, I], None),
-            "or_attn_decode": ([P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P],
+            "or_tail_init": ([P, P, I, I, I, I, P, P, P, P, P, P], None),
+            "or_append_kv": ([P, P, I, I, I, P, P, I, P, P, P, P, P, P, P, P, P, P, P, P], None),
+            "or_attn_decode": ([P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P,
+                                P, P, P, P],
                                None),
             "or_attn_exact": ([P, P, P, I, I, I, I, I, I, D, I, P, P], None),
         }
@@ -81,7 +84,9 @@ def lib():
     return _lib
 
 
-def _p(a: np.ndarray):
+def _p(a):
+    if a is None:
+        return None
     assert a.flags["C_CONTIGUOUS"]
     return a.ctypes.data_as(ctypes.c_void_p)
 
@@ -208,9 +213,11 @@ def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = Tr
 
 
 def attn_decode(q, qkv: dict, seq_lens, sm_scale: float, split: int, quant: bool = True,
-                sas: bool = True, trace=None):
+                sas: bool = True, trace=None, tail: dict = None):
     """Algorithm 2 (+ split-KV merge).  q [B][Hq][d] fp16 values; qkv is the
-    dict of quantize_kv; seq_lens int [B].  trace=(b, h, group)."""
+    dict of quantize_kv (or empty_cache); seq_lens int [B].  trace=(b, h, group)
+    (group ng = seq_len // 64 selects the buffer).  tail: the Sec. 3.3 int8
+    buffer of tail_init / append_kv, attended as one more chunk."""
     q = _f32(q)
     B, Hq, d = q.shape
     Hkv = qkv["kc"].shape[1]
@@ -223,10 +230,12 @@ def attn_decode(q, qkv: dict, seq_lens, sm_scale: float, split: int, quant: bool
     lse = np.empty((B, Hq), np.float64)
     tr, bufs = _trace(d, None if trace is None else (trace[0], trace[1], 0, trace[2]))
     c = {n: np.ascontiguousarray(qkv[n]) for n in ("kc", "vc", "ks", "kz", "vs", "vz")}
+    t = {n: None for n in ("tk", "tv", "tsk", "tsv")} if tail is None else tail
     lib().or_attn_decode(_p(q), _p(c["kc"]), _p(c["vc"]), _p(c["ks"]), _p(c["kz"]), _p(c["vs"]),
                          _p(c["vz"]), _p(sk), _p(sv), _p(sl), B, Hq, Hkv, Nc, d,
                          float(np.float32(sm_scale)), int(split), _Opts(int(quant), int(sas)),
-                         _p(o), _p(lse), ctypes.byref(tr) if tr is not None else None)
+                         _p(o), _p(lse), ctypes.byref(tr) if tr is not None else None,
+                         _p(t["tk"]), _p(t["tv"]), _p(t["tsk"]), _p(t["tsv"]))
     if tr is None:
         return o, lse
     bufs.update(hit=tr.hit, sq=np.float32(tr.sq), pmax=np.float32(tr.pmax))
@@ -263,4 +272,61 @@ def int2_heads(prio, n_int2: int):
     bits = np.empty(p.size, np.uint8)
     lib().or_int2_heads(_p(p), p.size, int(n_int2), _p(bits))
     return bits
+
+
+def empty_cache(B: int, Hkv: int, Nc: int, d: int = 128, bits=None) -> dict:
+    """A compressed cache of capacity Nc tokens (Nc/64 groups) in the layout of
+    quantize_kv, all zero; sk, sv [B][Hkv][Nc/64]."""
+    ng = Nc // 64
+    return dict(kc=np.zeros((B, Hkv, Nc, d), np.uint8), vc=np.zeros((B, Hkv, Nc, d), np.uint8),
+                ks=np.zeros((B, Hkv, ng, d), np.uint8), kz=np.zeros((B, Hkv, ng, d), np.int8),
+                vs=np.zeros((B, Hkv, ng, d), np.uint8), vz=np.zeros((B, Hkv, ng, d), np.int8),
+                sk=np.zeros((B, Hkv, ng), np.float32), sv=np.zeros((B, Hkv, ng), np.float32),
+                bits=np.ascontiguousarray(np.asarray(bits if bits is not None else [4] * Hkv,
+                                                     dtype=np.int32)))
+
+
+def cache_from_prefill(qkv: dict, Nc: int) -> dict:
+    """The groups of quantize_kv placed in an empty cache of capacity Nc."""
+    B, Hkv, _, d = qkv["k8"].shape
+    c = empty_cache(B, Hkv, Nc, d, qkv["bits"])
+    n = qkv["kc"].shape[2]
+    ng = n // 64
+    for key in ("kc", "vc"):
+        c[key][:, :, :n] = qkv[key]
+    for key in ("ks", "kz", "vs", "vz"):
+        c[key][:, :, :ng] = qkv[key]
+    c["sk"][:, :, :ng] = qkv["sk"][:, :, :ng]
+    c["sv"][:, :, :ng] = qkv["sv"][:, :, :ng]
+    return c
+
+
+def tail_init(k, v, qkv: dict) -> dict:
+    """Sec. 3.3 buffer after a prefill: universal scales (largest block scale
+    of each (b, kv-head)) and the N mod 64 trailing tokens as int8.
+    Returns dict tk [B][Hkv][64][d], tv [B][Hkv][d][64], tsk, tsv [B][Hkv]."""
+    k, v = _f32(k), _f32(v)
+    B, Hkv, N, d = k.shape
+    t = dict(tk=np.zeros((B, Hkv, 64, d), np.int8), tv=np.zeros((B, Hkv, d, 64), np.int8),
+             tsk=np.zeros((B, Hkv), np.float32), tsv=np.zeros((B, Hkv), np.float32))
+    sk, sv = np.ascontiguousarray(qkv["sk"]), np.ascontiguousarray(qkv["sv"])
+    lib().or_tail_init(_p(k), _p(v), B, Hkv, N, d, _p(sk), _p(sv), _p(t["tk"]), _p(t["tv"]),
+                       _p(t["tsk"]), _p(t["tsv"]))
+    return t
+
+
+def append_kv(cache: dict, tail: dict, knew, vnew, seq_lens):
+    """Sec. 3.3 decoding step: the new key/value [B][Hkv][d] of each sequence
+    into its buffer at row seq_len % 64; a full buffer is compressed (step 2)
+    into group seq_len // 64 of `cache` (from empty_cache / cache_from_prefill).
+    Updates cache and tail in place; seq_lens are the lengths before the step."""
+    knew, vnew = _f32(knew), _f32(vnew)
+    B, Hkv, d = knew.shape
+    Nc = cache["kc"].shape[2]
+    sl = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int32))
+    c = cache
+    lib().or_append_kv(_p(knew), _p(vnew), B, Hkv, d, _p(sl), _p(c["bits"]), Nc, _p(c["kc"]),
+                       _p(c["vc"]), _p(c["ks"]), _p(c["kz"]), _p(c["vs"]), _p(c["vz"]),
+                       _p(c["sk"]), _p(c["sv"]), _p(tail["tk"]), _p(tail["tv"]), _p(tail["tsk"]),
+                       _p(tail["tsv"]))
 

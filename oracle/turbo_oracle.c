@@ -422,12 +422,19 @@ void or_attn_prefill(const float* q, const float* k, const float* v, int B, int 
  * the loop from m = -inf; with more than one chunk the states are merged in
  * ascending order with m* = max m_s, w_s = SAS(m_s - m*),
  * O = sum w_s O_s / sum w_s l_s, L = m* + ln(sum w_s l_s).
- * No group: o = 0, lse = -inf.  Outputs o double [B][Hq][d], lse [B][Hq]. */
+ * No group: o = 0, lse = -inf.  Outputs o double [B][Hq][d], lse [B][Hq].
+ * With the int8 buffer of Sec. 3.3 (tk != NULL): the seq_len - 64 ng newest
+ * tokens (at most 63) sit in tk [B][Hkv][64][d] (token-major) and
+ * tv [B][Hkv][d][64] (channel-major) with the universal scales tsk, tsv
+ * [B][Hkv].  Reading: they are attended as one more chunk after the group
+ * chunks (same online step, P scale over the row's buffered keys), merged
+ * with the others as above. */
 void or_attn_decode(const float* q, const uint8_t* kc, const uint8_t* vc, const uint8_t* ks,
                     const int8_t* kz, const uint8_t* vs, const int8_t* vz, const float* sk,
                     const float* sv, const int* seq_lens, int B, int Hq, int Hkv, int Nc, int d,
                     float sm_scale, int split, or_opts opts, double* o, double* lse,
-                    or_trace* tr) {
+                    or_trace* tr, const int8_t* tk, const int8_t* tv, const float* tsk,
+                    const float* tsv) {
   const int G = Hq / Hkv, ngc = Nc / OR_BS;
 #pragma omp parallel
   {
@@ -458,7 +465,12 @@ void or_attn_decode(const float* q, const uint8_t* kc, const uint8_t* vc, const 
           memcpy(tr->q8, q8, (size_t)d);
           tr->sq = sq;
         }
-        const int nsplit = ng == 0 ? 0 : (ng + split - 1) / split;
+        /* the int8 buffer of Sec. 3.3 holds the seq_len - 64 ng newest tokens */
+        int ntail = tk ? seq_lens[b] - ng * OR_BS : 0;
+        if (ntail < 0) ntail = 0;
+        if (ntail > OR_BS - 1) ntail = OR_BS - 1;
+        const int ngchunks = ng == 0 ? 0 : (ng + split - 1) / split;
+        const int nsplit = ngchunks + (ntail > 0);
         double mstar = -INFINITY, den = 0.0;
         for (int e = 0; e < d; ++e) num[e] = 0.0;
         /* first pass over chunks for m* (needed only when merging) */
@@ -468,6 +480,40 @@ void or_attn_decode(const float* q, const uint8_t* kc, const uint8_t* vc, const 
         for (int s = 0; s < nsplit; ++s) {
           or_row row = {-INFINITY, 0.0, Oall + (size_t)s * d};
           for (int e = 0; e < d; ++e) row.O[e] = 0.0;
+          if (s == ngchunks) {
+            /* the buffer: one more chunk of ntail int8 tokens with the
+             * universal scales, merged like the others */
+            const int8_t* kb = tk + u * (size_t)OR_BS * d;
+            const int8_t* vbuf = tv + u * (size_t)d * OR_BS; /* channel-major */
+            for (int t = 0; t < OR_BS; ++t)
+              for (int e = 0; e < d; ++e) {
+                k1[t * d + e] = t < ntail ? kb[(size_t)t * d + e] : 0;
+                v1[t * d + e] = t < ntail ? vbuf[(size_t)e * OR_BS + t] : 0;
+              }
+            const float c = (float)(sq * tsk[u]) * sm_scale;
+            for (int t = 0; t < OR_BS; ++t) {
+              vis[t] = (unsigned char)(t < ntail);
+              if (!vis[t]) continue;
+              if (opts.quant) {
+                int32_t acc = 0;
+                for (int e = 0; e < d; ++e) acc += (int32_t)q8[e] * (int32_t)k1[t * d + e];
+                sc[t] = (double)((float)acc * c);
+                if (trq && tr->j == ng) tr->sacc[t] = acc;
+              } else {
+                double acc = 0.0;
+                for (int e = 0; e < d; ++e) acc += (double)qq[e] * (double)k1[t * d + e] * tsk[u];
+                sc[t] = acc * (double)sm_scale;
+                for (int e = 0; e < d; ++e) vf[t * d + e] = (float)((double)v1[t * d + e] * tsv[u]);
+              }
+            }
+            or_trace* tt = (trq && tr->j == ng) ? tr : NULL;
+            if (tt) tt->hit = 1;
+            or_tile(&opts, &row, 1, OR_BS, sc, vis, OR_BS, v1, tsv[u], vf, d, p, pd, qp, tt);
+            ms[s] = row.m;
+            ls[s] = row.l;
+            if (row.m > mstar) mstar = row.m;
+            continue;
+          }
           const int g1 = (s + 1) * split < ng ? (s + 1) * split : ng;
           for (int g = s * split; g < g1; ++g) {
             const size_t cb = (u * (size_t)ngc * OR_BS + (size_t)g * OR_BS) * d;
@@ -569,6 +615,87 @@ void or_attn_exact(const float* q, const float* k, const float* v, int B, int Hq
 }
 
 /* ---- vector helpers for the Python wrapper ---------------------------- */
+/* ---- Sec. 3.3: the int8 KV-cache buffer -------------------------------- */
+/* Universal-scale int8 code of x (Sec. 3.3): nearest integer (ties to even)
+ * of x * inv, inv = 1/s rounded to binary32, clamped to [-119, 119] (values
+ * beyond the scale's range are clamped, as Sec. 3.3 prescribes); s = 0
+ * gives 0. */
+static int8_t or_quant_univ(float x, float s) {
+  if (!(s > 0.0f)) return 0;
+  const float inv = 1.0f / s;
+  double r = rint((double)x * (double)inv);
+  if (r > OR_QMAX) r = OR_QMAX;
+  if (r < -OR_QMAX) r = -OR_QMAX;
+  return (int8_t)r;
+}
+
+/* Start of the buffer after a prefill of N tokens (Sec. 3.3).  Reading: the
+ * universal scale of (b, kv-head) is the largest step-1 block scale of its
+ * prefill (sk, sv [B][Hkv][ceil(N/64)] from or_quantize_kv), so the prefill's
+ * range is representable; the N mod 64 tokens that form no step-2 group are
+ * the buffer's first entries, coded with that scale.  tk [B][Hkv][64][d]
+ * token-major, tv [B][Hkv][d][64] channel-major; unused rows are 0. */
+void or_tail_init(const float* k, const float* v, int B, int Hkv, int N, int d, const float* sk,
+                  const float* sv, int8_t* tk, int8_t* tv, float* tsk, float* tsv) {
+  const int nb = (N + OR_BS - 1) / OR_BS, ng = N / OR_BS, nt = N - ng * OR_BS;
+  for (int b = 0; b < B; ++b)
+    for (int h = 0; h < Hkv; ++h) {
+      const size_t u = (size_t)b * Hkv + h;
+      float mk = 0.0f, mv = 0.0f;
+      for (int j = 0; j < nb; ++j) {
+        mk = sk[u * nb + j] > mk ? sk[u * nb + j] : mk;
+        mv = sv[u * nb + j] > mv ? sv[u * nb + j] : mv;
+      }
+      tsk[u] = mk;
+      tsv[u] = mv;
+      for (int t = 0; t < OR_BS; ++t)
+        for (int e = 0; e < d; ++e) {
+          const size_t src = (u * (size_t)N + (size_t)ng * OR_BS + t) * d + e;
+          tk[(u * OR_BS + t) * d + e] = t < nt ? or_quant_univ(k[src], mk) : 0;
+          tv[(u * d + e) * OR_BS + t] = t < nt ? or_quant_univ(v[src], mv) : 0;
+        }
+    }
+}
+
+/* One decoding step's new key and value per (b, kv-head) (Sec. 3.3): the
+ * token at position p = seq_lens[b] (before the append) goes to buffer row
+ * p mod 64 with the universal scales.  When that row is the 64th, the buffer
+ * is compressed like any other group (step 2, eq. step2bpq) into group
+ * p / 64 of the cache, whose float scales are the universal scales; groups
+ * at or beyond Nc/64 are not written (the caller's cache is full).
+ * knew, vnew float [B][Hkv][d]; cache arrays as in or_quantize_kv with
+ * Nc = ngc * 64 and sk, sv [B][Hkv][ngc]; bits int [Hkv]. */
+void or_append_kv(const float* knew, const float* vnew, int B, int Hkv, int d,
+                  const int* seq_lens, const int* bits, int Nc, uint8_t* kc, uint8_t* vc,
+                  uint8_t* ks, int8_t* kz, uint8_t* vs, int8_t* vz, float* sk, float* sv,
+                  int8_t* tk, int8_t* tv, const float* tsk, const float* tsv) {
+  const int ngc = Nc / OR_BS;
+  int8_t* col = malloc((size_t)OR_BS);
+  for (int b = 0; b < B; ++b) {
+    const int p = seq_lens[b];
+    if (p < 0) continue;
+    const int r = p % OR_BS, g = p / OR_BS;
+    for (int h = 0; h < Hkv; ++h) {
+      const size_t u = (size_t)b * Hkv + h;
+      for (int e = 0; e < d; ++e) {
+        tk[(u * OR_BS + r) * d + e] = or_quant_univ(knew[u * d + e], tsk[u]);
+        tv[(u * d + e) * OR_BS + r] = or_quant_univ(vnew[u * d + e], tsv[u]);
+      }
+      if (r != OR_BS - 1 || g >= ngc) continue;
+      for (int e = 0; e < d; ++e) {
+        const size_t m = (u * ngc + g) * (size_t)d + e;
+        const size_t dst = (u * (size_t)ngc * OR_BS + (size_t)g * OR_BS) * d + e;
+        or_step2_group(tk + u * OR_BS * (size_t)d + e, OR_BS, d, bits[h], ks + m, kz + m, kc + dst, d);
+        for (int t = 0; t < OR_BS; ++t) col[t] = tv[(u * d + e) * OR_BS + t];
+        or_step2_group(col, OR_BS, 1, bits[h], vs + m, vz + m, vc + dst, d);
+      }
+      sk[u * ngc + g] = tsk[u];
+      sv[u * ngc + g] = tsv[u];
+    }
+  }
+  free(col);
+}
+
 /* ---- Sec. 3.2: head-wise mixed precision ------------------------------ */
 /* Priority of KV head h (Sec. 3.2, the priority equation):
  *   gap_c   = max - min of channel c over every token of every sequence;
