@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define TURBO_ABI_VERSION 1
+#define TURBO_ABI_VERSION 2
 
 #define TURBO_HEAD_DIM 128       /* d */
 #define TURBO_BLOCK 64           /* B_r = B_c = step-2 group length (tokens) */
@@ -108,6 +108,28 @@ typedef struct turbo_kv_cache {
   int32_t head_dim;
   uint8_t head_bits[TURBO_MAX_KV_HEADS];
 } turbo_kv_cache;
+
+/*
+ * int8 KV-cache buffer of Sec. 3.3: per (sequence b, KV head h) the newest
+ * tokens that do not yet form a full 64-token group, kept as int8 under one
+ * "universal" scale per (b, h) and tensor, so that appending a token never
+ * re-quantizes the others.
+ *
+ * k      device int8 [batch][num_kv_heads][64][128], token-major: row r holds
+ *        token 64*floor(len/64) + r of the sequence (r < len mod 64).
+ * v      device int8 [batch][num_kv_heads][128][64], channel-major (element
+ *        (token r, channel c) at [c][r]).
+ * scale  device fp32 [batch][num_kv_heads][2]: universal scales s_K, s_V
+ *        (int8 value * s = real value).
+ * batch, num_kv_heads   the sizes the buffers are allocated for.
+ */
+typedef struct turbo_kv_tail {
+  int8_t* k;
+  int8_t* v;
+  float* scale;
+  int32_t batch;
+  int32_t num_kv_heads;
+} turbo_kv_tail;
 
 /* ABI version of the loaded library (TURBO_ABI_VERSION). */
 int turbo_abi_version(void);
@@ -213,13 +235,22 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
  * L = m* + ln(sum w_s l_s), chunks in ascending order.  With one chunk the
  * result is the unsplit Algorithm 2.
  *
+ * int8 buffer (Sec. 3.3): with tail != NULL the seq_len mod 64 newest tokens
+ * (rows of the buffer) are attended as well.  Reading: the buffer is one more
+ * chunk after the group chunks, running the same online step from m = -inf
+ * with the universal scales (QK^T and PV on its int8 codes), merged with the
+ * others as above.
+ *
  * q               fp16 [B][Hq][128].
- * cache           as filled by turbo_quantize_kv (num_kv_heads = Hkv).
- * seq_lens        device int32 [B]: cached tokens of each sequence; only the
- *                 floor(seq_len/64) full groups are attended (the int8 tail
- *                 buffer of Sec. 3.3 is not part of this call); values are
- *                 clamped to [0, 64*max_groups_per_seq].  A sequence with no
- *                 full group yields o = 0 and lse = -inf.
+ * cache           as filled by turbo_quantize_kv / turbo_append_kv
+ *                 (num_kv_heads = Hkv).
+ * tail            NULL (groups only) or the Sec. 3.3 buffer (batch >= B,
+ *                 num_kv_heads == Hkv).
+ * seq_lens        device int32 [B]: tokens of each sequence.  The
+ *                 floor(seq_len/64) full groups (at most max_groups_per_seq)
+ *                 come from the cache; with a tail, the next seq_len mod 64
+ *                 tokens (at most 63) from the buffer.  A sequence with
+ *                 nothing to attend yields o = 0 and lse = -inf.
  * block_table,
  * group_table     as for turbo_quantize_kv.  A group whose page or slot entry
  *                 is out of range is skipped (its memory is never read).
@@ -228,14 +259,14 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
  *                 turbo_decode_auto_split(B, Hkv, max_groups_per_seq) with
  *                 Hkv = cache->num_kv_heads (see below).
  * workspace       device scratch of at least turbo_decode_workspace_bytes()
- *                 bytes (may be NULL when that is 0).
+ *                 bytes (with_tail = tail != NULL; may be NULL when that is 0).
  * o               fp16 [B][Hq][128];  lse fp32 [B][Hq] or NULL.
  */
-int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
-                      const int32_t* block_table, const int32_t* group_table,
-                      int max_groups_per_seq, int B, int Hq, float sm_scale, int kv_split_groups,
-                      void* workspace, size_t workspace_bytes, void* o, float* lse,
-                      hipStream_t stream);
+int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const turbo_kv_tail* tail,
+                      const int32_t* seq_lens, const int32_t* block_table,
+                      const int32_t* group_table, int max_groups_per_seq, int B, int Hq,
+                      float sm_scale, int kv_split_groups, void* workspace,
+                      size_t workspace_bytes, void* o, float* lse, hipStream_t stream);
 
 /*
  * Test hook (not part of the method): turbo_attn_decode with the integers of
@@ -246,11 +277,13 @@ int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t*
  *   P[0][t]    Q(P~) code of token t;
  *   PV[0][c]   int32 sum_t P[t] * V^{q1}[t][c];
  *   SQ, PMAX   s_Q and the group's maximum of P~.
- * Nothing is written when group tg is not attended (tg >= seq_len/64 or a
- * table entry out of range).  INVALID_ARG also when trace is NULL or an index
- * is out of range.
+ * With a tail, group tg = floor(seq_len/64) selects the buffer (K^{q1}, V^{q1}
+ * its int8 codes).  Nothing is written when group tg is not attended (beyond
+ * the sequence, or a table entry out of range).  INVALID_ARG also when trace
+ * is NULL or an index is out of range.
  */
-int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache,
+                            const turbo_kv_tail* tail, const int32_t* seq_lens,
                             const int32_t* block_table, const int32_t* group_table,
                             int max_groups_per_seq, int B, int Hq, float sm_scale,
                             int kv_split_groups, void* workspace, size_t workspace_bytes, void* o,
@@ -277,6 +310,43 @@ int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, float* prio
  */
 int turbo_int2_heads(const float* priority, int Hkv, int n_int2, uint8_t* head_bits);
 
+/*
+ * turbo_tail_init — start of the int8 buffer after a prefill (Sec. 3.3).
+ * Reading: the universal scale of (b, h) is the largest step-1 block scale of
+ * the prefill (max over j of s_k[b][h][j], likewise for V), so every prefill
+ * value is representable; the N mod 64 trailing tokens, which form no step-2
+ * group, become the buffer's first rows, coded as
+ *   code = clamp(round_half_even(x * inv), -119, 119), inv = 1/s in binary32
+ * (0 when s = 0).  Rows beyond N mod 64 are zeroed.
+ *
+ * k, v      fp16 [B][Hkv][N][128] (the prefill keys and values).
+ * s_k, s_v  fp32 [B][Hkv][ceil(N/64)] as written by turbo_quantize_kv.
+ * tail      buffers with batch >= B, num_kv_heads == Hkv.
+ * B == 0 is a no-op; N == 0 is INVALID_ARG (no scale to start from).
+ */
+int turbo_tail_init(const void* k, const void* v, int B, int Hkv, int N, int d, const float* s_k,
+                    const float* s_v, const turbo_kv_tail* tail, hipStream_t stream);
+
+/*
+ * turbo_append_kv — one decoding step's new key and value per sequence
+ * (Sec. 3.3).  The token of sequence b at position p = seq_lens[b] (the
+ * length BEFORE this step; p < 0 skips the sequence) goes to buffer row
+ * p mod 64 with the universal scales and clamping (as in turbo_tail_init).
+ * When that row is the 64th, the buffer is compressed like any other group:
+ * step 2 (eq. step2bpq) into group g = p / 64 of the cache, pages
+ * block_table[b][4g..4g+3], slot group_table[b][g], with the universal
+ * scales as the group's s_K, s_V.  A flush whose group is >= max_groups_per_seq
+ * or whose table entries are out of range is skipped (never touching memory).
+ * The caller advances seq_lens afterwards.
+ *
+ * k_new, v_new  fp16 [B][Hkv][128].
+ * cache, tail   cache->num_kv_heads == tail->num_kv_heads == Hkv, batch >= B.
+ */
+int turbo_append_kv(const void* k_new, const void* v_new, int B, int Hkv, int d,
+                    const int32_t* seq_lens, const turbo_kv_cache* cache,
+                    const turbo_kv_tail* tail, const int32_t* block_table,
+                    const int32_t* group_table, int max_groups_per_seq, hipStream_t stream);
+
 /* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
  * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq.  It
  * minimizes ceil(B*Hkv*chunks / 2048) * (chunk length + 2), the number of
@@ -288,10 +358,11 @@ int turbo_int2_heads(const float* priority, int Hkv, int n_int2, uint8_t* head_b
 int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq);
 
 /* Workspace bytes turbo_attn_decode needs for these arguments (0 when every
- * sequence fits one chunk).  kv_split_groups = 0 means
- * turbo_decode_auto_split(B, Hkv, max_groups_per_seq). */
+ * sequence fits one chunk and there is no tail).  kv_split_groups = 0 means
+ * turbo_decode_auto_split(B, Hkv, max_groups_per_seq); with_tail != 0 adds
+ * the buffer's chunk. */
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
-                                    int kv_split_groups);
+                                    int kv_split_groups, int with_tail);
 
 #ifdef __cplusplus
 }

@@ -3,12 +3,14 @@
 The computation lives in libturboattn.so (hand-written HIP for gfx950 behind
 the C ABI of include/turbo_attn.h); this package only marshals arguments.
 """
-from .binding import (PagedKVCache, TurboKVCacheStruct, decode_split, decode_workspace, lib,
+from .binding import (KVTail, PagedKVCache, TurboKVCacheStruct, TurboKVTailStruct, decode_split,
+                      decode_workspace, lib,
                       page_bytes, turbo_attn_decode, turbo_attn_decode_trace, turbo_attn_prefill,
-                      turbo_attn_prefill_trace, turbo_head_priority, turbo_int2_heads,
-                      turbo_quantize_kv)
+                      turbo_attn_prefill_trace, turbo_append_kv, turbo_head_priority,
+                      turbo_int2_heads, turbo_quantize_kv, turbo_tail_init)
 
-__all__ = ["PagedKVCache", "TurboKVCacheStruct", "decode_split", "decode_workspace", "lib",
+__all__ = ["KVTail", "PagedKVCache", "TurboKVCacheStruct", "TurboKVTailStruct", "decode_split",
+           "decode_workspace", "lib",
            "page_bytes", "turbo_attn_decode", "turbo_attn_decode_trace", "turbo_attn_prefill",
-           "turbo_attn_prefill_trace", "turbo_head_priority", "turbo_int2_heads",
-           "turbo_quantize_kv"]
+           "turbo_attn_prefill_trace", "turbo_append_kv", "turbo_head_priority",
+           "turbo_int2_heads", "turbo_quantize_kv", "turbo_tail_init"]

@@ -52,15 +52,17 @@ def lib() -> ctypes.CDLL:
             "turbo_page_bytes": ([P, I], Z),
             "turbo_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, I, P], I),
             "turbo_attn_prefill": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
-            "turbo_attn_decode": ([P, P, P, P, P, I, I, I, F, I, P, Z, P, P, P], I),
+            "turbo_attn_decode": ([P, P, P, P, P, P, I, I, I, F, I, P, Z, P, P, P], I),
             "turbo_attn_prefill_trace": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, I, I, I, I, P,
                                           P], I),
-            "turbo_attn_decode_trace": ([P, P, P, P, P, I, I, I, F, I, P, Z, P, P, I, I, I, P, P],
-                                        I),
+            "turbo_attn_decode_trace": ([P, P, P, P, P, P, I, I, I, F, I, P, Z, P, P, I, I, I, P,
+                                         P], I),
+            "turbo_tail_init": ([P, P, I, I, I, I, P, P, P, P], I),
+            "turbo_append_kv": ([P, P, I, I, I, P, P, P, P, P, I, P], I),
             "turbo_head_priority": ([P, I, I, I, I, P, P], I),
             "turbo_int2_heads": ([P, I, I, P], I),
             "turbo_decode_auto_split": ([I, I, I], I),
-            "turbo_decode_workspace_bytes": ([I, I, I, I, I], Z),
+            "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -121,6 +123,52 @@ class PagedKVCache:
         for i, b in enumerate(self.head_bits):
             s.head_bits[i] = int(b)
         return s
+
+
+class TurboKVTailStruct(ctypes.Structure):
+    """Mirror of turbo_kv_tail (include/turbo_attn.h)."""
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("scale", ctypes.c_void_p),
+                ("batch", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32)]
+
+
+class KVTail:
+    """Device storage of the Sec. 3.3 int8 buffer: k [batch][Hkv][64][128]
+    (token-major), v [batch][Hkv][128][64] (channel-major), universal scales
+    [batch][Hkv][2]."""
+
+    def __init__(self, batch: int, num_kv_heads: int, device="cuda"):
+        self.batch, self.num_kv_heads = batch, num_kv_heads
+        self.k = torch.zeros(batch, num_kv_heads, BLOCK, HEAD_DIM, dtype=torch.int8, device=device)
+        self.v = torch.zeros(batch, num_kv_heads, HEAD_DIM, BLOCK, dtype=torch.int8, device=device)
+        self.scale = torch.zeros(batch, num_kv_heads, 2, dtype=torch.float32, device=device)
+
+    def struct(self) -> TurboKVTailStruct:
+        s = TurboKVTailStruct()
+        s.k, s.v, s.scale = self.k.data_ptr(), self.v.data_ptr(), self.scale.data_ptr()
+        s.batch, s.num_kv_heads = self.batch, self.num_kv_heads
+        return s
+
+
+def turbo_tail_init(k: torch.Tensor, v: torch.Tensor, s_k, s_v, tail: KVTail):
+    """Sec. 3.3 buffer after a prefill of k, v fp16 [B][Hkv][N][128] with the
+    block scales s_k, s_v of turbo_quantize_kv."""
+    B, Hkv, N, d = k.shape
+    ts = tail.struct()
+    _check(lib().turbo_tail_init(_ptr(k), _ptr(v), B, Hkv, N, d, _ptr(s_k), _ptr(s_v),
+                                 ctypes.byref(ts), _stream(k.device)), "turbo_tail_init")
+
+
+def turbo_append_kv(k_new: torch.Tensor, v_new: torch.Tensor, seq_lens: torch.Tensor,
+                    cache: PagedKVCache, tail: KVTail, block_table: torch.Tensor,
+                    group_table: torch.Tensor):
+    """Sec. 3.3 decoding step: k_new, v_new fp16 [B][Hkv][128] at positions
+    seq_lens (lengths before the step, device int32 [B])."""
+    B, Hkv, d = k_new.shape
+    cs, ts = cache.struct(), tail.struct()
+    _check(lib().turbo_append_kv(_ptr(k_new), _ptr(v_new), B, Hkv, d, _ptr(seq_lens),
+                                 ctypes.byref(cs), ctypes.byref(ts), _ptr(block_table),
+                                 _ptr(group_table), group_table.shape[1], _stream(k_new.device)),
+           "turbo_append_kv")
 
 
 def turbo_quantize_kv(k: torch.Tensor, v: torch.Tensor, cache: Optional[PagedKVCache] = None,
@@ -200,8 +248,9 @@ def decode_split(B: int, Hkv: int, max_groups: int, kv_split_groups: int = 0) ->
 
 
 def decode_workspace(B: int, Hq: int, Hkv: int, max_groups: int, kv_split_groups: int = 0,
-                     device="cuda") -> Optional[torch.Tensor]:
-    n = int(lib().turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups, kv_split_groups))
+                     device="cuda", with_tail: bool = False) -> Optional[torch.Tensor]:
+    n = int(lib().turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups, kv_split_groups,
+                                               int(bool(with_tail))))
     if n == 0:
         return None
     return torch.empty(n // 4, dtype=torch.float32, device=device)
@@ -211,39 +260,48 @@ def turbo_attn_decode(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tens
                       block_table: torch.Tensor, group_table: torch.Tensor,
                       sm_scale: Optional[float] = None, kv_split_groups: int = 0,
                       workspace: Optional[torch.Tensor] = None, return_lse: bool = False,
-                      out=None):
-    """Algorithm 2 decode over the paged cache.  q fp16 [B][Hq][128]."""
+                      out=None, tail: Optional[KVTail] = None):
+    """Algorithm 2 decode over the paged cache (and the Sec. 3.3 buffer when
+    tail is given).  q fp16 [B][Hq][128]."""
     B, Hq, d = q.shape
     mg = group_table.shape[1]
     sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
     if workspace is None:
-        workspace = decode_workspace(B, Hq, cache.num_kv_heads, mg, kv_split_groups, q.device)
+        workspace = decode_workspace(B, Hq, cache.num_kv_heads, mg, kv_split_groups, q.device,
+                                     with_tail=tail is not None)
     wbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty(B, Hq, dtype=torch.float32, device=q.device) if return_lse else None
     cs = cache.struct()
-    st = lib().turbo_attn_decode(_ptr(q), ctypes.byref(cs), _ptr(seq_lens), _ptr(block_table),
-                                 _ptr(group_table), mg, B, Hq, sm, int(kv_split_groups),
-                                 _ptr(workspace), wbytes, _ptr(o), _ptr(lse), _stream(q.device))
+    ts = tail.struct() if tail is not None else None
+    st = lib().turbo_attn_decode(_ptr(q), ctypes.byref(cs),
+                                 ctypes.byref(ts) if ts is not None else None, _ptr(seq_lens),
+                                 _ptr(block_table), _ptr(group_table), mg, B, Hq, sm,
+                                 int(kv_split_groups), _ptr(workspace), wbytes, _ptr(o),
+                                 _ptr(lse), _stream(q.device))
     _check(st, "turbo_attn_decode")
     return (o, lse) if return_lse else o
 
 
 def turbo_attn_decode_trace(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tensor,
                             block_table: torch.Tensor, group_table: torch.Tensor, sel,
-                            sm_scale: Optional[float] = None, kv_split_groups: int = 0):
+                            sm_scale: Optional[float] = None, kv_split_groups: int = 0,
+                            tail: Optional[KVTail] = None):
     """Test hook: turbo_attn_decode that also returns the integers of group g
     of (sequence b, query head h), sel = (b, h, g); row 0 of each array."""
     B, Hq, d = q.shape
     mg = group_table.shape[1]
     sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
-    workspace = decode_workspace(B, Hq, cache.num_kv_heads, mg, kv_split_groups, q.device)
+    workspace = decode_workspace(B, Hq, cache.num_kv_heads, mg, kv_split_groups, q.device,
+                                 with_tail=tail is not None)
     wbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     o = torch.empty_like(q)
     buf = _trace_buffer(q.device)
     cs = cache.struct()
+    ts = tail.struct() if tail is not None else None
     b, h, g = sel
-    st = lib().turbo_attn_decode_trace(_ptr(q), ctypes.byref(cs), _ptr(seq_lens),
+    st = lib().turbo_attn_decode_trace(_ptr(q), ctypes.byref(cs),
+                                       ctypes.byref(ts) if ts is not None else None, _ptr(seq_lens),
                                        _ptr(block_table), _ptr(group_table), mg, B, Hq, sm,
                                        int(kv_split_groups), _ptr(workspace), wbytes, _ptr(o),
                                        None, b, h, g, _ptr(buf), _stream(q.device))

@@ -50,8 +50,13 @@ struct DecodeArgs {
   int B, Hq, Hkv, G;
   float sm_scale;
   int split;                 // groups per chunk
-  int nsplit;                // chunks per sequence (grid dimension)
-  float* ws;                 // [B][Hq][nsplit][132] when nsplit > 1: m, l, -, -, O[128]
+  int nsplit;                // group chunks per sequence (grid dimension)
+  int nws;                   // workspace slots per row: nsplit, plus one with a tail
+  int direct;                // one chunk and no tail: write o and lse directly
+  float* ws;                 // [B][Hq][nws][132] unless direct: m, l, -, -, O[128]
+  const int8_t* tk;          // Sec. 3.3 buffer (null: none): [B][Hkv][64][128]
+  const int8_t* tv;          //   [B][Hkv][128][64]
+  const float* tscale;       //   [B][Hkv][2]
   uint2* o;                  // fp16 [B][Hq][128]
   float* lse;                // [B][Hq] or null
   unsigned char* trace;      // test hook: integers of (sequence tr_b, query head tr_h, group tr_g)
@@ -532,7 +537,7 @@ __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
   if (cc == 0) L.rowv[rr] = make_float4(mrow, l, beta, 0.0f);
   __syncthreads();
   const bool empty = g1 <= g0;
-  if (a.nsplit == 1) {
+  if (a.direct) {
 #pragma unroll
     for (int r = 0; r < GP; ++r) {
       if (r >= G) break;
@@ -551,11 +556,11 @@ __global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
     for (int r = 0; r < GP; ++r) {
       if (r >= G) break;
       const float be = L.rowv[r].z;
-      float* w = a.ws + (((long)b * a.Hq + kh * G + r) * a.nsplit + s) * kWsStride;
+      float* w = a.ws + (((long)b * a.Hq + kh * G + r) * a.nws + s) * kWsStride;
       *reinterpret_cast<float2*>(w + kWsO + 2 * lane) = make_float2(O[r][0] * be, O[r][1] * be);
     }
     if (cc == 0 && rr < G) {
-      float* w = a.ws + (((long)b * a.Hq + kh * G + rr) * a.nsplit + s) * kWsStride;
+      float* w = a.ws + (((long)b * a.Hq + kh * G + rr) * a.nws + s) * kWsStride;
       w[0] = mrow;
       w[1] = l;
     }
@@ -574,8 +579,10 @@ __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
   const int b = bh / a.Hq;
   int ng = a.seq_lens[b] / 64;
   ng = min(max(ng, 0), a.max_groups);
-  const int ns = (ng + a.split - 1) / a.split;
-  const float* w = a.ws + (long)bh * a.nsplit * kWsStride;
+  // group chunks, then the buffer's chunk when there is one
+  const int nt = a.tk ? min(max(a.seq_lens[b] - 64 * ng, 0), 63) : 0;
+  const int ns = (ng + a.split - 1) / a.split + (nt > 0);
+  const float* w = a.ws + (long)bh * a.nws * kWsStride;
   float o0 = 0.0f, o1 = 0.0f, L = -INFINITY;
   if (ns == 1) {
     const float l = w[1];
@@ -628,6 +635,8 @@ __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
   if (a.lse && lane == 0) a.lse[bh] = L;
 }
 
+hipError_t launch_decode_tail(const DecodeArgs& a, hipStream_t stream);  // kv_tail.hip
+
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hkv * a.nsplit;
   const int gp = a.G <= 1 ? 1 : a.G <= 2 ? 2 : a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
@@ -649,7 +658,11 @@ hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
     }
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.nsplit == 1) return e;
+  if (e != hipSuccess || a.direct) return e;
+  if (a.tk) {
+    e = launch_decode_tail(a, stream);
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(k_decode_combine, dim3(a.B * a.Hq), dim3(64), 0, stream, a);
   return hipGetLastError();
 }

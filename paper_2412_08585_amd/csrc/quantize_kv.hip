@@ -111,6 +111,77 @@ __device__ void step2_channel(const int8_t* tile, int bits, int8_t* meta_s, int8
   }
 }
 
+// Step 2 of the K group staged token-major in `tile` (LDS), its group
+// metadata and float scale, and the token-major packing of the codes into
+// the four pages of the group (head region at head_off).
+__device__ void compress_k(const int8_t* tile, uint8_t* ctile, int bits, int8_t* meta,
+                           float* gscale_k, float s, const long (&page)[4], uint8_t* pages,
+                           int page_bytes, int head_off) {
+  const int tid = threadIdx.x;
+  int code[32];
+  step2_channel(tile, bits, meta, meta + 128, code);
+  if (tid == 0) *gscale_k = s;
+  const int c = tid >> 1, hh = tid & 1;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) ctile[(32 * hh + i) * kTileStride + c] = (uint8_t)code[i];
+  __syncthreads();
+  // token-major packing: thread (t = tid>>2, chunk = tid&3) packs 32 channels
+  const int t = tid >> 2, ch = tid & 3;
+  const uint8_t* src = ctile + t * kTileStride + 32 * ch;
+  uint8_t* dst = pages + page[t >> 4] * page_bytes + head_off + (t & 15) * 16 * bits;
+  if (bits == 4) {
+    unsigned w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      unsigned x = 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x |= (unsigned)src[8 * i + e] << (4 * e);
+      w[i] = x;
+    }
+    *reinterpret_cast<uint4*>(dst + 16 * ch) = make_uint4(w[0], w[1], w[2], w[3]);
+  } else {
+    unsigned w[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      unsigned x = 0;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) x |= (unsigned)src[16 * i + e] << (2 * e);
+      w[i] = x;
+    }
+    *reinterpret_cast<uint2*>(dst + 8 * ch) = make_uint2(w[0], w[1]);
+  }
+}
+
+// Step 2 of the V group staged token-major in `tile`, its metadata and float
+// scale, and the channel-major packing of the codes into the group's pages.
+__device__ void compress_v(const int8_t* tile, int bits, int8_t* meta, float* gscale_v, float s,
+                           const long (&page)[4], uint8_t* pages, int page_bytes, int head_off) {
+  const int tid = threadIdx.x;
+  int code[32];
+  step2_channel(tile, bits, meta + 256, meta + 384, code);
+  if (tid == 0) *gscale_v = s;
+  // channel-major packing: tokens 32hh..32hh+31 are pages 2hh, 2hh+1
+  const int c = tid >> 1, hh = tid & 1;
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    uint8_t* dst = pages + page[2 * hh + pp] * page_bytes + head_off + 256 * bits + c * 2 * bits;
+    if (bits == 4) {
+      unsigned lo = 0, hi = 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        lo |= (unsigned)code[16 * pp + e] << (4 * e);
+        hi |= (unsigned)code[16 * pp + 8 + e] << (4 * e);
+      }
+      *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+    } else {
+      unsigned x = 0;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) x |= (unsigned)code[16 * pp + e] << (2 * e);
+      *reinterpret_cast<unsigned*>(dst) = x;
+    }
+  }
+}
+
 __global__ __launch_bounds__(kQkvThreads) void k_quantize_kv(QuantArgs a) {
   __shared__ int8_t tile[64 * kTileStride];
   __shared__ uint8_t ctile[64 * kTileStride];  // K codes, token-major
@@ -145,40 +216,9 @@ __global__ __launch_bounds__(kQkvThreads) void k_quantize_kv(QuantArgs a) {
   float s = quant_block(a.k + xoff, nr, tile, red, a.k8 + (unit * a.nb + j) * 8192);
   if (tid == 0) a.sk[unit * a.nb + j] = s;
   __syncthreads();
-  if (do_cache) {
-    int code[32];
-    step2_channel(tile, bits, meta, meta + 128, code);
-    if (tid == 0) a.gscale[(slot * a.Hkv + h) * 2 + 0] = s;
-    const int c = tid >> 1, hh = tid & 1;
-#pragma unroll
-    for (int i = 0; i < 32; ++i) ctile[(32 * hh + i) * kTileStride + c] = (uint8_t)code[i];
-    __syncthreads();
-    // token-major packing: thread (t = tid>>2, chunk = tid&3) packs 32 channels
-    const int t = tid >> 2, ch = tid & 3;
-    const uint8_t* src = ctile + t * kTileStride + 32 * ch;
-    uint8_t* dst = a.pages + page[t >> 4] * a.page_bytes + head_off + (t & 15) * 16 * bits;
-    if (bits == 4) {
-      unsigned w[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        unsigned x = 0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x |= (unsigned)src[8 * i + e] << (4 * e);
-        w[i] = x;
-      }
-      *reinterpret_cast<uint4*>(dst + 16 * ch) = make_uint4(w[0], w[1], w[2], w[3]);
-    } else {
-      unsigned w[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        unsigned x = 0;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) x |= (unsigned)src[16 * i + e] << (2 * e);
-        w[i] = x;
-      }
-      *reinterpret_cast<uint2*>(dst + 8 * ch) = make_uint2(w[0], w[1]);
-    }
-  }
+  if (do_cache)
+    compress_k(tile, ctile, bits, meta, a.gscale + (slot * a.Hkv + h) * 2 + 0, s, page, a.pages,
+               a.page_bytes, head_off);
   __syncthreads();
 
   // ---- V ----
@@ -199,32 +239,9 @@ __global__ __launch_bounds__(kQkvThreads) void k_quantize_kv(QuantArgs a) {
     dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
     dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
   }
-  if (do_cache) {
-    int code[32];
-    step2_channel(tile, bits, meta + 256, meta + 384, code);
-    if (tid == 0) a.gscale[(slot * a.Hkv + h) * 2 + 1] = s;
-    // channel-major packing: tokens 32hh..32hh+31 are pages 2hh, 2hh+1
-    const int c = tid >> 1, hh = tid & 1;
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp) {
-      uint8_t* dst = a.pages + page[2 * hh + pp] * a.page_bytes + head_off + 256 * bits +
-                     c * 2 * bits;
-      if (bits == 4) {
-        unsigned lo = 0, hi = 0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          lo |= (unsigned)code[16 * pp + e] << (4 * e);
-          hi |= (unsigned)code[16 * pp + 8 + e] << (4 * e);
-        }
-        *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
-      } else {
-        unsigned x = 0;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) x |= (unsigned)code[16 * pp + e] << (2 * e);
-        *reinterpret_cast<unsigned*>(dst) = x;
-      }
-    }
-  }
+  if (do_cache)
+    compress_v(tile, bits, meta, a.gscale + (slot * a.Hkv + h) * 2 + 1, s, page, a.pages,
+               a.page_bytes, head_off);
 }
 
 hipError_t launch_quantize_kv(const QuantArgs& a, int B, hipStream_t stream) {

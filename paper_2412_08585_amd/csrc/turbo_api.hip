@@ -12,6 +12,7 @@
 #include "attn_prefill.hip"
 #include "attn_decode.hip"
 #include "head_priority.hip"
+#include "kv_tail.hip"
 
 namespace {
 
@@ -195,16 +196,24 @@ int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {
 }
 
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
-                                    int kv_split_groups) {
+                                    int kv_split_groups, int with_tail) {
   if (B < 1 || Hq < 1 || Hkv < 1 || max_groups_per_seq < 1 || kv_split_groups < 0) return 0;
   const int split = kv_split_groups ? kv_split_groups
                                     : turbo_decode_auto_split(B, Hkv, max_groups_per_seq);
-  const long nsplit = (max_groups_per_seq + split - 1) / split;
-  if (nsplit <= 1) return 0;
-  return (size_t)B * Hq * nsplit * turbo::kWsStride * sizeof(float);
+  const long nws = (max_groups_per_seq + split - 1) / split + (with_tail ? 1 : 0);
+  if (nws <= 1) return 0;
+  return (size_t)B * Hq * nws * turbo::kWsStride * sizeof(float);
 }
 
-static int attn_decode_impl(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+static int check_tail(const turbo_kv_tail* tail, int B, int Hkv) {
+  if (!tail) return TURBO_OK;
+  if (!tail->k || !tail->v || !tail->scale || tail->batch < B || tail->num_kv_heads != Hkv)
+    return TURBO_ERR_INVALID_ARG;
+  return TURBO_OK;
+}
+
+static int attn_decode_impl(const void* q, const turbo_kv_cache* cache,
+                            const turbo_kv_tail* tail, const int32_t* seq_lens,
                             const int32_t* block_table, const int32_t* group_table,
                             int max_groups_per_seq, int B, int Hq, float sm_scale,
                             int kv_split_groups, void* workspace, size_t workspace_bytes, void* o,
@@ -221,11 +230,14 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache, const in
   turbo::DecodeArgs a{};
   int st = check_cache(cache, Hkv, &a.int2_mask, &a.page_bytes);
   if (st != TURBO_OK) return st;
+  st = check_tail(tail, B, Hkv);
+  if (st != TURBO_OK) return st;
   const int split = kv_split_groups ? kv_split_groups
                                     : turbo_decode_auto_split(B, Hkv, max_groups_per_seq);
   const long nsplit = (max_groups_per_seq + split - 1) / split;
   if ((long)B * Hkv * nsplit > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
-  const size_t need = turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups_per_seq, split);
+  const size_t need =
+      turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups_per_seq, split, tail != nullptr);
   if (need > 0 && (!workspace || workspace_bytes < need)) return TURBO_ERR_WORKSPACE_TOO_SMALL;
   st = check_device();
   if (st != TURBO_OK) return st;
@@ -246,7 +258,14 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache, const in
   a.sm_scale = sm_scale;
   a.split = split;
   a.nsplit = (int)nsplit;
+  a.nws = (int)nsplit + (tail ? 1 : 0);
+  a.direct = a.nws == 1;
   a.ws = static_cast<float*>(workspace);
+  if (tail) {
+    a.tk = tail->k;
+    a.tv = tail->v;
+    a.tscale = tail->scale;
+  }
   a.o = static_cast<uint2*>(o);
   a.lse = lse;
   a.trace = trace;
@@ -256,25 +275,26 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache, const in
   return turbo::launch_attn_decode(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
 }
 
-int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
-                      const int32_t* block_table, const int32_t* group_table,
-                      int max_groups_per_seq, int B, int Hq, float sm_scale, int kv_split_groups,
-                      void* workspace, size_t workspace_bytes, void* o, float* lse,
-                      hipStream_t stream) {
-  return attn_decode_impl(q, cache, seq_lens, block_table, group_table, max_groups_per_seq, B, Hq,
-                          sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse, nullptr,
-                          -1, -1, -1, stream);
+int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const turbo_kv_tail* tail,
+                      const int32_t* seq_lens, const int32_t* block_table,
+                      const int32_t* group_table, int max_groups_per_seq, int B, int Hq,
+                      float sm_scale, int kv_split_groups, void* workspace,
+                      size_t workspace_bytes, void* o, float* lse, hipStream_t stream) {
+  return attn_decode_impl(q, cache, tail, seq_lens, block_table, group_table, max_groups_per_seq,
+                          B, Hq, sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse,
+                          nullptr, -1, -1, -1, stream);
 }
 
-int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache, const int32_t* seq_lens,
+int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache,
+                            const turbo_kv_tail* tail, const int32_t* seq_lens,
                             const int32_t* block_table, const int32_t* group_table,
                             int max_groups_per_seq, int B, int Hq, float sm_scale,
                             int kv_split_groups, void* workspace, size_t workspace_bytes, void* o,
                             float* lse, int tb, int th, int tg, void* trace, hipStream_t stream) {
-  if (!trace || tb < 0 || tb >= B || th < 0 || th >= Hq || tg < 0 || tg >= max_groups_per_seq)
+  if (!trace || tb < 0 || tb >= B || th < 0 || th >= Hq || tg < 0 || tg > max_groups_per_seq)
     return TURBO_ERR_INVALID_ARG;
-  return attn_decode_impl(q, cache, seq_lens, block_table, group_table, max_groups_per_seq, B, Hq,
-                          sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse,
+  return attn_decode_impl(q, cache, tail, seq_lens, block_table, group_table, max_groups_per_seq,
+                          B, Hq, sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse,
                           static_cast<unsigned char*>(trace), tb, th, tg, stream);
 }
 
@@ -308,6 +328,66 @@ int turbo_int2_heads(const float* priority, int Hkv, int n_int2, uint8_t* head_b
     head_bits[h] = rank < n_int2 ? 2 : 4;
   }
   return TURBO_OK;
+}
+
+int turbo_tail_init(const void* k, const void* v, int B, int Hkv, int N, int d, const float* s_k,
+                    const float* s_v, const turbo_kv_tail* tail, hipStream_t stream) {
+  if (B < 0 || N < 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || d != TURBO_HEAD_DIM)
+    return TURBO_ERR_INVALID_ARG;
+  if (B == 0) return TURBO_OK;
+  if (N == 0 || !k || !v || !s_k || !s_v || !tail) return TURBO_ERR_INVALID_ARG;
+  int st = check_tail(tail, B, Hkv);
+  if (st != TURBO_OK) return st;
+  if ((long)B * Hkv * N > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
+  st = check_device();
+  if (st != TURBO_OK) return st;
+  turbo::TailInitArgs a{};
+  a.k = static_cast<const unsigned short*>(k);
+  a.v = static_cast<const unsigned short*>(v);
+  a.sk = s_k;
+  a.sv = s_v;
+  a.Hkv = Hkv;
+  a.N = N;
+  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.tk = tail->k;
+  a.tv = tail->v;
+  a.tscale = tail->scale;
+  return turbo::launch_tail_init(a, B, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_append_kv(const void* k_new, const void* v_new, int B, int Hkv, int d,
+                    const int32_t* seq_lens, const turbo_kv_cache* cache,
+                    const turbo_kv_tail* tail, const int32_t* block_table,
+                    const int32_t* group_table, int max_groups_per_seq, hipStream_t stream) {
+  if (B < 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || d != TURBO_HEAD_DIM ||
+      max_groups_per_seq < 1)
+    return TURBO_ERR_INVALID_ARG;
+  if (B == 0) return TURBO_OK;
+  if (!k_new || !v_new || !seq_lens || !cache || !tail || !block_table || !group_table)
+    return TURBO_ERR_INVALID_ARG;
+  turbo::AppendArgs a{};
+  int st = check_cache(cache, Hkv, &a.int2_mask, &a.page_bytes);
+  if (st != TURBO_OK) return st;
+  st = check_tail(tail, B, Hkv);
+  if (st != TURBO_OK) return st;
+  st = check_device();
+  if (st != TURBO_OK) return st;
+  a.knew = static_cast<const unsigned short*>(k_new);
+  a.vnew = static_cast<const unsigned short*>(v_new);
+  a.seq_lens = seq_lens;
+  a.Hkv = Hkv;
+  a.tk = tail->k;
+  a.tv = tail->v;
+  a.tscale = tail->scale;
+  a.pages = cache->pages;
+  a.gmeta = cache->group_meta;
+  a.gscale = cache->group_scale;
+  a.num_pages = cache->num_pages;
+  a.num_slots = cache->num_group_slots;
+  a.block_table = block_table;
+  a.group_table = group_table;
+  a.max_groups = max_groups_per_seq;
+  return turbo::launch_append_kv(a, B, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
 }
 
 }  // extern "C"

@@ -43,7 +43,7 @@ def test_exports_every_declared_function(ta):
 
 def test_version_and_strerror(ta):
     L = ta.lib()
-    assert L.turbo_abi_version() == 1
+    assert L.turbo_abi_version() == 2
     for st in (0, -1, -2, -3, -4, 7):
         assert L.turbo_strerror(st)
 
@@ -86,12 +86,12 @@ def test_invalid_arguments_rejected_before_launch(ta):
     c.pages, c.group_meta, c.group_scale = 16, 16, 16
     c.num_pages, c.num_group_slots, c.num_kv_heads, c.head_dim = 4, 1, 1, 128
     c.head_bits[0] = 3
-    assert L.turbo_attn_decode(dummy, ctypes.byref(c), dummy, dummy, dummy, 1, 1, 1, 0.1, 1, None,
-                               0, dummy, None, None) == -1
+    assert L.turbo_attn_decode(dummy, ctypes.byref(c), None, dummy, dummy, dummy, 1, 1, 1, 0.1, 1,
+                               None, 0, dummy, None, None) == -1
     c.head_bits[0] = 4
     # workspace required for 2 chunks of 1 group each but not given
-    assert L.turbo_attn_decode(dummy, ctypes.byref(c), dummy, dummy, dummy, 2, 1, 1, 0.1, 1, None,
-                               0, dummy, None, None) == -3
+    assert L.turbo_attn_decode(dummy, ctypes.byref(c), None, dummy, dummy, dummy, 2, 1, 1, 0.1, 1,
+                               None, 0, dummy, None, None) == -3
     # quantize with a cache whose head count differs from Hkv
     assert L.turbo_quantize_kv(dummy, dummy, 1, 2, 64, 128, dummy, dummy, dummy, dummy,
                                ctypes.byref(c), dummy, dummy, 1, None) == -1
@@ -116,9 +116,9 @@ def test_trace_hooks_reject_bad_arguments(ta):
     c.pages, c.group_meta, c.group_scale = 16, 16, 16
     c.num_pages, c.num_group_slots, c.num_kv_heads, c.head_dim = 4, 1, 1, 128
     c.head_bits[0] = 4
-    dec = (dummy, ctypes.byref(c), dummy, dummy, dummy, 2, 1, 1, 0.1, 1, None, 0, dummy, None)
+    dec = (dummy, ctypes.byref(c), None, dummy, dummy, dummy, 2, 1, 1, 0.1, 1, None, 0, dummy, None)
     assert L.turbo_attn_decode_trace(*dec, 0, 0, 0, None, None) == -1
-    for sel in [(1, 0, 0), (0, 1, 0), (0, 0, 2), (0, 0, -1)]:
+    for sel in [(1, 0, 0), (0, 1, 0), (0, 0, 3), (0, 0, -1)]:
         assert L.turbo_attn_decode_trace(*dec, *sel, dummy, None) == -1
 
 
@@ -203,8 +203,10 @@ def test_decode_split_and_workspace(ta):
         return best[1]
     for B, Hkv, G in [(1, 8, 256), (8, 8, 128), (32, 4, 300), (128, 16, 64), (3, 5, 7)]:
         assert L.turbo_decode_auto_split(B, Hkv, G) == brute(B, Hkv, G)
-    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10) == 0
-    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3) == 4 * 8 * 4 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10, 0) == 0
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3, 0) == 4 * 8 * 4 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10, 1) == 4 * 8 * 2 * 132 * 4  # + buffer
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3, 1) == 4 * 8 * 5 * 132 * 4
 
 
 def test_step2_reciprocal_division_is_exact():
