@@ -283,8 +283,10 @@ def bench_decode(args, w):
     bt, gt = W.tables(w)
     ncopy = 2
     caches = []
+    tails = []
     for c in range(ncopy):
         cache = ta.PagedKVCache(bt.size, gt.size, bits, dev)
+        tail = ta.KVTail(B, Hkv, dev)
         btd, gtd = torch.from_numpy(bt).to(dev), torch.from_numpy(gt).to(dev)
         chunk = 16
         for b0 in range(0, B, chunk):
@@ -294,9 +296,11 @@ def bench_decode(args, w):
             for bb in range(nbat):
                 for h in range(Hkv):
                     k[bb, h], v[bb, h] = W.unit_kv(w, b0 + bb, h, device=dev)
-            ta.turbo_quantize_kv(k, v, cache, btd[b0:b0 + nbat], gtd[b0:b0 + nbat])
-            del k, v
+            _, _, sk, sv = ta.turbo_quantize_kv(k, v, cache, btd[b0:b0 + nbat], gtd[b0:b0 + nbat])
+            ta.turbo_tail_init(k, v, sk, sv, tail.narrow(b0, nbat))
+            del k, v, sk, sv
         caches.append((cache, btd, gtd))
+        tails.append(tail)
     torch.cuda.synchronize()
     q = W.decode_query(w, device=dev)
     sl = torch.full((B,), N, dtype=torch.int32, device=dev)
@@ -327,6 +331,40 @@ def bench_decode(args, w):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
+
+    # ---- the Sec. 3.3 decoding step: append the new token's K/V to the int8
+    # buffer, then attend the cache plus the buffer (not the headline) -------
+    g = torch.Generator(device="cpu").manual_seed(7)
+    knew = torch.randn(B, Hkv, 128, generator=g).half().to(dev)
+    vnew = torch.randn(B, Hkv, 128, generator=g).half().to(dev)
+    sl1 = torch.full((B,), N + 1, dtype=torch.int32, device=dev)
+    ws1 = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev, with_tail=True)
+    it1 = [0]
+
+    def run_append():
+        cache, btd, gtd = caches[it1[0] % ncopy]
+        ta.turbo_append_kv(knew, vnew, sl, cache, tails[it1[0] % ncopy], btd, gtd)
+
+    def run_decode_buf():
+        cache, btd, gtd = caches[it1[0] % ncopy]
+        ta.turbo_attn_decode(q, cache, sl1, btd, gtd, w.sm_scale, split, workspace=ws1, out=o,
+                             tail=tails[it1[0] % ncopy])
+        it1[0] += 1
+
+    def time_loop(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps
+
+    ms_app = time_loop(run_append)
+    ms_buf = time_loop(lambda: (run_append(), run_decode_buf()))
     kv_bytes = sum(decode_bytes_per_token(int(bits[h])) for h in range(Hkv)) * B * N
     qo_bytes = B * Hq * 128 * 2 * 2
     gbs = (kv_bytes + qo_bytes) / (ms * 1e-3) / 1e9
@@ -347,6 +385,11 @@ def bench_decode(args, w):
                      "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
                      "per_launch_bytes": kv_bytes + qo_bytes},
+        "buffer_step": {
+            "note": "Sec. 3.3 decoding step: turbo_append_kv of the new token, then "
+                    "turbo_attn_decode over the cache plus the int8 buffer (seq_len N+1)",
+            "append_ms": round(ms_app, 4), "step_ms": round(ms_buf, 4),
+            "GB/s": round((kv_bytes + qo_bytes) / (ms_buf * 1e-3) / 1e9, 1)},
     }
     print(json.dumps(result), flush=True)
 

@@ -148,6 +148,15 @@ class KVTail:
         s.batch, s.num_kv_heads = self.batch, self.num_kv_heads
         return s
 
+    def narrow(self, b0: int, n: int) -> "KVTail":
+        """The buffers of sequences b0 .. b0+n-1 (a view sharing the storage)."""
+        if not (0 <= b0 and n >= 1 and b0 + n <= self.batch):
+            raise ValueError("sequence range outside the buffer")
+        t = KVTail.__new__(KVTail)
+        t.batch, t.num_kv_heads = n, self.num_kv_heads
+        t.k, t.v, t.scale = self.k[b0:b0 + n], self.v[b0:b0 + n], self.scale[b0:b0 + n]
+        return t
+
 
 def turbo_tail_init(k: torch.Tensor, v: torch.Tensor, s_k, s_v, tail: KVTail):
     """Sec. 3.3 buffer after a prefill of k, v fp16 [B][Hkv][N][128] with the

@@ -248,3 +248,21 @@ def test_decode_with_empty_buffer_matches_plain_decode(orc, ta, dev):
         else:
             assert torch.equal(a.view(torch.int16), b.view(torch.int16))
             assert torch.equal(la, lb)
+
+
+def test_tail_init_on_views_of_one_buffer(ta, dev):
+    """KVTail.narrow: starting the buffers of a batch in two parts (as a caller
+    that builds the cache sequence by sequence does) gives the same buffer as
+    one call over the whole batch."""
+    B, Hkv, N = 4, 2, 64 + 30
+    k, v = _rand((B, Hkv, N, 128), 2600).to(dev), _rand((B, Hkv, N, 128), 2601).to(dev)
+    whole = ta.KVTail(B, Hkv, dev)
+    _, _, sk, sv = ta.turbo_quantize_kv(k, v)
+    ta.turbo_tail_init(k, v, sk, sv, whole)
+    parts = ta.KVTail(B, Hkv, dev)
+    for b0, n in ((0, 1), (1, 3)):
+        _, _, skp, svp = ta.turbo_quantize_kv(k[b0:b0 + n], v[b0:b0 + n])
+        ta.turbo_tail_init(k[b0:b0 + n], v[b0:b0 + n], skp, svp, parts.narrow(b0, n))
+    torch.cuda.synchronize()
+    assert torch.equal(whole.k, parts.k) and torch.equal(whole.v, parts.v)
+    assert torch.equal(whole.scale, parts.scale)
