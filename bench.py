@@ -103,6 +103,8 @@ def main():
     w = W.WORKLOADS[args.workload]
     if w.kind == "decode":
         return bench_decode(args, w)
+    if w.kind == "softmax":
+        return bench_softmax(args, w)
     B, Hq, Hkv, N, G = w.B, w.Hq, w.Hkv, w.N, w.G
     d = 128
 
@@ -391,6 +393,56 @@ def bench_decode(args, w):
             "append_ms": round(ms_app, 4), "step_ms": round(ms_buf, 4),
             "GB/s": round((kv_bytes + qo_bytes) / (ms_buf * 1e-3) / 1e9, 1)},
     }
+    print(json.dumps(result), flush=True)
+
+
+def bench_softmax(args, w):
+    """Algorithm 3 on its own: turbo_sas_softmax over the B*Hq*N score rows
+    of N keys (fp32 in, fp32 out, resident in HBM)."""
+    import torch
+
+    import paper_2412_08585_amd as ta
+    from paper_2412_08585_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    x = W.softmax_scores(w, device=dev)
+    y = torch.empty_like(x)
+    rows, cols = x.shape
+    run = lambda: ta.turbo_sas_softmax(x, out=y)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    nbytes = rows * cols * 4 * 2               # fp32 read once, written once
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    result = {
+        "metric": "attention TOPS (prefill) & HBM GB/s (decode), % of MI355X roofline",
+        "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": f"synthetic (seeded N(0, {W.SCORE_STD:.3f}^2) fp32 score rows)",
+        "config": {"workload": w.name, "rows": rows, "cols": cols},
+        "roofline": {"kernel": "k_sas_softmax_block<4>", "bound": "hbm", "achieved": round(gbs, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": None, "per_launch_bytes": nbytes},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        n = 4096
+        xs = x[:n].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.sas_softmax_rows(xs)
+        dt = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": round(n * cols * 8 / dt / 1e9, 3), "unit": "GB/s",
+                                  "cores": 1, "kind": "oracle",
+                                  "sample": f"{n} of {rows} rows, {dt:.1f} s"}
     print(json.dumps(result), flush=True)
 
 

@@ -347,6 +347,21 @@ int turbo_append_kv(const void* k_new, const void* v_new, int B, int Hkv, int d,
                     const turbo_kv_tail* tail, const int32_t* block_table,
                     const int32_t* group_table, int max_groups_per_seq, hipStream_t stream);
 
+/*
+ * turbo_sas_softmax — Algorithm 3 (Appendix B; SAS of Sec. 4) as a
+ * stand-alone row softmax: for every row r of x (fp32 [rows][cols], row-major,
+ * device), with m = max_c x[r][c]:
+ *   e_c = SAS(x[r][c] - m): 0 when x - m < -6, else LUT[floor y] * POLY(y -
+ *         floor y) with y = m - x in binary32, LUT[k] = e^-k in binary32 and
+ *         POLY the cubic of Sec. 4 (Horner, fused multiply-adds);
+ *   y[r][c] = e_c / sum_c e_c   (fp32, device; may alias x).
+ * The e_c are the same binary32 values the attention kernels use; the row sum
+ * is accumulated in fp32.  -inf entries contribute 0; a row without a finite
+ * value gives NaN (0/0).  INVALID_ARG for null pointers, rows < 0,
+ * rows > 2^31 - 1 or cols < 1.  rows == 0 is a no-op.
+ */
+int turbo_sas_softmax(const float* x, float* y, int64_t rows, int cols, hipStream_t stream);
+
 /* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
  * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq.  It
  * minimizes ceil(B*Hkv*chunks / 2048) * (chunk length + 2), the number of

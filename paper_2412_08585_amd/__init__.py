@@ -7,10 +7,12 @@ from .binding import (KVTail, PagedKVCache, TurboKVCacheStruct, TurboKVTailStruc
                       decode_workspace, lib,
                       page_bytes, turbo_attn_decode, turbo_attn_decode_trace, turbo_attn_prefill,
                       turbo_attn_prefill_trace, turbo_append_kv, turbo_head_priority,
-                      turbo_int2_heads, turbo_quantize_kv, turbo_tail_init)
+                      turbo_int2_heads, turbo_quantize_kv, turbo_sas_softmax,
+                      turbo_tail_init)
 
 __all__ = ["KVTail", "PagedKVCache", "TurboKVCacheStruct", "TurboKVTailStruct", "decode_split",
            "decode_workspace", "lib",
            "page_bytes", "turbo_attn_decode", "turbo_attn_decode_trace", "turbo_attn_prefill",
            "turbo_attn_prefill_trace", "turbo_append_kv", "turbo_head_priority",
-           "turbo_int2_heads", "turbo_quantize_kv", "turbo_tail_init"]
+           "turbo_int2_heads", "turbo_quantize_kv", "turbo_sas_softmax",
+           "turbo_tail_init"]

@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
             "turbo_append_kv": ([P, P, I, I, I, P, P, P, P, P, I, P], I),
             "turbo_head_priority": ([P, I, I, I, I, P, P], I),
             "turbo_int2_heads": ([P, I, I, P], I),
+            "turbo_sas_softmax": ([P, P, ctypes.c_int64, I, P], I),
             "turbo_decode_auto_split": ([I, I, I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
         }
@@ -338,3 +339,15 @@ def turbo_int2_heads(priority, n_int2: int) -> np.ndarray:
                                   bits.ctypes.data_as(ctypes.c_void_p)), "turbo_int2_heads")
     return bits
 
+
+def turbo_sas_softmax(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Algorithm 3: SAS softmax of the rows of x (fp32, contiguous, last dim =
+    columns).  out may be x itself."""
+    if x.dtype != torch.float32 or not x.is_contiguous() or x.dim() < 1:
+        raise ValueError("x must be a contiguous float32 tensor")
+    cols = x.shape[-1]
+    rows = x.numel() // max(cols, 1)
+    y = torch.empty_like(x) if out is None else out
+    _check(lib().turbo_sas_softmax(_ptr(x), _ptr(y), rows, cols, _stream(x.device)),
+           "turbo_sas_softmax")
+    return y

@@ -13,6 +13,7 @@
 #include "attn_decode.hip"
 #include "head_priority.hip"
 #include "kv_tail.hip"
+#include "sas_softmax.hip"
 
 namespace {
 
@@ -328,6 +329,22 @@ int turbo_int2_heads(const float* priority, int Hkv, int n_int2, uint8_t* head_b
     head_bits[h] = rank < n_int2 ? 2 : 4;
   }
   return TURBO_OK;
+}
+
+int turbo_sas_softmax(const float* x, float* y, int64_t rows, int cols, hipStream_t stream) {
+  if (rows < 0 || rows > 0x7fffffffLL || cols < 1) return TURBO_ERR_INVALID_ARG;
+  if (rows == 0) return TURBO_OK;
+  if (!x || !y) return TURBO_ERR_INVALID_ARG;
+  const int st = check_device();
+  if (st != TURBO_OK) return st;
+  turbo::SasSoftmaxArgs a{};
+  a.x = x;
+  a.y = y;
+  a.rows = rows;
+  a.cols = cols;
+  a.vec = cols % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+          reinterpret_cast<uintptr_t>(y) % 16 == 0;
+  return turbo::launch_sas_softmax(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
 }
 
 int turbo_tail_init(const void* k, const void* v, int B, int Hkv, int N, int d, const float* s_k,

@@ -80,7 +80,14 @@ WORKLOADS = {
     "phi3m-decode-8k": Workload("phi3m-decode-8k", 2, "decode", 64, 40, 10, 8192, "mixed"),
     "llama3-8b-prefill-16k": Workload("llama3-8b-prefill-16k", 3, "prefill", 1, 32, 8, 16384, "int4"),
     "long-decode-32k": Workload("long-decode-32k", 4, "decode", 256, 32, 8, 32768, "int4"),
+    # Algorithm 3 on its own: the score rows of one Phi-3-medium-shaped
+    # sequence (40 query heads x 4096 queries, 4096 keys each).
+    "phi3m-sas-softmax-4k": Workload("phi3m-sas-softmax-4k", 5, "softmax", 1, 40, 10, 4096, "int4"),
 }
+
+# Standard deviation of the score stand-in: q.k / sqrt(128) for N(0,1) q and
+# k with 4 of 128 channels of k scaled by 10 has variance (124 + 4*100)/128.
+SCORE_STD = float(np.sqrt((HEAD_DIM - N_OUTLIER + N_OUTLIER * OUTLIER_GAIN ** 2) / HEAD_DIM))
 
 
 def seed_of(wid: int, b: int, h: int, stream: int) -> int:
@@ -171,3 +178,18 @@ def tables(w: Workload, B: Optional[int] = None, max_groups: Optional[int] = Non
     pages = rng.permutation(B * 4 * mg).astype(np.int32).reshape(B, 4 * mg)
     slots = rng.permutation(B * mg).astype(np.int32).reshape(B, mg)
     return pages, slots
+
+
+def softmax_scores(w: Workload, device="cpu", rows: Optional[int] = None, row0: int = 0):
+    """fp32 score rows [rows][N] for Algorithm 3: N(0, SCORE_STD^2), drawn in
+    blocks of 1024 rows, block i from seed_of(workload_id, i, 0, 4), so that
+    any block can be drawn alone (row0 must be a multiple of 1024)."""
+    total = w.B * w.Hq * w.N
+    rows = total - row0 if rows is None else rows
+    assert row0 % 1024 == 0 and row0 + rows <= total
+    out = torch.empty(rows, w.N, dtype=torch.float32, device=device)
+    for r in range(0, rows, 1024):
+        n = min(1024, rows - r)
+        g = _gen(device, seed_of(w.wid, (row0 + r) // 1024, 0, 4))
+        out[r:r + n] = torch.randn(n, w.N, generator=g, device=device) * SCORE_STD
+    return out

@@ -98,6 +98,12 @@ def test_invalid_arguments_rejected_before_launch(ta):
     # max_groups too small for N
     assert L.turbo_quantize_kv(dummy, dummy, 1, 1, 192, 128, dummy, dummy, dummy, dummy,
                                ctypes.byref(c), dummy, dummy, 2, None) == -1
+    # SAS softmax: bad sizes and null pointers; zero rows is a no-op
+    assert L.turbo_sas_softmax(dummy, dummy, -1, 8, None) == -1
+    assert L.turbo_sas_softmax(dummy, dummy, 4, 0, None) == -1
+    assert L.turbo_sas_softmax(dummy, dummy, 1 << 31, 8, None) == -1
+    assert L.turbo_sas_softmax(None, dummy, 4, 8, None) == -1
+    assert L.turbo_sas_softmax(None, None, 0, 8, None) == 0
 
 
 def test_trace_hooks_reject_bad_arguments(ta):
