@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_INT8_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, 8 TB/s
+PEAK_FP16_TFLOPS = 2500.0  # MI355X dense fp16 MFMA, 2.5 PFLOP/s
 
 
 def measured_traffic(kernel: str, workload: str):
@@ -105,6 +106,8 @@ def main():
         return bench_decode(args, w)
     if w.kind == "softmax":
         return bench_softmax(args, w)
+    if w.kind == "projection":
+        return bench_projection(args, w)
     B, Hq, Hkv, N, G = w.B, w.Hq, w.Hkv, w.N, w.G
     d = 128
 
@@ -443,6 +446,77 @@ def bench_softmax(args, w):
         result["cpu_baseline"] = {"value": round(n * cols * 8 / dt / 1e9, 3), "unit": "GB/s",
                                   "cores": 1, "kind": "oracle",
                                   "sample": f"{n} of {rows} rows, {dt:.1f} s"}
+    print(json.dumps(result), flush=True)
+
+
+def bench_projection(args, w):
+    """The QKV projection with FlashQ fused (turbo_qkv_project: fp16 GEMM on
+    the MFMA, FlashQ step 1 of Q/K/V and step 2 + cache write of K/V in the
+    epilogue), inputs resident in HBM."""
+    import torch
+
+    import paper_2412_08585_amd as ta
+    from paper_2412_08585_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    B, N, D, Hq, Hkv = w.B, w.N, w.hidden, w.Hq, w.Hkv
+    F = (Hq + 2 * Hkv) * 128
+    x, wt = W.projection_inputs(w, device=dev)
+    bits = W.head_bits(w)
+    bt, gt = W.tables(w)
+    cache = ta.PagedKVCache(bt.size, gt.size, bits, dev)
+    btd, gtd = torch.from_numpy(bt).to(dev), torch.from_numpy(gt).to(dev)
+    outs = ta.turbo_qkv_project(x, wt, Hq, Hkv, cache, btd, gtd)
+    run = lambda: ta.turbo_qkv_project(x, wt, Hq, Hkv, cache, btd, gtd, out=outs)
+    stream = torch.cuda.current_stream()
+
+    def time_loop(fn, iters):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    ms = time_loop(run, args.steps)
+    # context: the library fp16 GEMM alone (no quantization, fp16 output)
+    y = torch.empty(B * N, F, dtype=torch.float16, device=dev)
+    x2 = x.view(B * N, D)
+    ms_lib = time_loop(lambda: torch.matmul(x2, wt.t(), out=y), args.steps)
+    flops = 2.0 * B * N * D * F
+    tflops = flops / (ms * 1e-3) / 1e12
+    result = {
+        "metric": "attention TOPS (prefill) & HBM GB/s (decode), % of MI355X roofline",
+        "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic (seeded N(0,1) fp16 hidden states, N(0,1/D) fp16 weights with 4 "
+                "outlier channels per key head x10)",
+        "config": {"workload": w.name, "batch": B, "seq_len": N, "hidden": D, "q_heads": Hq,
+                   "kv_heads": Hkv, "head_dim": 128, "kv_cache": w.bits},
+        "library_gemm_fp16_out": {"ms": round(ms_lib, 4),
+                                  "TFLOP/s": round(flops / (ms_lib * 1e-3) / 1e12, 2),
+                                  "note": "torch.matmul X W^T alone, fp16 output, no FlashQ"},
+        "roofline": {"kernel": "k_qkv_project", "bound": "mfma", "achieved": round(tflops, 2),
+                     "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / PEAK_FP16_TFLOPS, 4), "traffic": None,
+                     "per_launch_flops": flops},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        n = 512
+        xs = x[0, :n].float().cpu().numpy()[None]
+        ws = wt.float().cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.qkv_project(xs, ws, Hq, Hkv, bits)
+        dt = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": round(2.0 * n * D * F / dt / 1e12, 5), "unit": "TFLOP/s",
+                                  "cores": oracle.num_threads(), "kind": "oracle",
+                                  "sample": f"{n} of {B * N} tokens, {dt:.1f} s"}
     print(json.dumps(result), flush=True)
 
 

@@ -202,6 +202,51 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
                        int causal, void* o, float* lse, hipStream_t stream);
 
 /*
+ * turbo_attn_prefill_q8 — turbo_attn_prefill with Q already quantized
+ * (FlashQ step 1 done by turbo_qkv_project): the prologue loads the int8
+ * block and its scale instead of quantizing fp16 Q.  Given the codes and
+ * scales the fp16 path would compute, the output is bit-identical to
+ * turbo_attn_prefill's.
+ *
+ * q8          int8 [B][Hq][64*ceil(N/64)][128], rows >= N zero.
+ * s_q         fp32 [B][Hq][ceil(N/64)]: the scale of each 64-row block.
+ * Other arguments and errors as turbo_attn_prefill.
+ */
+int turbo_attn_prefill_q8(const int8_t* q8, const float* s_q, const int8_t* k8, const int8_t* v8,
+                          const float* s_k, const float* s_v, int B, int Hq, int Hkv, int N,
+                          int d, float sm_scale, int causal, void* o, float* lse,
+                          hipStream_t stream);
+
+/*
+ * turbo_qkv_project — the QKV projection with FlashQ fused into it (Sec. 5.2
+ * folds the quantization of Q, K and V into the projection that produces
+ * them; Sec. 3.1 steps 1 and 2):
+ *   Y = X W^T in fp32 (fp16 MFMA), each output rounded to fp16, then
+ *   Q: int8 codes and scale per (sequence, query head, 64-row block), the rule
+ *      of the prefill's Q quantization (so turbo_attn_prefill_q8 can use it);
+ *   K, V: exactly what turbo_quantize_kv writes for the same fp16 K and V
+ *      (k8, v8, s_k, s_v and, when cache != NULL, the int4/int2 groups).
+ * Q, K and V are never stored in fp16.
+ *
+ * x           fp16 [B][N][D] hidden states, row-major; D % 64 == 0.
+ * w           fp16 [(Hq + 2 Hkv) * 128][D]: output feature f < 128 Hq is
+ *             channel f % 128 of query head f / 128; then the key heads, then
+ *             the value heads (the rows of a fused QKV linear layer).
+ * q8, s_q     int8 [B][Hq][64*ceil(N/64)][128] (rows >= N zero), fp32
+ *             [B][Hq][ceil(N/64)].
+ * k8, v8, s_k, s_v, cache, block_table, group_table, max_groups_per_seq
+ *             as turbo_quantize_kv.
+ * B, N        B == 0 or N == 0 is a no-op.  Errors: INVALID_ARG for null
+ *             outputs, D not a positive multiple of 64, d != 128,
+ *             Hq % Hkv != 0, Hkv outside 1..64, or a cache that
+ *             turbo_quantize_kv would reject.
+ */
+int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv, int d,
+                      int8_t* q8, float* s_q, int8_t* k8, int8_t* v8, float* s_k, float* s_v,
+                      const turbo_kv_cache* cache, const int32_t* block_table,
+                      const int32_t* group_table, int max_groups_per_seq, hipStream_t stream);
+
+/*
  * Test hook (not part of the method): turbo_attn_prefill with the integers of
  * one (sequence tb, query head th, query block ti, key block tj) tile written
  * to `trace` (device, TURBO_TRACE_BYTES, layout above).  The same kernel runs;

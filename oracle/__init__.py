@@ -179,6 +179,36 @@ def quantize_kv(k, v, bits) -> dict:
     return out
 
 
+def qkv_project(x, w, Hq: int, Hkv: int, bits, d: int = 128) -> dict:
+    """The QKV projection followed by FlashQ (Sec. 5.2 folds the quantization
+    into this projection; Sec. 3.1 step 1 and step 2).
+
+    x: [B][N][D] hidden states, w: [(Hq + 2 Hkv) d][D] weights (fp16 values;
+    query heads, then key heads, then value heads).  Reading: each projection
+    output is the exact sum X W^T rounded to fp16 (the precision of the
+    unfused path's Q, K, V) before FlashQ.  The sum is a float64 matmul, exact
+    for the small-integer test inputs whose partial sums fit in 53 bits.
+
+    Returns the fp16 values q [B][Hq][N][d], k, v [B][Hkv][N][d]; the Q block
+    codes q8 [B][Hq][N][d] and scales sq [B][Hq][ceil(N/64)] (the prefill's
+    Q rule: one block per 64 rows of a head); and quantize_kv(k, v, bits)."""
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    B, N, D = x.shape
+    y = (x.reshape(B * N, D) @ w.T).astype(np.float16).astype(np.float32)
+    y = y.reshape(B, N, Hq + 2 * Hkv, d).transpose(0, 2, 1, 3)
+    q = np.ascontiguousarray(y[:, :Hq])
+    k = np.ascontiguousarray(y[:, Hq:Hq + Hkv])
+    v = np.ascontiguousarray(y[:, Hq + Hkv:])
+    nb = (N + 63) // 64
+    qp = np.zeros((B, Hq, nb * 64, d), np.float32)
+    qp[:, :, :N] = q
+    q8, sq = block_quant(qp.reshape(B, Hq, nb, 64 * d))
+    out = quantize_kv(k, v, bits)
+    out.update(q=q, k=k, v=v, q8=q8.reshape(B, Hq, nb * 64, d)[:, :, :N].copy(), sq=sq)
+    return out
+
+
 def _trace(d: int, sel):
     if sel is None:
         return None, None

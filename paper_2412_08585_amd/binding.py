@@ -62,6 +62,8 @@ def lib() -> ctypes.CDLL:
             "turbo_head_priority": ([P, I, I, I, I, P, P], I),
             "turbo_int2_heads": ([P, I, I, P], I),
             "turbo_sas_softmax": ([P, P, ctypes.c_int64, I, P], I),
+            "turbo_attn_prefill_q8": ([P, P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
+            "turbo_qkv_project": ([P, P, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P], I),
             "turbo_decode_auto_split": ([I, I, I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
         }
@@ -351,3 +353,48 @@ def turbo_sas_softmax(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> to
     _check(lib().turbo_sas_softmax(_ptr(x), _ptr(y), rows, cols, _stream(x.device)),
            "turbo_sas_softmax")
     return y
+
+
+def turbo_qkv_project(x: torch.Tensor, w: torch.Tensor, Hq: int, Hkv: int,
+                      cache: Optional[PagedKVCache] = None,
+                      block_table: Optional[torch.Tensor] = None,
+                      group_table: Optional[torch.Tensor] = None, out=None):
+    """QKV projection with FlashQ fused (Sec. 5.2): x fp16 [B][N][D], w fp16
+    [(Hq + 2 Hkv) 128][D].  Returns (q8, s_q, k8, v8, s_k, s_v) in the layouts
+    of include/turbo_attn.h; writes the full K/V groups into `cache`."""
+    B, N, D = x.shape
+    nb = (N + BLOCK - 1) // BLOCK
+    dev = x.device
+    if out is None:
+        q8 = torch.empty(B, Hq, nb * BLOCK, HEAD_DIM, dtype=torch.int8, device=dev)
+        s_q = torch.empty(B, Hq, nb, dtype=torch.float32, device=dev)
+        k8 = torch.empty(B, Hkv, nb * BLOCK, HEAD_DIM, dtype=torch.int8, device=dev)
+        v8 = torch.empty(B, Hkv, nb, HEAD_DIM, BLOCK, dtype=torch.int8, device=dev)
+        s_k = torch.empty(B, Hkv, nb, dtype=torch.float32, device=dev)
+        s_v = torch.empty_like(s_k)
+    else:
+        q8, s_q, k8, v8, s_k, s_v = out
+    cs = cache.struct() if cache is not None else None
+    mg = group_table.shape[1] if group_table is not None else 0
+    _check(lib().turbo_qkv_project(_ptr(x), _ptr(w), B, N, D, Hq, Hkv, HEAD_DIM, _ptr(q8),
+                                   _ptr(s_q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v),
+                                   ctypes.byref(cs) if cs is not None else None,
+                                   _ptr(block_table), _ptr(group_table), mg, _stream(dev)),
+           "turbo_qkv_project")
+    return q8, s_q, k8, v8, s_k, s_v
+
+
+def turbo_attn_prefill_q8(q8: torch.Tensor, s_q: torch.Tensor, k8, v8, s_k, s_v, N: int,
+                          sm_scale: Optional[float] = None, causal: bool = True,
+                          return_lse: bool = False, out=None):
+    """Algorithm 1 prefill on pre-quantized Q (q8 [B][Hq][64 nb][128], s_q)."""
+    B, Hq = q8.shape[0], q8.shape[1]
+    Hkv = k8.shape[1]
+    sm = float(1.0 / np.sqrt(HEAD_DIM)) if sm_scale is None else float(sm_scale)
+    o = torch.empty(B, Hq, N, HEAD_DIM, dtype=torch.float16, device=q8.device) if out is None else out
+    lse = torch.empty(B, Hq, N, dtype=torch.float32, device=q8.device) if return_lse else None
+    _check(lib().turbo_attn_prefill_q8(_ptr(q8), _ptr(s_q), _ptr(k8), _ptr(v8), _ptr(s_k),
+                                       _ptr(s_v), B, Hq, Hkv, N, HEAD_DIM, sm, int(causal),
+                                       _ptr(o), _ptr(lse), _stream(q8.device)),
+           "turbo_attn_prefill_q8")
+    return (o, lse) if return_lse else o

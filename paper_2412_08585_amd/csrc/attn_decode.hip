@@ -168,7 +168,7 @@ __device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
     const uint8_t* krow = D.krow + mb * kstep;
-    if (BITS == 4) {
+    if constexpr (BITS == 4) {
       const uint4 x = *reinterpret_cast<const uint4*>(krow);
       D.kraw[mb][0] = x.x; D.kraw[mb][1] = x.y; D.kraw[mb][2] = x.z; D.kraw[mb][3] = x.w;
     } else {
@@ -188,7 +188,7 @@ __device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb) {
     const int ch = 16 * cb + n;
-    if (BITS == 4) {
+    if constexpr (BITS == 4) {
       const uint2 x = *reinterpret_cast<const uint2*>(D.vreg + ch * vstep);
       D.vraw[cb][0] = x.x; D.vraw[cb][1] = x.y;
     } else {

@@ -28,7 +28,9 @@
 namespace turbo {
 
 struct PrefillArgs {
-  const uint4* q;      // fp16 [B][Hq][N][128]
+  const uint4* q;      // fp16 [B][Hq][N][128] (null when q8 is given)
+  const int8_t* q8;    // pre-quantized Q: int8 [B][Hq][nb*64][128], scales sq [B][Hq][nb]
+  const float* sq;
   const int8_t* k8;    // [B][Hkv][nb*64][128]
   const int8_t* v8;    // [B][Hkv][nb][128][64]
   const float* sk;     // [B][Hkv][nb]
@@ -59,8 +61,10 @@ __device__ __forceinline__ int prefill_order(int x, int total, int G) {
 }
 
 // kTrace = true only for the test hook that also stores one tile's integers
-// (the production instance carries no trace code).
-template <bool kTrace>
+// (the production instance carries no trace code).  kQ8: Q arrives already
+// quantized (FlashQ step 1 of the fused projection), so the prologue only
+// loads the int8 block and its scale.
+template <bool kTrace, bool kQ8>
 __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillArgs a) {
   __shared__ float lut[8];
   __shared__ float xmax[2][kPrefillWaves];  // per-wave P maxima, double-buffered
@@ -82,7 +86,12 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
   // lane (n + 32hf), k-step ks: channels 32ks + 16hf .. +15 of query qrow
   v4i qop[4];
   float sq;
-  {
+  if (kQ8) {
+    const int8_t* src = a.q8 + (((long)b * a.Hq + h) * a.nb * 64 + qrow) * 128 + 16 * hf;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) qop[ks] = *reinterpret_cast<const v4i*>(src + 32 * ks);
+    sq = a.sq[((long)b * a.Hq + h) * a.nb + i];
+  } else {
     uint4 raw[4][2];
     float amax = 0.0f;
     const uint4* src = a.q + (((long)b * a.Hq + h) * N + qrow) * 16;
@@ -318,9 +327,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hq * a.nb;
   if (a.trace)
-    hipLaunchKernelGGL(k_attn_prefill<true>, dim3(total), dim3(64 * kPrefillWaves), 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill<true, false>), dim3(total), dim3(64 * kPrefillWaves), 0,
+                       stream, a);
+  else if (a.q8)
+    hipLaunchKernelGGL((k_attn_prefill<false, true>), dim3(total), dim3(64 * kPrefillWaves), 0,
+                       stream, a);
   else
-    hipLaunchKernelGGL(k_attn_prefill<false>, dim3(total), dim3(64 * kPrefillWaves), 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill<false, false>), dim3(total), dim3(64 * kPrefillWaves), 0,
+                       stream, a);
   return hipGetLastError();
 }
 

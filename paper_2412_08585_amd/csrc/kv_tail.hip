@@ -231,10 +231,11 @@ __global__ __launch_bounds__(64) void k_decode_tail(DecodeArgs a) {
     if (lane == 0) sqs[r] = sq;
   }
   __syncthreads();
-  if (trow >= 0) {
+  if (kTrace && trow >= 0) {
+    const int tr = trow >= 0 ? trow : 0;
     reinterpret_cast<unsigned short*>(a.trace + TURBO_TRACE_Q8)[lane] =
-        reinterpret_cast<const unsigned short*>(q8s[trow])[lane];
-    if (lane == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = sqs[trow];
+        reinterpret_cast<const unsigned short*>(q8s[tr])[lane];
+    if (lane == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = sqs[tr];
   }
 
   // ---- scores (lane t = buffer row t), online step from m = -inf ------------

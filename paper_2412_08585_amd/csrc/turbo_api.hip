@@ -14,6 +14,7 @@
 #include "head_priority.hip"
 #include "kv_tail.hip"
 #include "sas_softmax.hip"
+#include "qkv_project.hip"
 
 namespace {
 
@@ -117,7 +118,8 @@ int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d
   return turbo::launch_quantize_kv(a, B, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
 }
 
-static int attn_prefill_impl(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
+static int attn_prefill_impl(const void* q, const int8_t* q8, const float* s_q,
+                             const int8_t* k8, const int8_t* v8, const float* s_k,
                              const float* s_v, int B, int Hq, int Hkv, int N, int d,
                              float sm_scale, int causal, void* o, float* lse,
                              unsigned char* trace, int tr_L, int tr_j, hipStream_t stream) {
@@ -125,13 +127,15 @@ static int attn_prefill_impl(const void* q, const int8_t* k8, const int8_t* v8, 
       d != TURBO_HEAD_DIM || !(sm_scale > 0.0f) || sm_scale > 3.0e38f)
     return TURBO_ERR_INVALID_ARG;
   if (B == 0 || N == 0) return TURBO_OK;
-  if (!q || !k8 || !v8 || !s_k || !s_v || !o) return TURBO_ERR_INVALID_ARG;
+  if (!(q || (q8 && s_q)) || !k8 || !v8 || !s_k || !s_v || !o) return TURBO_ERR_INVALID_ARG;
   const long tiles = (long)B * Hq * ((N + TURBO_BLOCK - 1) / TURBO_BLOCK);
   if (tiles > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
   int st = check_device();
   if (st != TURBO_OK) return st;
   turbo::PrefillArgs a{};
   a.q = static_cast<const uint4*>(q);
+  a.q8 = q ? nullptr : q8;
+  a.sq = q ? nullptr : s_q;
   a.k8 = k8;
   a.v8 = v8;
   a.sk = s_k;
@@ -154,8 +158,64 @@ static int attn_prefill_impl(const void* q, const int8_t* k8, const int8_t* v8, 
 int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
                        const float* s_v, int B, int Hq, int Hkv, int N, int d, float sm_scale,
                        int causal, void* o, float* lse, hipStream_t stream) {
-  return attn_prefill_impl(q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale, causal, o, lse,
-                           nullptr, -1, -1, stream);
+  return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
+                           causal, o, lse, nullptr, -1, -1, stream);
+}
+
+int turbo_attn_prefill_q8(const int8_t* q8, const float* s_q, const int8_t* k8, const int8_t* v8,
+                          const float* s_k, const float* s_v, int B, int Hq, int Hkv, int N,
+                          int d, float sm_scale, int causal, void* o, float* lse,
+                          hipStream_t stream) {
+  if (B > 0 && N > 0 && (!q8 || !s_q)) return TURBO_ERR_INVALID_ARG;
+  return attn_prefill_impl(nullptr, q8, s_q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
+                           causal, o, lse, nullptr, -1, -1, stream);
+}
+
+int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv, int d,
+                      int8_t* q8, float* s_q, int8_t* k8, int8_t* v8, float* s_k, float* s_v,
+                      const turbo_kv_cache* cache, const int32_t* block_table,
+                      const int32_t* group_table, int max_groups_per_seq, hipStream_t stream) {
+  if (B < 0 || N < 0 || D < 64 || D % 64 != 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || Hq < 1 ||
+      Hq % Hkv != 0 || d != TURBO_HEAD_DIM)
+    return TURBO_ERR_INVALID_ARG;
+  if (B == 0 || N == 0) return TURBO_OK;
+  if (!x || !w || !q8 || !s_q || !k8 || !v8 || !s_k || !s_v) return TURBO_ERR_INVALID_ARG;
+  const long ntile = (N + 255) / 256;
+  if ((long)B * ntile * (Hq + 2 * Hkv) > 0x7fffffffL || (long)B * N > 0x7fffffffL)
+    return TURBO_ERR_INVALID_ARG;
+  turbo::QkvArgs a{};
+  if (cache) {
+    if (!block_table || !group_table || max_groups_per_seq < N / TURBO_BLOCK)
+      return TURBO_ERR_INVALID_ARG;
+    int st = check_cache(cache, Hkv, &a.int2_mask, &a.page_bytes);
+    if (st != TURBO_OK) return st;
+    a.pages = cache->pages;
+    a.gmeta = cache->group_meta;
+    a.gscale = cache->group_scale;
+    a.num_pages = cache->num_pages;
+    a.num_slots = cache->num_group_slots;
+    a.block_table = block_table;
+    a.group_table = group_table;
+    a.max_groups = max_groups_per_seq;
+  }
+  int st = check_device();
+  if (st != TURBO_OK) return st;
+  a.x = static_cast<const uint4*>(x);
+  a.w = static_cast<const uint4*>(w);
+  a.B = B;
+  a.N = N;
+  a.D = D;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.ntile = (int)ntile;
+  a.q8 = q8;
+  a.sq = s_q;
+  a.k8 = k8;
+  a.v8 = v8;
+  a.sk = s_k;
+  a.sv = s_v;
+  return turbo::launch_qkv_project(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
 }
 
 int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
@@ -168,8 +228,8 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
     return TURBO_ERR_INVALID_ARG;
   // logical work index of (tb, th, ti): longest query blocks first
   const int tr_L = (nb - 1 - ti) * B * Hq + tb * Hq + th;
-  return attn_prefill_impl(q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale, causal, o, lse,
-                           static_cast<unsigned char*>(trace), tr_L, tj, stream);
+  return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
+                           causal, o, lse, static_cast<unsigned char*>(trace), tr_L, tj, stream);
 }
 
 int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {

@@ -54,6 +54,7 @@ class Workload:
     N: int            # sequence length (prefill) or cached KV length (decode)
     bits: str         # "int4" or "mixed"
     causal: bool = True
+    hidden: int = 0   # model width D of the QKV projection (projection workloads)
 
     @property
     def G(self) -> int:
@@ -83,6 +84,10 @@ WORKLOADS = {
     # Algorithm 3 on its own: the score rows of one Phi-3-medium-shaped
     # sequence (40 query heads x 4096 queries, 4096 keys each).
     "phi3m-sas-softmax-4k": Workload("phi3m-sas-softmax-4k", 5, "softmax", 1, 40, 10, 4096, "int4"),
+    # The QKV projection with FlashQ fused (Sec. 5.2) for the Phi-3-medium
+    # prefill: hidden width 5120 -> 40 query + 10 key + 10 value heads.
+    "phi3m-qkv-4k": Workload("phi3m-qkv-4k", 6, "projection", 4, 40, 10, 4096, "int4",
+                             hidden=5120),
 }
 
 # Standard deviation of the score stand-in: q.k / sqrt(128) for N(0,1) q and
@@ -193,3 +198,22 @@ def softmax_scores(w: Workload, device="cpu", rows: Optional[int] = None, row0: 
         g = _gen(device, seed_of(w.wid, (row0 + r) // 1024, 0, 4))
         out[r:r + n] = torch.randn(n, w.N, generator=g, device=device) * SCORE_STD
     return out
+
+
+def projection_inputs(w: Workload, device="cpu"):
+    """fp16 hidden states X [B][N][D] ~ N(0,1) and weights W [(Hq+2Hkv)128][D]
+    ~ N(0, 1/D), with 4 channels of every key head scaled by 10 (the outlier
+    channels of Fig. 3 come from the projection); X from seed_of(wid, b, 0, 5)
+    per sequence, W from seed_of(wid, 0, 0, 6)."""
+    D = w.hidden
+    F = (w.Hq + 2 * w.Hkv) * HEAD_DIM
+    x = torch.empty(w.B, w.N, D, dtype=torch.float16, device=device)
+    for b in range(w.B):
+        g = _gen(device, seed_of(w.wid, b, 0, 5))
+        x[b] = torch.randn(w.N, D, generator=g, device=device).half()
+    g = _gen(device, seed_of(w.wid, 0, 0, 6))
+    wt = torch.randn(F, D, generator=g, device=device) / float(np.sqrt(D))
+    for h in range(w.Hkv):
+        ch = torch.randperm(HEAD_DIM, generator=g, device=device)[:N_OUTLIER]
+        wt[(w.Hq + h) * HEAD_DIM + ch] *= OUTLIER_GAIN
+    return x, wt.half()
