@@ -62,18 +62,32 @@ __device__ __forceinline__ f32x16_t mfma_f16(uint4 a, uint4 b, f32x16_t c) {
                                                 __builtin_bit_cast(h8_t, b), c, 0, 0, 0);
 }
 
-// Work-group order: when the token tiles are a multiple of 8, XCD k (which
-// receives work-groups k, k+8, ...) runs every head of token tiles k, k+8,
-// ..., so the X rows of a tile are read by one XCD's L2.
+// Work-group order.  The dispatcher hands work-group x to XCD x % 8.  When
+// the token tiles are a multiple of 8, XCD k owns tiles k, k+8, ... and walks
+// them in blocks of (all its tiles) x (8 heads): the ~64 work-groups resident
+// on an XCD then share 8 X tiles and 8 W heads in its L2, so X is fetched
+// about nheads/8 times and W about ntiles/8 times in all (tile-major order
+// would fetch all of W once per tile).
 __device__ __forceinline__ void qkv_tile(int x, int ntiles, int nheads, int& tile, int& head) {
-  if (ntiles % 8 == 0) {
-    const int i = x / 8;
-    head = i % nheads;
-    tile = (i / nheads) * 8 + x % 8;
-  } else {
+  if (ntiles % 8 != 0) {
     head = x % nheads;
     tile = x / nheads;
+    return;
   }
+  const int k = x % 8, i = x / 8;
+  const int ntk = ntiles / 8;        // tiles of this XCD
+  const int full = nheads / 8;       // complete groups of 8 heads
+  int tl;
+  if (i < full * ntk * 8) {
+    const int hg = i / (ntk * 8), rem = i % (ntk * 8);
+    tl = rem / 8;
+    head = 8 * hg + rem % 8;
+  } else {
+    const int r = nheads - 8 * full, rem = i - full * ntk * 8;
+    tl = rem / r;
+    head = 8 * full + rem % r;
+  }
+  tile = tl * 8 + k;
 }
 
 __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
@@ -107,20 +121,18 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x16_t{};
 
-  // A holds the X slice of the current step; each k16 slot is refilled with
-  // the next step's slice as soon as its MFMAs are issued (one step of
-  // prefetch without a second register set).
-  // A holds the X slice of the current step; each k16 slot is refilled with
-  // the next step's slice as soon as its MFMAs are issued (one step of
-  // prefetch without a second register set).  The W slice of the next step
-  // is loaded at the top of the step and stored to the other LDS stage at its
-  // end.
-  uint4 A[2][4];
+  // X operands in two half-step register sets: P holds k16-slots 0-1 of a
+  // step, R slots 2-3.  R is loaded at the top of its step and P (for the
+  // next step) after slots 0-1 are done, so each load has half a step of
+  // MFMAs to land, and each set is waited for only when it is used.  The W
+  // slice of the next step is loaded at the top and stored to the other LDS
+  // stage at the end of the step.
+  uint4 P[2][2], R[2][2];
   const int nk = a.D / 64;
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
-    for (int s = 0; s < 4; ++s) A[mb][s] = xr[mb][s];
+    for (int mb = 0; mb < 2; ++mb) P[mb][j] = xr[mb][j];
   {
     const uint4 w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
     uint4* d = reinterpret_cast<uint4*>(wdst);
@@ -136,22 +148,35 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
     const int st = kk & 1, kn = min(kk + 1, nk - 1);
     const uint4* wn = wr + kn * 8;
     const uint4 w0 = wn[0], w1 = wn[1], w2 = wn[2], w3 = wn[3];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) R[mb][j] = xr[mb][kk * 8 + 2 + j];
     // keep the prefetches where they are: issued early, their latency hides
-    // behind this step's MFMAs (the scheduler would otherwise sink them)
+    // behind MFMAs (the scheduler would otherwise sink them to their use)
     __builtin_amdgcn_sched_barrier(0);
     const uint8_t* base = lds + st * kWStage + m * kWRow + 64 * h;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) {
         const uint4 bv = *reinterpret_cast<const uint4*>(base + nb * 32 * kWRow + 16 * s);
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) acc[mb][nb] = mfma_f16(A[mb][s], bv, acc[mb][nb]);
+        for (int mb = 0; mb < 2; ++mb) acc[mb][nb] = mfma_f16(P[mb][s], bv, acc[mb][nb]);
       }
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) A[mb][s] = xr[mb][kn * 8 + s];
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) P[mb][j] = xr[mb][kn * 8 + j];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 2; s < 4; ++s)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const uint4 bv = *reinterpret_cast<const uint4*>(base + nb * 32 * kWRow + 16 * s);
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) acc[mb][nb] = mfma_f16(R[mb][s - 2], bv, acc[mb][nb]);
+      }
     uint4* d = reinterpret_cast<uint4*>(wdst + (st ^ 1) * kWStage);
     d[0] = w0;
     d[1] = w1;

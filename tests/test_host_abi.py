@@ -269,3 +269,38 @@ def test_cache_format_round_trip(bits):
     else:
         assert first == (u["kc"][0, 0] | (u["kc"][0, 1] << 2) | (u["kc"][0, 2] << 4)
                          | (u["kc"][0, 3] << 6))
+
+
+def _qkv_tile(x, ntiles, nheads):
+    """Host replica of the work-group order of k_qkv_project (qkv_tile)."""
+    if ntiles % 8:
+        return x // nheads, x % nheads
+    k, i = x % 8, x // 8
+    ntk, full = ntiles // 8, nheads // 8
+    if i < full * ntk * 8:
+        hg, rem = divmod(i, ntk * 8)
+        tl, head = rem // 8, 8 * hg + rem % 8
+    else:
+        r = nheads - 8 * full
+        rem = i - full * ntk * 8
+        tl, head = rem // r, 8 * full + rem % r
+    return tl * 8 + k, head
+
+
+@pytest.mark.parametrize("ntiles,nheads", [(64, 60), (8, 3), (16, 8), (8, 17), (24, 60), (3, 5),
+                                           (8, 1), (64, 48), (1, 1)])
+def test_projection_work_order_is_a_bijection(ntiles, nheads):
+    """Every (token tile, head) unit gets exactly one work-group; with 8 | ntiles,
+    XCD k (work-groups x = k mod 8) runs only tiles = k mod 8, in blocks of
+    consecutive work-groups that cover all of its tiles and at most 8 heads."""
+    got = [_qkv_tile(x, ntiles, nheads) for x in range(ntiles * nheads)]
+    assert sorted(got) == [(t, h) for t in range(ntiles) for h in range(nheads)]
+    if ntiles % 8 == 0:
+        ntk = ntiles // 8
+        for k in range(8):
+            seq = [got[x] for x in range(k, ntiles * nheads, 8)]
+            assert all(t % 8 == k for t, _ in seq)
+            for b0 in range(0, len(seq), 8 * ntk):
+                blk = seq[b0:b0 + 8 * ntk]
+                assert len({h for _, h in blk}) <= 8
+                assert {t for t, _ in blk} == set(range(k, ntiles, 8))
