@@ -111,9 +111,12 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
     const int n = min(n0 + 32 * mb + m, a.N - 1);
     xr[mb] = a.x + ((long)b * a.N + n) * dq + 4 * h;
   }
-  const int fr = tid >> 1, fh = tid & 1;
-  const uint4* wr = a.w + ((long)head * 128 + fr) * dq + 4 * fh;
-  uint8_t* wdst = lds + fr * kWRow + 64 * fh;
+  // W staging: thread (row 32 j + tid/8, 16-byte chunk tid%8) for j = 0..3, so
+  // one load instruction reads 8 whole 128-byte rows of the slice
+  const int wrow = tid >> 3, wc = tid & 7;
+  const uint4* wr = a.w + ((long)head * 128 + wrow) * dq + wc;
+  const long wj = 32L * dq;  // 32 rows
+  uint8_t* wdst = lds + wrow * kWRow + 16 * wc;
 
   f32x16_t acc[2][4];
 #pragma unroll
@@ -134,12 +137,11 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) P[mb][j] = xr[mb][j];
   {
-    const uint4 w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
-    uint4* d = reinterpret_cast<uint4*>(wdst);
-    d[0] = w0;
-    d[1] = w1;
-    d[2] = w2;
-    d[3] = w3;
+    const uint4 w0 = wr[0], w1 = wr[wj], w2 = wr[2 * wj], w3 = wr[3 * wj];
+    *reinterpret_cast<uint4*>(wdst) = w0;
+    *reinterpret_cast<uint4*>(wdst + 32 * kWRow) = w1;
+    *reinterpret_cast<uint4*>(wdst + 64 * kWRow) = w2;
+    *reinterpret_cast<uint4*>(wdst + 96 * kWRow) = w3;
   }
   __syncthreads();
   // every load is issued on every path (the index is clamped at the end), so
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
   for (int kk = 0; kk < nk; ++kk) {
     const int st = kk & 1, kn = min(kk + 1, nk - 1);
     const uint4* wn = wr + kn * 8;
-    const uint4 w0 = wn[0], w1 = wn[1], w2 = wn[2], w3 = wn[3];
+    const uint4 w0 = wn[0], w1 = wn[wj], w2 = wn[2 * wj], w3 = wn[3 * wj];
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -177,11 +179,11 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) acc[mb][nb] = mfma_f16(R[mb][s - 2], bv, acc[mb][nb]);
       }
-    uint4* d = reinterpret_cast<uint4*>(wdst + (st ^ 1) * kWStage);
-    d[0] = w0;
-    d[1] = w1;
-    d[2] = w2;
-    d[3] = w3;
+    uint8_t* d = wdst + (st ^ 1) * kWStage;
+    *reinterpret_cast<uint4*>(d) = w0;
+    *reinterpret_cast<uint4*>(d + 32 * kWRow) = w1;
+    *reinterpret_cast<uint4*>(d + 64 * kWRow) = w2;
+    *reinterpret_cast<uint4*>(d + 96 * kWRow) = w3;
     __syncthreads();
   }
 
