@@ -368,7 +368,7 @@ int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, float* prio
   int st = check_device();
   if (st != TURBO_OK) return st;
   turbo::PriorityArgs a{};
-  a.k = static_cast<const uint2*>(k);
+  a.k = static_cast<const uint4*>(k);
   a.B = B;
   a.Hkv = Hkv;
   a.N = N;
