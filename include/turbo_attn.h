@@ -202,6 +202,21 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
                        int causal, void* o, float* lse, hipStream_t stream);
 
 /*
+ * turbo_attn_prefill_blocks — turbo_attn_prefill with another query block
+ * size B_r (Table 3 evaluates several): Q is quantized per block_rows rows
+ * of a head and the P scale covers the block_rows x 64 tile; K and V keep
+ * their 64-token blocks (B_c = 64).  block_rows = 64 is turbo_attn_prefill.
+ * With B_r = 128 and causal masking, a 32-row quarter of a block that sees no
+ * key of a tile leaves its rows untouched (Algorithm 1 processes no such
+ * pair).  INVALID_ARG for block_rows not in {32, 64, 128}; other arguments
+ * and errors as turbo_attn_prefill.
+ */
+int turbo_attn_prefill_blocks(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
+                              const float* s_v, int B, int Hq, int Hkv, int N, int d,
+                              float sm_scale, int causal, int block_rows, void* o, float* lse,
+                              hipStream_t stream);
+
+/*
  * turbo_attn_prefill_q8 — turbo_attn_prefill with Q already quantized
  * (FlashQ step 1 done by turbo_qkv_project): the prologue loads the int8
  * block and its scale instead of quantizing fp16 Q.  Given the codes and

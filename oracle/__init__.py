@@ -70,6 +70,8 @@ def lib():
             "or_sas_softmax_rows": ([P, I, I, P], None),
             "or_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P], None),
             "or_attn_prefill": ([P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P, I, I], None),
+            "or_attn_prefill_blocks": ([P, P, P, I, I, I, I, I, F, I, _Opts, I, P, P, P, I, I],
+                                       None),
             "or_tail_init": ([P, P, I, I, I, I, P, P, P, P, P, P], None),
             "or_append_kv": ([P, P, I, I, I, P, P, I, P, P, P, P, P, P, P, P, P, P, P, P], None),
             "or_attn_decode": ([P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P,
@@ -221,11 +223,12 @@ def _trace(d: int, sel):
 
 
 def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = True,
-                 sas: bool = True, trace=None, qblocks=None):
+                 sas: bool = True, trace=None, qblocks=None, block_rows: int = 64):
     """Algorithm 1.  q [B][Hq][N][d], k, v [B][Hkv][N][d] (fp16 values).
     Returns (o float64 [B][Hq][N][d] = O/l before fp16 rounding, lse float64
     [B][Hq][N]) and, with trace=(b, h, i, j), a dict of that tile's integers.
-    qblocks=(i0, i1) restricts the work to query blocks i0..i1-1 (other rows NaN)."""
+    qblocks=(i0, i1) restricts the work to query blocks i0..i1-1 (other rows NaN).
+    block_rows = B_r (Table 3): the query block of the Q scale and P tile."""
     q, k, v = _f32(q), _f32(k), _f32(v)
     B, Hq, N, d = q.shape
     Hkv = k.shape[1]
@@ -233,9 +236,11 @@ def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = Tr
     lse = np.full((B, Hq, N), np.nan, np.float64)
     tr, bufs = _trace(d, trace)
     i0, i1 = (-1, -1) if qblocks is None else qblocks
-    lib().or_attn_prefill(_p(q), _p(k), _p(v), B, Hq, Hkv, N, d, float(np.float32(sm_scale)),
-                          int(causal), _Opts(int(quant), int(sas)), _p(o), _p(lse),
-                          ctypes.byref(tr) if tr is not None else None, int(i0), int(i1))
+    assert block_rows in (32, 64, 128) and (tr is None or block_rows == 64)
+    lib().or_attn_prefill_blocks(_p(q), _p(k), _p(v), B, Hq, Hkv, N, d,
+                                 float(np.float32(sm_scale)), int(causal),
+                                 _Opts(int(quant), int(sas)), int(block_rows), _p(o), _p(lse),
+                                 ctypes.byref(tr) if tr is not None else None, int(i0), int(i1))
     if tr is None:
         return o, lse
     bufs.update(hit=tr.hit, sq=np.float32(tr.sq), pmax=np.float32(tr.pmax))

@@ -39,6 +39,8 @@
 #define OR_NR 6
 /* Query/key block B_r = B_c = 64 and step-2 group length (Sec. 5.2). */
 #define OR_BS 64
+/* Largest query block of the block-size variants (Table 3: B_r up to 128). */
+#define OR_MAXBR 128
 /* POLY(x) = -0.1025 x^3 + 0.4626 x^2 - 0.9922 x + 0.9996 (Sec. 4). */
 static const float OR_C3 = -0.1025f, OR_C2 = 0.4626f, OR_C1 = -0.9922f, OR_C0 = 0.9996f;
 
@@ -250,8 +252,8 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
                     const unsigned char* vis, int ldsc, const int8_t* vq, float sv,
                     const float* vf, int d, float* p, double* pd, int8_t* qp,
                     or_trace* tr) {
-  double alpha[OR_BS];
-  int act[OR_BS];
+  double alpha[OR_MAXBR];
+  int act[OR_MAXBR];
   float pmax = 0.0f;
   for (int r = 0; r < nr; ++r) {
     act[r] = 0;
@@ -322,25 +324,30 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
  * accumulator update with the inverse of diag(SAS(m_old - m_new)), which
  * would not compute a softmax and disagrees with the l update next to it, so
  * O is multiplied by that factor; when the maximum does not move the factor
- * is SAS(0) as written. */
-void or_attn_prefill(const float* q, const float* k, const float* v, int B, int Hq, int Hkv,
-                     int N, int d, float sm_scale, int causal, or_opts opts, double* o,
-                     double* lse, or_trace* tr, int i0, int i1) {
-  const int G = Hq / Hkv, nb = (N + OR_BS - 1) / OR_BS;
+ * is SAS(0) as written.
+ * Block sizes (Table 3 varies them): Q is quantized per br rows of a head
+ * (br = B_r in {32, 64, 128}) and the P scale covers the br x 64 tile; K and
+ * V keep their 64-token blocks (B_c = 64).  Query blocks i0..i1 count br-row
+ * blocks.  The trace is produced for br = 64 only. */
+void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int B, int Hq,
+                            int Hkv, int N, int d, float sm_scale, int causal, or_opts opts,
+                            int br, double* o, double* lse, or_trace* tr, int i0, int i1) {
+  const int G = Hq / Hkv, nb = (N + OR_BS - 1) / OR_BS, nbq = (N + br - 1) / br;
+  if (br != OR_BS) tr = NULL; /* the trace layout is that of 64-row blocks */
 #pragma omp parallel
   {
     int8_t* k8 = malloc((size_t)N * d + 1);
     int8_t* v8 = malloc((size_t)N * d + 1);
     float* sk = malloc(sizeof(float) * (nb + 1));
     float* sv = malloc(sizeof(float) * (nb + 1));
-    int8_t* q8 = malloc((size_t)OR_BS * d);
-    double* sc = malloc(sizeof(double) * OR_BS * OR_BS);
-    unsigned char* vis = malloc((size_t)OR_BS * OR_BS);
-    float* p = malloc(sizeof(float) * OR_BS * OR_BS);
-    double* pd = malloc(sizeof(double) * OR_BS * OR_BS);
-    int8_t* qp = malloc((size_t)OR_BS * OR_BS);
-    double* Obuf = malloc(sizeof(double) * OR_BS * d);
-    or_row rows[OR_BS];
+    int8_t* q8 = malloc((size_t)br * d);
+    double* sc = malloc(sizeof(double) * br * OR_BS);
+    unsigned char* vis = malloc((size_t)br * OR_BS);
+    float* p = malloc(sizeof(float) * br * OR_BS);
+    double* pd = malloc(sizeof(double) * br * OR_BS);
+    int8_t* qp = malloc((size_t)br * OR_BS);
+    double* Obuf = malloc(sizeof(double) * br * d);
+    or_row rows[OR_MAXBR];
 #pragma omp for collapse(2) schedule(dynamic)
     for (int b = 0; b < B; ++b)
       for (int h = 0; h < Hq; ++h) {
@@ -354,8 +361,8 @@ void or_attn_prefill(const float* q, const float* k, const float* v, int B, int 
             sk[j] = or_block_quant(kk + (size_t)r0 * d, (long)nr * d, k8 + (size_t)r0 * d);
             sv[j] = or_block_quant(vv + (size_t)r0 * d, (long)nr * d, v8 + (size_t)r0 * d);
           }
-        for (int i = i0 < 0 ? 0 : i0; i < (i1 < 0 || i1 > nb ? nb : i1); ++i) {
-          const int q0 = i * OR_BS, nq = (N - q0) < OR_BS ? (N - q0) : OR_BS;
+        for (int i = i0 < 0 ? 0 : i0; i < (i1 < 0 || i1 > nbq ? nbq : i1); ++i) {
+          const int q0 = i * br, nq = (N - q0) < br ? (N - q0) : br;
           float sq = 0.0f; /* Q_i^{q1} (eq. step1bpq) */
           if (opts.quant) sq = or_block_quant(qq + (size_t)q0 * d, (long)nq * d, q8);
           const int trq = tr && tr->b == b && tr->h == h && tr->i == i;
@@ -368,7 +375,7 @@ void or_attn_prefill(const float* q, const float* k, const float* v, int B, int 
             rows[r].l = 0.0;
             rows[r].O = Obuf + (size_t)r * d;
           }
-          memset(Obuf, 0, sizeof(double) * OR_BS * d);
+          memset(Obuf, 0, sizeof(double) * br * d);
           for (int j = 0; j < nb; ++j) {
             const int k0 = j * OR_BS, nk = (N - k0) < OR_BS ? (N - k0) : OR_BS;
             if (causal && k0 > q0 + nq - 1) break;
@@ -407,6 +414,14 @@ void or_attn_prefill(const float* q, const float* k, const float* v, int B, int 
     free(k8); free(v8); free(sk); free(sv); free(q8); free(sc); free(vis); free(p); free(pd);
     free(qp); free(Obuf);
   }
+}
+
+/* Algorithm 1 with the paper's query/key blocks B_r = B_c = 64. */
+void or_attn_prefill(const float* q, const float* k, const float* v, int B, int Hq, int Hkv,
+                     int N, int d, float sm_scale, int causal, or_opts opts, double* o,
+                     double* lse, or_trace* tr, int i0, int i1) {
+  or_attn_prefill_blocks(q, k, v, B, Hq, Hkv, N, d, sm_scale, causal, opts, OR_BS, o, lse, tr,
+                         i0, i1);
 }
 
 /* ---- Algorithm 2: decode over the compressed cache -------------------- */

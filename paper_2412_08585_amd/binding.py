@@ -63,6 +63,7 @@ def lib() -> ctypes.CDLL:
             "turbo_int2_heads": ([P, I, I, P], I),
             "turbo_sas_softmax": ([P, P, ctypes.c_int64, I, P], I),
             "turbo_attn_prefill_q8": ([P, P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
+            "turbo_attn_prefill_blocks": ([P, P, P, P, P, I, I, I, I, I, F, I, I, P, P, P], I),
             "turbo_qkv_project": ([P, P, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P], I),
             "turbo_decode_auto_split": ([I, I, I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
@@ -208,17 +209,25 @@ def turbo_quantize_kv(k: torch.Tensor, v: torch.Tensor, cache: Optional[PagedKVC
 
 
 def turbo_attn_prefill(q: torch.Tensor, k8, v8, s_k, s_v, sm_scale: Optional[float] = None,
-                       causal: bool = True, return_lse: bool = False, out=None):
+                       causal: bool = True, return_lse: bool = False, out=None,
+                       block_rows: int = 64):
     """Algorithm 1 prefill.  q fp16 [B][Hq][N][128]; k8/v8/s_k/s_v from
-    turbo_quantize_kv.  Returns o fp16 [B][Hq][N][128] (and lse fp32)."""
+    turbo_quantize_kv.  Returns o fp16 [B][Hq][N][128] (and lse fp32).
+    block_rows = B_r in {32, 64, 128} (Table 3); 64 is the default path."""
     B, Hq, N, d = q.shape
     Hkv = s_k.shape[1]
     sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty(B, Hq, N, dtype=torch.float32, device=q.device) if return_lse else None
-    st = lib().turbo_attn_prefill(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B, Hq, Hkv,
-                                  N, d, sm, int(bool(causal)), _ptr(o), _ptr(lse),
-                                  _stream(q.device))
+    if block_rows == 64:
+        st = lib().turbo_attn_prefill(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B, Hq,
+                                      Hkv, N, d, sm, int(bool(causal)), _ptr(o), _ptr(lse),
+                                      _stream(q.device))
+    else:
+        st = lib().turbo_attn_prefill_blocks(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B,
+                                             Hq, Hkv, N, d, sm, int(bool(causal)),
+                                             int(block_rows), _ptr(o), _ptr(lse),
+                                             _stream(q.device))
     _check(st, "turbo_attn_prefill")
     return (o, lse) if return_lse else o
 

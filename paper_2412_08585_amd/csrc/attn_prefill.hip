@@ -1,12 +1,16 @@
 // TurboAttention prefill on gfx950 (Algorithm 1): int8 QK^T and PV on the
 // 32x32x32 i8 MFMA, SAS online softmax in fp32 on the VALU.
 //
-// A workgroup of two waves owns one (sequence b, query head h, 64-query
-// block i); wave qh holds queries 64i + 32qh .. +31 and both run over the key
-// blocks j (j <= i when causal).  The P scale of Algorithm 1 covers the whole
-// 64x64 tile, so the two waves exchange their partial maxima through LDS once
-// per tile.  32 queries per wave keep a wave under 256 VGPRs (two waves per
-// SIMD, MFMA results in VGPRs).
+// A workgroup of B_r / 32 waves owns one (sequence b, query head h, query
+// block i of B_r rows); wave qh holds queries B_r i + 32qh .. +31 and all run
+// over the key blocks j (those with a key at or before the block's last row
+// when causal).  B_r = 64 (two waves) is the paper's setting; 32 and 128 are
+// its Table 3 variants.  The Q scale and the P scale of Algorithm 1 cover the
+// whole B_r x 64 tile, so the waves exchange their partial maxima through LDS
+// (once for Q, once per tile for P).  32 queries per wave keep a wave under
+// 256 VGPRs (two waves per SIMD, MFMA results in VGPRs).  With B_r = 128 the
+// first waves of a diagonal block see no key of its last tile; their rows
+// keep m and l unchanged there (factor 1, not SAS(0)).
 //
 // Register layout.  The scores are computed transposed, S^T = K Q^T, so that
 // each lane holds one query column:  for the 32x32 output block kb (32-key
@@ -36,6 +40,8 @@ struct PrefillArgs {
   const float* sk;     // [B][Hkv][nb]
   const float* sv;
   int B, Hq, Hkv, N, nb;
+  int waves;           // 1, 2 or 4: B_r = 32 * waves
+  int nbq;             // query blocks of B_r rows
   float sm_scale;
   int causal;
   uint2* o;            // fp16 [B][Hq][N][128] (as 4-half units)
@@ -43,8 +49,6 @@ struct PrefillArgs {
   unsigned char* trace;  // test hook: integers of tile (logical index tr_L, key block tr_j)
   int tr_L, tr_j;
 };
-
-constexpr int kPrefillWaves = 2;
 
 // Logical work-group order L: longest causal query blocks first, and within
 // a query block the G query heads of one KV head next to each other.  The
@@ -64,23 +68,25 @@ __device__ __forceinline__ int prefill_order(int x, int total, int G) {
 // (the production instance carries no trace code).  kQ8: Q arrives already
 // quantized (FlashQ step 1 of the fused projection), so the prologue only
 // loads the int8 block and its scale.
-template <bool kTrace, bool kQ8>
-__global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillArgs a) {
+template <bool kTrace, bool kQ8, int kWaves>
+__global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) {
+  constexpr int kBr = 32 * kWaves;
   __shared__ float lut[8];
-  __shared__ float xmax[2][kPrefillWaves];  // per-wave P maxima, double-buffered
+  __shared__ float xmax[2][kWaves];  // per-wave P maxima, double-buffered
   const int tid = threadIdx.x;
   const int lane = tid & 63, qh = tid >> 6;
   if (tid < 8) lut[tid] = kLut[tid];
   __syncthreads();
 
   const int BH = a.B * a.Hq;
-  const int L = prefill_order(blockIdx.x, BH * a.nb, a.Hq / a.Hkv);
-  const int i = a.nb - 1 - L / BH;  // longest causal rows first
+  const int L = prefill_order(blockIdx.x, BH * a.nbq, a.Hq / a.Hkv);
+  const int i = a.nbq - 1 - L / BH;  // longest causal rows first
   const int b = (L % BH) / a.Hq, h = L % a.Hq;
   const int G = a.Hq / a.Hkv, kh = h / G;
   const int n = lane & 31, hf = lane >> 5;
   const int N = a.N;
-  const int qrow = 64 * i + 32 * qh + n;
+  const int row0 = kBr * i + 32 * qh;  // first query row of this wave
+  const int qrow = row0 + n;
 
   // ---- Q_i -> int8 (eq. step1bpq; scale over the 64-row block) ----------
   // lane (n + 32hf), k-step ks: channels 32ks + 16hf .. +15 of query qrow
@@ -105,10 +111,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
         for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
       }
     amax = wave_max_fast(amax);
-    if (lane == 0) xmax[0][qh] = amax;
-    __syncthreads();
-    amax = fmaxf(xmax[0][0], xmax[0][1]);
-    __syncthreads();
+    if (kWaves > 1) {
+      if (lane == 0) xmax[0][qh] = amax;
+      __syncthreads();
+      amax = xmax[0][0];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) amax = fmaxf(amax, xmax[0][w]);
+      __syncthreads();
+    }
     float inv = 0.0f;
     sq = 0.0f;
     if (amax > 0.0f) {
@@ -180,7 +190,8 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
     for (int r = 0; r < 16; ++r) O[cb][r] = 0.0f;
   float mrow = -INFINITY, lhalf = 0.0f, beta = 1.0f;
 
-  const int jend = a.causal ? i : a.nb - 1;
+  // last key block: the one holding the block's last row when causal
+  const int jend = a.causal ? min(a.nb - 1, (kBr * i + kBr - 1) / 64) : a.nb - 1;
   // Software pipeline per tile j:  softmax of S_j on the VALU (K of tile j+1
   // already in flight) -> tile maximum exchange -> PV_j and then S_{j+1} on
   // the MFMA -> accumulator update on the VALU while S_{j+1} is computed.
@@ -210,8 +221,9 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) P[kb][r] = (float)S[kb][r] * c;
-    // masking only on the diagonal tile and on tiles that reach past N
-    if ((a.causal && j == i) || (64 * j + 64 > N) || (64 * i + 64 > N)) {
+    // masking only where a key can lie after one of this wave's rows (the
+    // diagonal) and on tiles that reach past N
+    if ((a.causal && 64 * j + 63 > row0) || (64 * j + 64 > N) || (row0 + 32 > N)) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -239,14 +251,21 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
         rs += p;
         pmax = fmaxf(pmax, p);
       }
-    const float alpha = sas_y(mnew - mold, lut);  // 0 when mold = -inf
+    float alpha = sas_y(mnew - mold, lut);  // 0 when mold = -inf
+    // with B_r = 128 a wave can see no key of the tile (its rows all precede
+    // it): the rows are not processed, so nothing is rescaled
+    if (kWaves > 2 && a.causal && 64 * j > row0 + 31) alpha = 1.0f;
     lhalf = alpha * lhalf + rs;
     mrow = mnew;
     // ---- tile maximum of P~ over both waves ----------------------------
     pmax = wave_max_fast(pmax);
-    if (lane == 0) xmax[j & 1][qh] = pmax;
-    __syncthreads();
-    pmax = fmaxf(xmax[j & 1][0], xmax[j & 1][1]);
+    if (kWaves > 1) {
+      if (lane == 0) xmax[j & 1][qh] = pmax;
+      __syncthreads();
+      pmax = xmax[j & 1][0];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) pmax = fmaxf(pmax, xmax[j & 1][w]);
+    }
     // ---- rescale factor: O = beta * Ost --------------------------------
     float nbeta = beta * alpha;
     if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
@@ -325,16 +344,17 @@ __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_attn_prefill(PrefillA
 }
 
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
-  const int total = a.B * a.Hq * a.nb;
-  if (a.trace)
-    hipLaunchKernelGGL((k_attn_prefill<true, false>), dim3(total), dim3(64 * kPrefillWaves), 0,
-                       stream, a);
+  const int total = a.B * a.Hq * a.nbq;
+  if (a.trace)  // test hook: B_r = 64 only
+    hipLaunchKernelGGL((k_attn_prefill<true, false, 2>), dim3(total), dim3(128), 0, stream, a);
   else if (a.q8)
-    hipLaunchKernelGGL((k_attn_prefill<false, true>), dim3(total), dim3(64 * kPrefillWaves), 0,
-                       stream, a);
+    hipLaunchKernelGGL((k_attn_prefill<false, true, 2>), dim3(total), dim3(128), 0, stream, a);
+  else if (a.waves == 1)
+    hipLaunchKernelGGL((k_attn_prefill<false, false, 1>), dim3(total), dim3(64), 0, stream, a);
+  else if (a.waves == 4)
+    hipLaunchKernelGGL((k_attn_prefill<false, false, 4>), dim3(total), dim3(256), 0, stream, a);
   else
-    hipLaunchKernelGGL((k_attn_prefill<false, false>), dim3(total), dim3(64 * kPrefillWaves), 0,
-                       stream, a);
+    hipLaunchKernelGGL((k_attn_prefill<false, false, 2>), dim3(total), dim3(128), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -121,14 +121,15 @@ int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d
 static int attn_prefill_impl(const void* q, const int8_t* q8, const float* s_q,
                              const int8_t* k8, const int8_t* v8, const float* s_k,
                              const float* s_v, int B, int Hq, int Hkv, int N, int d,
-                             float sm_scale, int causal, void* o, float* lse,
+                             float sm_scale, int causal, int block_rows, void* o, float* lse,
                              unsigned char* trace, int tr_L, int tr_j, hipStream_t stream) {
   if (B < 0 || N < 0 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || Hq / Hkv > TURBO_MAX_GQA ||
       d != TURBO_HEAD_DIM || !(sm_scale > 0.0f) || sm_scale > 3.0e38f)
     return TURBO_ERR_INVALID_ARG;
   if (B == 0 || N == 0) return TURBO_OK;
   if (!(q || (q8 && s_q)) || !k8 || !v8 || !s_k || !s_v || !o) return TURBO_ERR_INVALID_ARG;
-  const long tiles = (long)B * Hq * ((N + TURBO_BLOCK - 1) / TURBO_BLOCK);
+  if (block_rows != 32 && block_rows != 64 && block_rows != 128) return TURBO_ERR_INVALID_ARG;
+  const long tiles = (long)B * Hq * ((N + block_rows - 1) / block_rows);
   if (tiles > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
   int st = check_device();
   if (st != TURBO_OK) return st;
@@ -145,6 +146,8 @@ static int attn_prefill_impl(const void* q, const int8_t* q8, const float* s_q,
   a.Hkv = Hkv;
   a.N = N;
   a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.waves = block_rows / 32;
+  a.nbq = (N + block_rows - 1) / block_rows;
   a.sm_scale = sm_scale;
   a.causal = causal ? 1 : 0;
   a.o = static_cast<uint2*>(o);
@@ -159,7 +162,15 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
                        const float* s_v, int B, int Hq, int Hkv, int N, int d, float sm_scale,
                        int causal, void* o, float* lse, hipStream_t stream) {
   return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, o, lse, nullptr, -1, -1, stream);
+                           causal, 64, o, lse, nullptr, -1, -1, stream);
+}
+
+int turbo_attn_prefill_blocks(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
+                              const float* s_v, int B, int Hq, int Hkv, int N, int d,
+                              float sm_scale, int causal, int block_rows, void* o, float* lse,
+                              hipStream_t stream) {
+  return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
+                           causal, block_rows, o, lse, nullptr, -1, -1, stream);
 }
 
 int turbo_attn_prefill_q8(const int8_t* q8, const float* s_q, const int8_t* k8, const int8_t* v8,
@@ -168,7 +179,7 @@ int turbo_attn_prefill_q8(const int8_t* q8, const float* s_q, const int8_t* k8, 
                           hipStream_t stream) {
   if (B > 0 && N > 0 && (!q8 || !s_q)) return TURBO_ERR_INVALID_ARG;
   return attn_prefill_impl(nullptr, q8, s_q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, o, lse, nullptr, -1, -1, stream);
+                           causal, 64, o, lse, nullptr, -1, -1, stream);
 }
 
 int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv, int d,
@@ -229,7 +240,8 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
   // logical work index of (tb, th, ti): longest query blocks first
   const int tr_L = (nb - 1 - ti) * B * Hq + tb * Hq + th;
   return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, o, lse, static_cast<unsigned char*>(trace), tr_L, tj, stream);
+                           causal, 64, o, lse, static_cast<unsigned char*>(trace), tr_L, tj,
+                           stream);
 }
 
 int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {

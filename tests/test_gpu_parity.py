@@ -163,6 +163,39 @@ def test_prefill_parity(orc, ta, dev, B, Hq, Hkv, N, causal):
          f"{np.linalg.norm(ro - ex) / np.linalg.norm(ex):.3e}")
 
 
+BLOCK_CASES = [
+    # B, Hq, Hkv, N, causal, block_rows
+    (2, 8, 2, 64 * 3 + 40, True, 32),
+    (2, 8, 2, 64 * 3 + 40, True, 128),
+    (1, 2, 1, 130, False, 32),
+    (1, 2, 1, 130, False, 128),
+    (1, 4, 4, 512, True, 128),
+    (1, 16, 1, 200, True, 128),
+    (1, 3, 3, 64 * 2 + 63, False, 128),
+    (1, 2, 2, 1, True, 32),
+    (1, 2, 2, 97, True, 128),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,N,causal,br", BLOCK_CASES)
+def test_prefill_block_sizes(orc, ta, dev, B, Hq, Hkv, N, causal, br):
+    """Table 3's query block sizes: B_r = 32 (one wave per work-group) and
+    B_r = 128 (four waves sharing the Q scale and the P scale of the block)."""
+    _log(f"prefill B_r={br} B={B} Hq={Hq} Hkv={Hkv} N={N} causal={causal}")
+    q = _rand((B, Hq, N, 128), 310 + N)
+    k = _rand((B, Hkv, N, 128), 410 + N)
+    v = _rand((B, Hkv, N, 128), 510 + N)
+    k[..., 3] *= 10
+    (k8, v8, sk, sv) = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
+    o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, 1 / np.sqrt(128), causal,
+                                   return_lse=True, block_rows=br)
+    torch.cuda.synchronize()
+    ro, rl = orc.attn_prefill(q, k, v, 1 / np.sqrt(128), causal, block_rows=br)
+    err = _cmp_o(o, ro, f"prefill B_r={br} O")
+    _cmp_lse(lse, rl, f"prefill B_r={br} lse")
+    _log(f"  vs oracle {err:.2e}")
+
+
 def test_prefill_zero_query_block(orc, ta, dev):
     """An all-zero query block has s_Q = 0: every score is 0 (closed form)."""
     N = 64 * 3
@@ -283,6 +316,30 @@ def test_full_size_prefill(orc, ta, dev, name, qblocks):
         _cmp_o(o[b:b + 1, h * w.G:(h + 1) * w.G, rows], ro[:, :, rows], f"{name} O unit {b},{h}")
         _cmp_lse(lse[b:b + 1, h * w.G:(h + 1) * w.G, rows], rl[:, :, rows], f"{name} lse")
         _log(f"  unit ({b},{h}) ok")
+    del q, k, v, k8, v8, o
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("br,qblocks", [(32, (126, 128)), (128, (30, 32)), (128, (0, 1))])
+def test_full_size_prefill_block_sizes(orc, ta, dev, br, qblocks):
+    """The Phi-3-medium prefill (4 x 4096, 40 / 10 heads) at B_r = 32 and 128,
+    run in full; one (sequence, KV head) unit's last or first query blocks
+    recomputed by the oracle."""
+    from paper_2412_08585_amd import workloads as W
+    w = W.WORKLOADS["phi3m-prefill-4k"]
+    _log(f"full-size prefill B_r={br} qblocks={qblocks}")
+    q, k, v = W.prefill_inputs(w, device=dev)
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k, v)
+    o, lse = ta.turbo_attn_prefill(q, k8, v8, sk, sv, w.sm_scale, True, return_lse=True,
+                                   block_rows=br)
+    torch.cuda.synchronize()
+    (b, h), = _sample_units(w, 1, seed=br + qblocks[0])
+    qs = q[b:b + 1, h * w.G:(h + 1) * w.G].cpu()
+    ro, rl = orc.attn_prefill(qs, k[b:b + 1, h:h + 1].cpu(), v[b:b + 1, h:h + 1].cpu(),
+                              w.sm_scale, True, qblocks=qblocks, block_rows=br)
+    rows = slice(br * qblocks[0], br * qblocks[1])
+    _cmp_o(o[b:b + 1, h * w.G:(h + 1) * w.G, rows], ro[:, :, rows], f"B_r={br} O unit {b},{h}")
+    _cmp_lse(lse[b:b + 1, h * w.G:(h + 1) * w.G, rows], rl[:, :, rows], f"B_r={br} lse")
     del q, k, v, k8, v8, o
     torch.cuda.empty_cache()
 

@@ -98,6 +98,10 @@ def test_invalid_arguments_rejected_before_launch(ta):
     # max_groups too small for N
     assert L.turbo_quantize_kv(dummy, dummy, 1, 1, 192, 128, dummy, dummy, dummy, dummy,
                                ctypes.byref(c), dummy, dummy, 2, None) == -1
+    # query block size outside {32, 64, 128}
+    for br in (0, 16, 96, 256):
+        assert L.turbo_attn_prefill_blocks(dummy, dummy, dummy, dummy, dummy, 1, 4, 4, 64, 128,
+                                           0.1, 1, br, dummy, None, None) == -1
     # SAS softmax: bad sizes and null pointers; zero rows is a no-op
     assert L.turbo_sas_softmax(dummy, dummy, -1, 8, None) == -1
     assert L.turbo_sas_softmax(dummy, dummy, 4, 0, None) == -1
