@@ -70,8 +70,9 @@ def lib():
             "or_sas_softmax_rows": ([P, I, I, P], None),
             "or_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P], None),
             "or_attn_prefill": ([P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P, I, I], None),
-            "or_attn_prefill_blocks": ([P, P, P, I, I, I, I, I, F, I, _Opts, I, P, P, P, I, I],
-                                       None),
+            "or_attn_prefill_blocks": ([P, P, P, I, I, I, I, I, F, I, _Opts, I, I, P, P, P, I,
+                                        I], None),
+            "or_quantize_kv_blocks": ([P, P, I, I, I, I, I, P, P, P, P], None),
             "or_tail_init": ([P, P, I, I, I, I, P, P, P, P, P, P], None),
             "or_append_kv": ([P, P, I, I, I, P, P, I, P, P, P, P, P, P, P, P, P, P, P, P], None),
             "or_attn_decode": ([P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, F, I, _Opts, P, P, P,
@@ -181,6 +182,21 @@ def quantize_kv(k, v, bits) -> dict:
     return out
 
 
+def quantize_kv_blocks(k, v, block_cols: int) -> dict:
+    """FlashQ step 1 of K/V [B][Hkv][N][d] (fp16 values) with blocks of
+    block_cols = B_c tokens (Table 3): k8, v8 [B][Hkv][N][d] and sk, sv
+    [B][Hkv][ceil(N / B_c)].  No step 2: the cache keeps its 64-token groups."""
+    k, v = _f32(k), _f32(v)
+    B, Hkv, N, d = k.shape
+    assert block_cols in (32, 64, 128)
+    nbc = (N + block_cols - 1) // block_cols
+    out = dict(k8=np.empty((B, Hkv, N, d), np.int8), v8=np.empty((B, Hkv, N, d), np.int8),
+               sk=np.empty((B, Hkv, nbc), np.float32), sv=np.empty((B, Hkv, nbc), np.float32))
+    lib().or_quantize_kv_blocks(_p(k), _p(v), B, Hkv, N, d, int(block_cols), _p(out["k8"]),
+                                _p(out["v8"]), _p(out["sk"]), _p(out["sv"]))
+    return out
+
+
 def qkv_project(x, w, Hq: int, Hkv: int, bits, d: int = 128) -> dict:
     """The QKV projection followed by FlashQ (Sec. 5.2 folds the quantization
     into this projection; Sec. 3.1 step 1 and step 2).
@@ -223,12 +239,15 @@ def _trace(d: int, sel):
 
 
 def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = True,
-                 sas: bool = True, trace=None, qblocks=None, block_rows: int = 64):
+                 sas: bool = True, trace=None, qblocks=None, block_rows: int = 64,
+                 block_cols: int = 64):
     """Algorithm 1.  q [B][Hq][N][d], k, v [B][Hkv][N][d] (fp16 values).
     Returns (o float64 [B][Hq][N][d] = O/l before fp16 rounding, lse float64
     [B][Hq][N]) and, with trace=(b, h, i, j), a dict of that tile's integers.
     qblocks=(i0, i1) restricts the work to query blocks i0..i1-1 (other rows NaN).
-    block_rows = B_r (Table 3): the query block of the Q scale and P tile."""
+    block_rows = B_r, block_cols = B_c (Table 3): the query block of the Q
+    scale, the key block of the K/V scales and of each online step, and the
+    B_r x B_c tile of the P scale."""
     q, k, v = _f32(q), _f32(k), _f32(v)
     B, Hq, N, d = q.shape
     Hkv = k.shape[1]
@@ -236,10 +255,12 @@ def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = Tr
     lse = np.full((B, Hq, N), np.nan, np.float64)
     tr, bufs = _trace(d, trace)
     i0, i1 = (-1, -1) if qblocks is None else qblocks
-    assert block_rows in (32, 64, 128) and (tr is None or block_rows == 64)
+    assert block_rows in (32, 64, 128) and block_cols in (32, 64, 128)
+    assert tr is None or block_rows == block_cols == 64
     lib().or_attn_prefill_blocks(_p(q), _p(k), _p(v), B, Hq, Hkv, N, d,
                                  float(np.float32(sm_scale)), int(causal),
-                                 _Opts(int(quant), int(sas)), int(block_rows), _p(o), _p(lse),
+                                 _Opts(int(quant), int(sas)), int(block_rows), int(block_cols),
+                                 _p(o), _p(lse),
                                  ctypes.byref(tr) if tr is not None else None, int(i0), int(i1))
     if tr is None:
         return o, lse

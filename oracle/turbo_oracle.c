@@ -193,6 +193,25 @@ void or_quantize_kv(const float* k, const float* v, int B, int Hkv, int N, int d
     }
 }
 
+/* Step 1 alone with key/value blocks of bc tokens (Table 3 varies B_c):
+ * k8, v8 int8 [B][Hkv][N][d]; sk, sv float [B][Hkv][ceil(N/bc)].  The last
+ * block is quantized over its valid rows only. */
+void or_quantize_kv_blocks(const float* k, const float* v, int B, int Hkv, int N, int d, int bc,
+                           int8_t* k8, int8_t* v8, float* sk, float* sv) {
+  const int nbc = (N + bc - 1) / bc;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b)
+    for (int h = 0; h < Hkv; ++h) {
+      const size_t u = (size_t)b * Hkv + h;
+      for (int j = 0; j < nbc; ++j) {
+        const int r0 = j * bc, nr = (N - r0) < bc ? (N - r0) : bc;
+        const size_t off = (u * (size_t)N + r0) * d;
+        sk[u * nbc + j] = or_block_quant(k + off, (long)nr * d, k8 + off);
+        sv[u * nbc + j] = or_block_quant(v + off, (long)nr * d, v8 + off);
+      }
+    }
+}
+
 /* ---- the online softmax step shared by Algorithms 1 and 2 ------------- */
 /* Exponential factor e^{-(hi - lo)} of the online softmax for hi >= lo.
  * With FlashQ on, hi and lo are binary32 values and their difference is
@@ -326,14 +345,16 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
  * O is multiplied by that factor; when the maximum does not move the factor
  * is SAS(0) as written.
  * Block sizes (Table 3 varies them): Q is quantized per br rows of a head
- * (br = B_r in {32, 64, 128}) and the P scale covers the br x 64 tile; K and
- * V keep their 64-token blocks (B_c = 64).  Query blocks i0..i1 count br-row
- * blocks.  The trace is produced for br = 64 only. */
+ * (br = B_r in {32, 64, 128}); K and V are quantized per bc tokens (bc = B_c
+ * in {32, 64, 128}), each online step covers bc keys and the P scale covers
+ * the br x bc tile.  Query blocks i0..i1 count br-row blocks.  The trace is
+ * produced for br = bc = 64 only. */
 void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int B, int Hq,
                             int Hkv, int N, int d, float sm_scale, int causal, or_opts opts,
-                            int br, double* o, double* lse, or_trace* tr, int i0, int i1) {
-  const int G = Hq / Hkv, nb = (N + OR_BS - 1) / OR_BS, nbq = (N + br - 1) / br;
-  if (br != OR_BS) tr = NULL; /* the trace layout is that of 64-row blocks */
+                            int br, int bc, double* o, double* lse, or_trace* tr, int i0,
+                            int i1) {
+  const int G = Hq / Hkv, nb = (N + bc - 1) / bc, nbq = (N + br - 1) / br;
+  if (br != OR_BS || bc != OR_BS) tr = NULL; /* the trace layout is that of 64x64 tiles */
 #pragma omp parallel
   {
     int8_t* k8 = malloc((size_t)N * d + 1);
@@ -341,11 +362,11 @@ void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int 
     float* sk = malloc(sizeof(float) * (nb + 1));
     float* sv = malloc(sizeof(float) * (nb + 1));
     int8_t* q8 = malloc((size_t)br * d);
-    double* sc = malloc(sizeof(double) * br * OR_BS);
-    unsigned char* vis = malloc((size_t)br * OR_BS);
-    float* p = malloc(sizeof(float) * br * OR_BS);
-    double* pd = malloc(sizeof(double) * br * OR_BS);
-    int8_t* qp = malloc((size_t)br * OR_BS);
+    double* sc = malloc(sizeof(double) * br * bc);
+    unsigned char* vis = malloc((size_t)br * bc);
+    float* p = malloc(sizeof(float) * br * bc);
+    double* pd = malloc(sizeof(double) * br * bc);
+    int8_t* qp = malloc((size_t)br * bc);
     double* Obuf = malloc(sizeof(double) * br * d);
     or_row rows[OR_MAXBR];
 #pragma omp for collapse(2) schedule(dynamic)
@@ -357,7 +378,7 @@ void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int 
         const float* qq = q + ((size_t)b * Hq + h) * (size_t)N * d;
         if (opts.quant)
           for (int j = 0; j < nb; ++j) { /* K_j^{q1}, V_j^{q1} (eq. step1bpq) */
-            const int r0 = j * OR_BS, nr = (N - r0) < OR_BS ? (N - r0) : OR_BS;
+            const int r0 = j * bc, nr = (N - r0) < bc ? (N - r0) : bc;
             sk[j] = or_block_quant(kk + (size_t)r0 * d, (long)nr * d, k8 + (size_t)r0 * d);
             sv[j] = or_block_quant(vv + (size_t)r0 * d, (long)nr * d, v8 + (size_t)r0 * d);
           }
@@ -377,31 +398,31 @@ void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int 
           }
           memset(Obuf, 0, sizeof(double) * br * d);
           for (int j = 0; j < nb; ++j) {
-            const int k0 = j * OR_BS, nk = (N - k0) < OR_BS ? (N - k0) : OR_BS;
+            const int k0 = j * bc, nk = (N - k0) < bc ? (N - k0) : bc;
             if (causal && k0 > q0 + nq - 1) break;
             /* S_i^{(j)} = s_Q s_K Q_i^{q1} K_j^{q1 T} (times sm_scale) */
             const float c = (float)(sq * sk[j]) * sm_scale;
             for (int r = 0; r < nq; ++r)
               for (int t = 0; t < nk; ++t) {
                 const int visible = !causal || (k0 + t <= q0 + r);
-                vis[r * OR_BS + t] = (unsigned char)visible;
+                vis[r * bc + t] = (unsigned char)visible;
                 if (!visible) continue;
                 if (opts.quant) {
                   int32_t acc = 0;
                   for (int e = 0; e < d; ++e)
                     acc += (int32_t)q8[(size_t)r * d + e] * (int32_t)k8[(size_t)(k0 + t) * d + e];
-                  sc[r * OR_BS + t] = (double)((float)acc * c);
+                  sc[r * bc + t] = (double)((float)acc * c);
                   if (trq && tr->j == j) tr->sacc[r * OR_BS + t] = acc;
                 } else {
                   double acc = 0.0;
                   for (int e = 0; e < d; ++e)
                     acc += (double)qq[(size_t)(q0 + r) * d + e] * (double)kk[(size_t)(k0 + t) * d + e];
-                  sc[r * OR_BS + t] = acc * (double)sm_scale;
+                  sc[r * bc + t] = acc * (double)sm_scale;
                 }
               }
             or_trace* tt = (trq && tr->j == j) ? tr : NULL;
             if (tt) tt->hit = 1;
-            or_tile(&opts, rows, nq, nk, sc, vis, OR_BS, v8 + (size_t)k0 * d, sv[j],
+            or_tile(&opts, rows, nq, nk, sc, vis, bc, v8 + (size_t)k0 * d, sv[j],
                     vv + (size_t)k0 * d, d, p, pd, qp, tt);
           }
           for (int r = 0; r < nq; ++r) {
@@ -420,8 +441,8 @@ void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int 
 void or_attn_prefill(const float* q, const float* k, const float* v, int B, int Hq, int Hkv,
                      int N, int d, float sm_scale, int causal, or_opts opts, double* o,
                      double* lse, or_trace* tr, int i0, int i1) {
-  or_attn_prefill_blocks(q, k, v, B, Hq, Hkv, N, d, sm_scale, causal, opts, OR_BS, o, lse, tr,
-                         i0, i1);
+  or_attn_prefill_blocks(q, k, v, B, Hq, Hkv, N, d, sm_scale, causal, opts, OR_BS, OR_BS, o, lse,
+                         tr, i0, i1);
 }
 
 /* ---- Algorithm 2: decode over the compressed cache -------------------- */

@@ -1,8 +1,8 @@
 """Pins of the oracle's block-size variants of Algorithm 1 (Table 3 varies the
-query block B_r; key blocks stay 64): the partition the Q scale and the P
-scale are taken over, the reduction to the 64-row result where quantization
-is off, and the rows of a 128-row block that see no key of a tile being left
-untouched."""
+query block B_r and the key block B_c over {32, 64, 128}): the partitions the
+Q, K, V and P scales are taken over, the reduction to the 64 x 64 result or
+to exact attention where quantization (and SAS) are off, and the rows of a
+block that see no key of a tile being left untouched."""
 import numpy as np
 import pytest
 
@@ -70,3 +70,97 @@ def test_scales_follow_the_block_partition(orc):
     a128, _ = orc.attn_prefill(q, k, v, SM, False, block_rows=128)
     b128, _ = orc.attn_prefill(q2, k, v, SM, False, block_rows=128)
     assert not np.array_equal(a128[:, :, :64], b128[:, :, :64])
+
+
+# ---- key blocks B_c (Table 3) ---------------------------------------------
+
+@pytest.mark.parametrize("bc", [32, 128])
+def test_step1_blocks_nest(orc, bc):
+    """Step 1 over bc-token blocks: the scale of a 64-token block is the
+    larger of its two 32-token scales, and a 128-token scale the larger of its
+    two 64-token scales (the rounding of amax/119 is monotone); codes agree
+    wherever the scales agree."""
+    q, k, v = _qkv(5, 2, 1, 2, 64 * 4 + 50)
+    v[:, :, 64 * 2:64 * 2 + 40] *= 3
+    fine, coarse = (32, 64) if bc == 32 else (64, 128)
+    a = orc.quantize_kv_blocks(k, v, fine)
+    c = orc.quantize_kv_blocks(k, v, coarse)
+    ref = orc.quantize_kv(k, v, [4, 4])
+    b64 = a if fine == 64 else c
+    for key in ("k8", "v8", "sk", "sv"):
+        assert np.array_equal(b64[key], ref[key]), key
+    N = k.shape[2]
+    for s, x8 in (("sk", "k8"), ("sv", "v8")):
+        nf = a[s].shape[-1]
+        pad = np.zeros(a[s].shape[:-1] + (2 * c[s].shape[-1] - nf,), np.float32)
+        pairs = np.concatenate([a[s], pad], -1).reshape(a[s].shape[:-1] + (-1, 2))
+        assert np.array_equal(pairs.max(-1), c[s]), s
+        # codes equal in every fine block whose scale equals the coarse one
+        for j in range(nf):
+            rows = slice(fine * j, min(N, fine * j + fine))
+            same = a[s][..., j] == c[s][..., j // 2]
+            assert np.array_equal(a[x8][:, :, rows][same], c[x8][:, :, rows][same])
+    # a direct check of one block against the definition
+    blk = k[0, 1, bc:2 * bc] if 2 * bc <= N else k[0, 1, :bc]
+    j = 1 if 2 * bc <= N else 0
+    e = orc.quantize_kv_blocks(k, v, bc)
+    assert e["sk"][0, 1, j] == np.float32(np.abs(blk).max()) / np.float32(119)
+
+
+@pytest.mark.parametrize("br,bc", [(32, 32), (64, 32), (64, 128), (128, 128), (32, 128)])
+@pytest.mark.parametrize("causal", [True, False])
+def test_key_blocks_reduce_to_exact_attention(orc, br, bc, causal):
+    q, k, v = _qkv(6, 1, 4, 2, 64 * 3 + 45)
+    o, lse = orc.attn_prefill(q, k, v, SM, causal, quant=False, sas=False, block_rows=br,
+                              block_cols=bc)
+    ex, lex = orc.attn_exact(q, k, v, float(np.float32(SM)), causal)
+    np.testing.assert_allclose(o, ex, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, lex, rtol=0, atol=1e-12)
+
+
+def _split_v(v, lo, hi):
+    va, vb = v.copy(), v.copy()
+    va[:, :, lo:hi] = 0
+    vb[:, :, :lo] = 0
+    vb[:, :, hi:] = 0
+    return va, vb
+
+
+@pytest.mark.parametrize("bc,split", [(32, 32), (64, 64)])
+def test_v_scales_follow_the_key_blocks(orc, bc, split):
+    """P~ and its codes do not depend on V, and a V block that is all zero has
+    scale 0: so O(V) = O(V_a) + O(V_b) exactly (up to double rounding) when
+    V_a, V_b split V along a boundary of the V blocks, and not otherwise
+    (the block scales of V_a differ from V's)."""
+    q, k, v = _qkv(7, 1, 2, 1, 2 * split)
+    v[:, :, split:] *= 3                    # the block maximum lies after the split
+    kw = dict(block_cols=bc)
+    o, _ = orc.attn_prefill(q, k, v, SM, False, **kw)
+    va, vb = _split_v(v, split, 2 * split)
+    oa, _ = orc.attn_prefill(q, k, va, SM, False, **kw)
+    ob, _ = orc.attn_prefill(q, k, vb, SM, False, **kw)
+    np.testing.assert_allclose(oa + ob, o, rtol=0, atol=1e-12)
+    coarse = 64 if bc == 32 else 128
+    o2, _ = orc.attn_prefill(q, k, v, SM, False, block_cols=coarse)
+    oa2, _ = orc.attn_prefill(q, k, va, SM, False, block_cols=coarse)
+    ob2, _ = orc.attn_prefill(q, k, vb, SM, False, block_cols=coarse)
+    assert np.abs(oa2 + ob2 - o2).max() > 1e-4
+
+
+@pytest.mark.parametrize("fine,coarse", [(32, 64), (64, 128)])
+def test_kv_scales_follow_the_key_blocks(orc, fine, coarse):
+    """Causal rows before key `fine` see only the first key block.  Scaling K
+    and V after it by 8 leaves those rows bit-identical when B_c = fine (their
+    block's scales are its own) and changes them when B_c = coarse (the block
+    scale now covers the scaled keys)."""
+    q, k, v = _qkv(8, 1, 2, 1, 2 * fine)
+    k2, v2 = k.copy(), v.copy()
+    k2[:, :, fine:] *= 8
+    v2[:, :, fine:] *= 8
+    rows = slice(0, fine)
+    for bc, same in ((fine, True), (coarse, False)):
+        a, la = orc.attn_prefill(q, k, v, SM, True, block_rows=32, block_cols=bc)
+        b, lb = orc.attn_prefill(q, k2, v2, SM, True, block_rows=32, block_cols=bc)
+        eq = np.array_equal(a[:, :, rows], b[:, :, rows]) and np.array_equal(la[:, :, rows],
+                                                                             lb[:, :, rows])
+        assert eq == same, (bc, same)
