@@ -179,6 +179,24 @@ int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d
                       hipStream_t stream);
 
 /*
+ * turbo_quantize_kv_blocks — FlashQ step 1 of K and V (eq. step1bpq) with
+ * key blocks of block_cols = B_c tokens, the block sizes Table 3 compares
+ * (32, 64 or 128), for turbo_attn_prefill_blocks.  No cache write: the
+ * step-2 groups of the cache stay 64 tokens (Sec. 3.3 fixes n_b = 64), so
+ * the cache is written by turbo_quantize_kv only.
+ *
+ * k8, v8      the layouts of turbo_quantize_kv (64-token blocks, Np =
+ *             64*ceil(N/64) rows; rows N..Np-1 written as 0), holding the
+ *             codes of the B_c-token blocks.
+ * s_k, s_v    fp32 [B][Hkv][ceil(N/B_c)]: max|block| / 119 of each B_c block.
+ * block_cols  32, 64 or 128 (64: turbo_quantize_kv without a cache);
+ *             INVALID_ARG otherwise.  Other arguments as turbo_quantize_kv.
+ */
+int turbo_quantize_kv_blocks(const void* k, const void* v, int B, int Hkv, int N, int d,
+                             int block_cols, int8_t* k8, int8_t* v8, float* s_k, float* s_v,
+                             hipStream_t stream);
+
+/*
  * turbo_attn_prefill — Algorithm 1 (TurboAttention prefill): per 64-row query
  * block, int8 quantization of Q_i; for each key block j, int8 QK^T scaled by
  * s_Q * s_K * sm_scale, online row maximum, SAS in place of exp, running sum
@@ -202,19 +220,21 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
                        int causal, void* o, float* lse, hipStream_t stream);
 
 /*
- * turbo_attn_prefill_blocks — turbo_attn_prefill with another query block
- * size B_r (Table 3 evaluates several): Q is quantized per block_rows rows
- * of a head and the P scale covers the block_rows x 64 tile; K and V keep
- * their 64-token blocks (B_c = 64).  block_rows = 64 is turbo_attn_prefill.
- * With B_r = 128 and causal masking, a 32-row quarter of a block that sees no
- * key of a tile leaves its rows untouched (Algorithm 1 processes no such
- * pair).  INVALID_ARG for block_rows not in {32, 64, 128}; other arguments
- * and errors as turbo_attn_prefill.
+ * turbo_attn_prefill_blocks — turbo_attn_prefill with other block sizes
+ * (B_r, B_c) (Table 3 evaluates seven pairs from {32, 64, 128}): Q is
+ * quantized per block_rows rows of a head, each online step covers
+ * block_cols keys, and the P scale covers the block_rows x block_cols tile.
+ * k8, v8, s_k, s_v must come from turbo_quantize_kv_blocks with the same
+ * block_cols (s_k, s_v [B][Hkv][ceil(N/block_cols)]).  (64, 64) is
+ * turbo_attn_prefill.  With causal masking and B_r > B_c, a 32-row slice of
+ * a block that sees no key of a tile leaves its rows untouched (Algorithm 1
+ * processes no such pair).  INVALID_ARG for block sizes outside
+ * {32, 64, 128}; other arguments and errors as turbo_attn_prefill.
  */
 int turbo_attn_prefill_blocks(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
                               const float* s_v, int B, int Hq, int Hkv, int N, int d,
-                              float sm_scale, int causal, int block_rows, void* o, float* lse,
-                              hipStream_t stream);
+                              float sm_scale, int causal, int block_rows, int block_cols, void* o,
+                              float* lse, hipStream_t stream);
 
 /*
  * turbo_attn_prefill_q8 — turbo_attn_prefill with Q already quantized

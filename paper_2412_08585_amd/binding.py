@@ -63,7 +63,9 @@ def lib() -> ctypes.CDLL:
             "turbo_int2_heads": ([P, I, I, P], I),
             "turbo_sas_softmax": ([P, P, ctypes.c_int64, I, P], I),
             "turbo_attn_prefill_q8": ([P, P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
-            "turbo_attn_prefill_blocks": ([P, P, P, P, P, I, I, I, I, I, F, I, I, P, P, P], I),
+            "turbo_attn_prefill_blocks": ([P, P, P, P, P, I, I, I, I, I, F, I, I, I, P, P, P],
+                                          I),
+            "turbo_quantize_kv_blocks": ([P, P, I, I, I, I, I, P, P, P, P, P], I),
             "turbo_qkv_project": ([P, P, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P], I),
             "turbo_decode_auto_split": ([I, I, I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
@@ -186,19 +188,31 @@ def turbo_append_kv(k_new: torch.Tensor, v_new: torch.Tensor, seq_lens: torch.Te
 
 def turbo_quantize_kv(k: torch.Tensor, v: torch.Tensor, cache: Optional[PagedKVCache] = None,
                       block_table: Optional[torch.Tensor] = None,
-                      group_table: Optional[torch.Tensor] = None, out=None):
+                      group_table: Optional[torch.Tensor] = None, out=None,
+                      block_cols: int = 64):
     """FlashQ of K, V fp16 [B][Hkv][N][128].  Returns (k8, v8, s_k, s_v) in the
-    layouts of include/turbo_attn.h; writes the full groups into `cache`."""
+    layouts of include/turbo_attn.h; writes the full groups into `cache`.
+    block_cols = B_c in {32, 64, 128} (Table 3): the step-1 block of K and V
+    (s_k, s_v [B][Hkv][ceil(N / B_c)]); the cache needs B_c = 64."""
     B, Hkv, N, d = k.shape
     nb = (N + BLOCK - 1) // BLOCK
+    nbc = (N + block_cols - 1) // block_cols
     dev = k.device
     if out is None:
         k8 = torch.empty(B, Hkv, nb * BLOCK, d, dtype=torch.int8, device=dev)
         v8 = torch.empty(B, Hkv, nb, d, BLOCK, dtype=torch.int8, device=dev)
-        s_k = torch.empty(B, Hkv, nb, dtype=torch.float32, device=dev)
-        s_v = torch.empty(B, Hkv, nb, dtype=torch.float32, device=dev)
+        s_k = torch.empty(B, Hkv, nbc, dtype=torch.float32, device=dev)
+        s_v = torch.empty(B, Hkv, nbc, dtype=torch.float32, device=dev)
     else:
         k8, v8, s_k, s_v = out
+    if block_cols != BLOCK:
+        if cache is not None:
+            raise ValueError("the cache is written with 64-token blocks only")
+        st = lib().turbo_quantize_kv_blocks(_ptr(k), _ptr(v), B, Hkv, N, d, int(block_cols),
+                                            _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v),
+                                            _stream(dev))
+        _check(st, "turbo_quantize_kv_blocks")
+        return k8, v8, s_k, s_v
     cs = cache.struct() if cache is not None else None
     mg = group_table.shape[1] if group_table is not None else 0
     st = lib().turbo_quantize_kv(_ptr(k), _ptr(v), B, Hkv, N, d, _ptr(k8), _ptr(v8), _ptr(s_k),
@@ -210,24 +224,27 @@ def turbo_quantize_kv(k: torch.Tensor, v: torch.Tensor, cache: Optional[PagedKVC
 
 def turbo_attn_prefill(q: torch.Tensor, k8, v8, s_k, s_v, sm_scale: Optional[float] = None,
                        causal: bool = True, return_lse: bool = False, out=None,
-                       block_rows: int = 64):
+                       block_rows: int = 64, block_cols: int = 64):
     """Algorithm 1 prefill.  q fp16 [B][Hq][N][128]; k8/v8/s_k/s_v from
-    turbo_quantize_kv.  Returns o fp16 [B][Hq][N][128] (and lse fp32).
-    block_rows = B_r in {32, 64, 128} (Table 3); 64 is the default path."""
+    turbo_quantize_kv (with the same block_cols).  Returns o fp16
+    [B][Hq][N][128] (and lse fp32).  block_rows = B_r, block_cols = B_c in
+    {32, 64, 128} (Table 3); (64, 64) is the default path."""
     B, Hq, N, d = q.shape
     Hkv = s_k.shape[1]
     sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty(B, Hq, N, dtype=torch.float32, device=q.device) if return_lse else None
-    if block_rows == 64:
+    if s_k.shape[-1] != (N + block_cols - 1) // block_cols:
+        raise ValueError(f"s_k holds {s_k.shape[-1]} blocks, not those of B_c = {block_cols}")
+    if block_rows == 64 and block_cols == 64:
         st = lib().turbo_attn_prefill(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B, Hq,
                                       Hkv, N, d, sm, int(bool(causal)), _ptr(o), _ptr(lse),
                                       _stream(q.device))
     else:
         st = lib().turbo_attn_prefill_blocks(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B,
                                              Hq, Hkv, N, d, sm, int(bool(causal)),
-                                             int(block_rows), _ptr(o), _ptr(lse),
-                                             _stream(q.device))
+                                             int(block_rows), int(block_cols), _ptr(o),
+                                             _ptr(lse), _stream(q.device))
     _check(st, "turbo_attn_prefill")
     return (o, lse) if return_lse else o
 

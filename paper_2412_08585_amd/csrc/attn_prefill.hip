@@ -42,6 +42,7 @@ struct PrefillArgs {
   int B, Hq, Hkv, N, nb;
   int waves;           // 1, 2 or 4: B_r = 32 * waves
   int nbq;             // query blocks of B_r rows
+  int bc, nbc;         // key block B_c (32, 64, 128) and key blocks per (b, h); sk, sv [..][nbc]
   float sm_scale;
   int causal;
   uint2* o;            // fp16 [B][Hq][N][128] (as 4-half units)
@@ -68,9 +69,17 @@ __device__ __forceinline__ int prefill_order(int x, int total, int G) {
 // (the production instance carries no trace code).  kQ8: Q arrives already
 // quantized (FlashQ step 1 of the fused projection), so the prologue only
 // loads the int8 block and its scale.
-template <bool kTrace, bool kQ8, int kWaves>
+//
+// kBc = B_c: each online step (tile) covers kBc keys in kKb 32-key MFMA
+// blocks.  B_c <= 64 keeps the whole pipeline in registers (K of the next
+// tile loaded during the softmax); B_c = 128 would need 64 more registers for
+// that, so its K is fetched in two 64-key halves after the tile's PV.
+template <bool kTrace, bool kQ8, int kWaves, int kBc>
 __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) {
   constexpr int kBr = 32 * kWaves;
+  constexpr int kKb = kBc / 32;           // 32-key blocks per tile
+  constexpr bool kSplitK = kKb > 2;       // B_c = 128
+  constexpr int kKl = kSplitK ? 2 : kKb;  // 32-key K blocks held in registers
   __shared__ float lut[8];
   __shared__ float xmax[2][kWaves];  // per-wave P maxima, double-buffered
   const int tid = threadIdx.x;
@@ -142,44 +151,58 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
   }
   // wave-uniform; a key block the loop never reaches traces nothing
   const bool traced = kTrace && L == a.tr_L && a.tr_j <= (a.causal ? i : a.nb - 1);
-  if (traced) {
+  if constexpr (kTrace) {
+    if (traced) {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-      *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_Q8 + (32 * qh + n) * 128 + 32 * ks + 16 * hf) =
-          qop[ks];
-    if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = sq;
+      for (int ks = 0; ks < 4; ++ks)
+        *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_Q8 + (32 * qh + n) * 128 + 32 * ks +
+                                16 * hf) = qop[ks];
+      if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = sq;
+    }
   }
 
   const long kvu = (long)b * a.Hkv + kh;
-  const float* skp = a.sk + kvu * a.nb;
-  const float* svp = a.sv + kvu * a.nb;
-  // A-operand row m of a 32-key half holds key kidx(m)
+  const float* skp = a.sk + kvu * a.nbc;
+  const float* svp = a.sv + kvu * a.nbc;
+  // A-operand row m of a 32-key block holds key kidx(m)
   const int m = lane & 31;
   const int kidx = 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3);
   const int8_t* klane = a.k8 + kvu * a.nb * 8192 + kidx * 128 + 16 * hf;
   const int8_t* vlane = a.v8 + kvu * a.nb * 8192 + n * 64 + 16 * hf;
+  // 32-key blocks the K8/V8 buffers hold (64 nb keys).  Only a 128-key tile
+  // can reach past them; such blocks re-read the last one held, and their
+  // keys (all >= N) are masked, so their scores and Q(P~) codes do not count.
+  const int glast = 2 * a.nb - 1;
+  auto blk = [&](int g) { return kSplitK ? min(g, glast) : g; };
 
-  auto load_k = [&](v4i (&kop)[2][4], int j) {
+  // K of the 32-key blocks g0 .. g0 + kKl - 1 (token-major, 128 B a key)
+  auto load_k = [&](v4i (&kop)[kKl][4], int g0) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < kKl; ++kb)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
-        kop[kb][ks] = *reinterpret_cast<const v4i*>(klane + ((long)j * 64 + 32 * kb) * 128 + 32 * ks);
+        kop[kb][ks] =
+            *reinterpret_cast<const v4i*>(klane + (long)blk(g0 + kb) * 4096 + 32 * ks);
   };
-  auto load_v = [&](v4i (&vop)[4][2], int j) {
+  // V^T of the 32-key blocks g0 .. g0 + kKb - 1 (channel-major 64-key blocks)
+  auto load_v = [&](v4i (&vop)[4][kKb], int g0) {
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        vop[cb][kb] = *reinterpret_cast<const v4i*>(vlane + (long)j * 8192 + 32 * cb * 64 + 32 * kb);
+      for (int kb = 0; kb < kKb; ++kb) {
+        const int g = blk(g0 + kb);
+        vop[cb][kb] = *reinterpret_cast<const v4i*>(vlane + (long)(g >> 1) * 8192 +
+                                                    32 * cb * 64 + 32 * (g & 1));
+      }
   };
-  auto qk = [&](v16i (&S)[2], const v4i (&kop)[2][4]) {
+  // S^T of kKl 32-key blocks into S[off ..]
+  auto qk = [&](v16i (&S)[kKb], int off, const v4i (&kop)[kKl][4]) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < kKl; ++kb) {
       v16i acc = {};
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x32(kop[kb][ks], qop[ks], acc);
-      S[kb] = acc;
+      S[off + kb] = acc;
     }
   };
 
@@ -190,52 +213,60 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
     for (int r = 0; r < 16; ++r) O[cb][r] = 0.0f;
   float mrow = -INFINITY, lhalf = 0.0f, beta = 1.0f;
 
-  // last key block: the one holding the block's last row when causal
-  const int jend = a.causal ? min(a.nb - 1, (kBr * i + kBr - 1) / 64) : a.nb - 1;
+  // last key tile: the one holding the block's last row when causal
+  const int jend = a.causal ? min(a.nbc - 1, (kBr * i + kBr - 1) / kBc) : a.nbc - 1;
   // Software pipeline per tile j:  softmax of S_j on the VALU (K of tile j+1
   // already in flight) -> tile maximum exchange -> PV_j and then S_{j+1} on
   // the MFMA -> accumulator update on the VALU while S_{j+1} is computed.
-  v4i kop[2][4];
-  v4i vop[4][2];
-  v16i S[2];
+  // B_c = 128: K_{j+1} is loaded during the accumulator update and S_{j+1}
+  // computed after it.
+  v4i kop[kKl][4];
+  v4i vop[4][kKb];
+  v16i S[kKb];
   load_k(kop, 0);
-  qk(S, kop);
+  qk(S, 0, kop);
+  if constexpr (kSplitK) {
+    load_k(kop, 2);
+    qk(S, 2, kop);
+  }
   load_v(vop, 0);
   float skj = skp[0], svj = svp[0];
   for (int j = 0; j <= jend; ++j) {
     const int jn = min(j + 1, jend);
-    load_k(kop, jn);
+    if constexpr (!kSplitK) load_k(kop, kKb * jn);
     const float skn = skp[jn], svn = svp[jn];
     const bool trace_tile = traced && j == a.tr_j;
-    if (trace_tile) {
-      int* ts = reinterpret_cast<int*>(a.trace + TURBO_TRACE_S) + (32 * qh + n) * 64 + 16 * hf;
+    if constexpr (kTrace) {
+      if (trace_tile) {
+        int* ts = reinterpret_cast<int*>(a.trace + TURBO_TRACE_S) + (32 * qh + n) * 64 + 16 * hf;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < kKb; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ts[32 * kb + r] = S[kb][r];
+          for (int r = 0; r < 16; ++r) ts[32 * kb + r] = S[kb][r];
+      }
     }
     // ---- scores, online max, SAS (Algorithm 1, statistics step) --------
     const float c = (sq * skj) * a.sm_scale;
-    float P[2][16];
+    float P[kKb][16];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < kKb; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) P[kb][r] = (float)S[kb][r] * c;
     // masking only where a key can lie after one of this wave's rows (the
     // diagonal) and on tiles that reach past N
-    if ((a.causal && 64 * j + 63 > row0) || (64 * j + 64 > N) || (row0 + 32 > N)) {
+    if ((a.causal && kBc * j + kBc - 1 > row0) || (kBc * j + kBc > N) || (row0 + 32 > N)) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < kKb; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = 64 * j + 32 * kb + 16 * hf + r;
+          const int key = kBc * j + 32 * kb + 16 * hf + r;
           const bool vis = key < N && qrow < N && (!a.causal || key <= qrow);
           P[kb][r] = vis ? P[kb][r] : -INFINITY;
         }
     }
     float smax = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < kKb; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) smax = fmaxf(smax, P[kb][r]);
     smax = max_xor32(smax);
@@ -243,7 +274,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
     const float mnew = fmaxf(mold, smax);
     float rs = 0.0f, pmax = 0.0f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < kKb; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = sas_y(mnew - P[kb][r], lut);
@@ -252,12 +283,14 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
         pmax = fmaxf(pmax, p);
       }
     float alpha = sas_y(mnew - mold, lut);  // 0 when mold = -inf
-    // with B_r = 128 a wave can see no key of the tile (its rows all precede
+    // with B_r > B_c a wave can see no key of the tile (its rows all precede
     // it): the rows are not processed, so nothing is rescaled
-    if (kWaves > 2 && a.causal && 64 * j > row0 + 31) alpha = 1.0f;
+    if constexpr (kBr > kBc) {
+      if (a.causal && kBc * j > row0 + 31) alpha = 1.0f;
+    }
     lhalf = alpha * lhalf + rs;
     mrow = mnew;
-    // ---- tile maximum of P~ over both waves ----------------------------
+    // ---- tile maximum of P~ over the waves -----------------------------
     pmax = wave_max_fast(pmax);
     if (kWaves > 1) {
       if (lane == 0) xmax[j & 1][qh] = pmax;
@@ -276,13 +309,13 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
       nbeta = 1.0f;
     }
     beta = nbeta;
-    // ---- Q(P~) with scale pmax/119 over the 64x64 tile -----------------
+    // ---- Q(P~) with scale pmax/119 over the B_r x B_c tile --------------
     // (a tile with pmax = 0 gets inv = 0, Q(P~) = 0 and adds nothing)
     const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
     const float g = ((pmax / kQmax) * svj) * __builtin_amdgcn_rcpf(beta);
-    v4i pop[2];
+    v4i pop[kKb];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < kKb; ++kb) {
       int w[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u)
@@ -290,12 +323,14 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
                         rne_bits(P[kb][4 * u + 2], inv), rne_bits(P[kb][4 * u + 3], inv));
       pop[kb] = v4i{w[0], w[1], w[2], w[3]};
     }
-    if (trace_tile) {
+    if constexpr (kTrace) {
+      if (trace_tile) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_P + (32 * qh + n) * 64 + 32 * kb + 16 * hf) =
-            pop[kb];
-      if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
+        for (int kb = 0; kb < kKb; ++kb)
+          *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_P + (32 * qh + n) * 64 + 32 * kb +
+                                  16 * hf) = pop[kb];
+        if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
+      }
     }
     // ---- PV_j, then S_{j+1}, on the MFMA -------------------------------
     v16i acc[4];
@@ -303,24 +338,40 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
     for (int cb = 0; cb < 4; ++cb) {
       v16i t = {};
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) t = mfma32x32x32(vop[cb][kb], pop[kb], t);
+      for (int kb = 0; kb < kKb; ++kb) t = mfma32x32x32(vop[cb][kb], pop[kb], t);
       acc[cb] = t;
     }
-    qk(S, kop);
-    if (trace_tile) {
-      // register r of channel block cb <-> channel 32cb + 8(r/4) + 4hf + r%4
-      int* tp = reinterpret_cast<int*>(a.trace + TURBO_TRACE_PV) + (32 * qh + n) * 128;
+    if constexpr (!kSplitK) {
+      qk(S, 0, kop);
+    } else {
+      // keep the next tile's loads behind the PV (registers)
+      __builtin_amdgcn_sched_barrier(0);
+      load_k(kop, kKb * jn);
+    }
+    if constexpr (kTrace) {
+      if (trace_tile) {
+        // register r of channel block cb <-> channel 32cb + 8(r/4) + 4hf + r%4
+        int* tp = reinterpret_cast<int*>(a.trace + TURBO_TRACE_PV) + (32 * qh + n) * 128;
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
+        for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) tp[32 * cb + 8 * (r >> 2) + 4 * hf + (r & 3)] = acc[cb][r];
+          for (int r = 0; r < 16; ++r) tp[32 * cb + 8 * (r >> 2) + 4 * hf + (r & 3)] = acc[cb][r];
+      }
     }
     // ---- Ost += (s_P s_V / beta) V_j^T Q(P~)^T ---------------------------
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) O[cb][r] = __builtin_fmaf(g, (float)acc[cb][r], O[cb][r]);
-    load_v(vop, jn);
+    if constexpr (kSplitK) {
+      __builtin_amdgcn_sched_barrier(0);
+      qk(S, 0, kop);
+      __builtin_amdgcn_sched_barrier(0);
+      load_k(kop, kKb * jn + 2);
+      qk(S, 2, kop);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    load_v(vop, kKb * jn);
     skj = skn;
     svj = svn;
   }
@@ -343,18 +394,29 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
   }
 }
 
+template <int kWaves>
+static void launch_bc(const PrefillArgs& a, int total, hipStream_t stream) {
+  const dim3 grid(total), block(64 * kWaves);
+  if (a.bc == 32)
+    hipLaunchKernelGGL((k_attn_prefill<false, false, kWaves, 32>), grid, block, 0, stream, a);
+  else if (a.bc == 128)
+    hipLaunchKernelGGL((k_attn_prefill<false, false, kWaves, 128>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_attn_prefill<false, false, kWaves, 64>), grid, block, 0, stream, a);
+}
+
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hq * a.nbq;
-  if (a.trace)  // test hook: B_r = 64 only
-    hipLaunchKernelGGL((k_attn_prefill<true, false, 2>), dim3(total), dim3(128), 0, stream, a);
-  else if (a.q8)
-    hipLaunchKernelGGL((k_attn_prefill<false, true, 2>), dim3(total), dim3(128), 0, stream, a);
+  if (a.trace)  // test hook: B_r = B_c = 64 only
+    hipLaunchKernelGGL((k_attn_prefill<true, false, 2, 64>), dim3(total), dim3(128), 0, stream, a);
+  else if (a.q8)  // B_r = B_c = 64 only
+    hipLaunchKernelGGL((k_attn_prefill<false, true, 2, 64>), dim3(total), dim3(128), 0, stream, a);
   else if (a.waves == 1)
-    hipLaunchKernelGGL((k_attn_prefill<false, false, 1>), dim3(total), dim3(64), 0, stream, a);
+    launch_bc<1>(a, total, stream);
   else if (a.waves == 4)
-    hipLaunchKernelGGL((k_attn_prefill<false, false, 4>), dim3(total), dim3(256), 0, stream, a);
+    launch_bc<4>(a, total, stream);
   else
-    hipLaunchKernelGGL((k_attn_prefill<false, false, 2>), dim3(total), dim3(128), 0, stream, a);
+    launch_bc<2>(a, total, stream);
   return hipGetLastError();
 }
 

@@ -111,6 +111,36 @@ int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d
   a.Hkv = Hkv;
   a.N = N;
   a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.bc = TURBO_BLOCK;
+  a.nbc = a.nb;
+  a.k8 = k8;
+  a.v8 = v8;
+  a.sk = s_k;
+  a.sv = s_v;
+  return turbo::launch_quantize_kv(a, B, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_quantize_kv_blocks(const void* k, const void* v, int B, int Hkv, int N, int d,
+                             int block_cols, int8_t* k8, int8_t* v8, float* s_k, float* s_v,
+                             hipStream_t stream) {
+  if (block_cols == TURBO_BLOCK)
+    return turbo_quantize_kv(k, v, B, Hkv, N, d, k8, v8, s_k, s_v, nullptr, nullptr, nullptr, 0,
+                             stream);
+  if (B < 0 || N < 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || d != TURBO_HEAD_DIM ||
+      (block_cols != 32 && block_cols != 128))
+    return TURBO_ERR_INVALID_ARG;
+  if (B == 0 || N == 0) return TURBO_OK;
+  if (!k || !v || !k8 || !v8 || !s_k || !s_v) return TURBO_ERR_INVALID_ARG;
+  int st = check_device();
+  if (st != TURBO_OK) return st;
+  turbo::QuantArgs a{};
+  a.k = static_cast<const uint4*>(k);
+  a.v = static_cast<const uint4*>(v);
+  a.Hkv = Hkv;
+  a.N = N;
+  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.bc = block_cols;
+  a.nbc = (N + block_cols - 1) / block_cols;
   a.k8 = k8;
   a.v8 = v8;
   a.sk = s_k;
@@ -121,14 +151,17 @@ int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d
 static int attn_prefill_impl(const void* q, const int8_t* q8, const float* s_q,
                              const int8_t* k8, const int8_t* v8, const float* s_k,
                              const float* s_v, int B, int Hq, int Hkv, int N, int d,
-                             float sm_scale, int causal, int block_rows, void* o, float* lse,
-                             unsigned char* trace, int tr_L, int tr_j, hipStream_t stream) {
+                             float sm_scale, int causal, int block_rows, int block_cols,
+                             void* o, float* lse, unsigned char* trace, int tr_L, int tr_j,
+                             hipStream_t stream) {
   if (B < 0 || N < 0 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || Hq / Hkv > TURBO_MAX_GQA ||
       d != TURBO_HEAD_DIM || !(sm_scale > 0.0f) || sm_scale > 3.0e38f)
     return TURBO_ERR_INVALID_ARG;
   if (B == 0 || N == 0) return TURBO_OK;
   if (!(q || (q8 && s_q)) || !k8 || !v8 || !s_k || !s_v || !o) return TURBO_ERR_INVALID_ARG;
   if (block_rows != 32 && block_rows != 64 && block_rows != 128) return TURBO_ERR_INVALID_ARG;
+  if (block_cols != 32 && block_cols != 64 && block_cols != 128) return TURBO_ERR_INVALID_ARG;
+  if (q8 && (block_rows != 64 || block_cols != 64)) return TURBO_ERR_INVALID_ARG;
   const long tiles = (long)B * Hq * ((N + block_rows - 1) / block_rows);
   if (tiles > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
   int st = check_device();
@@ -148,6 +181,8 @@ static int attn_prefill_impl(const void* q, const int8_t* q8, const float* s_q,
   a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
   a.waves = block_rows / 32;
   a.nbq = (N + block_rows - 1) / block_rows;
+  a.bc = block_cols;
+  a.nbc = (N + block_cols - 1) / block_cols;
   a.sm_scale = sm_scale;
   a.causal = causal ? 1 : 0;
   a.o = static_cast<uint2*>(o);
@@ -162,15 +197,15 @@ int turbo_attn_prefill(const void* q, const int8_t* k8, const int8_t* v8, const 
                        const float* s_v, int B, int Hq, int Hkv, int N, int d, float sm_scale,
                        int causal, void* o, float* lse, hipStream_t stream) {
   return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, 64, o, lse, nullptr, -1, -1, stream);
+                           causal, 64, 64, o, lse, nullptr, -1, -1, stream);
 }
 
 int turbo_attn_prefill_blocks(const void* q, const int8_t* k8, const int8_t* v8, const float* s_k,
                               const float* s_v, int B, int Hq, int Hkv, int N, int d,
-                              float sm_scale, int causal, int block_rows, void* o, float* lse,
-                              hipStream_t stream) {
+                              float sm_scale, int causal, int block_rows, int block_cols,
+                              void* o, float* lse, hipStream_t stream) {
   return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, block_rows, o, lse, nullptr, -1, -1, stream);
+                           causal, block_rows, block_cols, o, lse, nullptr, -1, -1, stream);
 }
 
 int turbo_attn_prefill_q8(const int8_t* q8, const float* s_q, const int8_t* k8, const int8_t* v8,
@@ -179,7 +214,7 @@ int turbo_attn_prefill_q8(const int8_t* q8, const float* s_q, const int8_t* k8, 
                           hipStream_t stream) {
   if (B > 0 && N > 0 && (!q8 || !s_q)) return TURBO_ERR_INVALID_ARG;
   return attn_prefill_impl(nullptr, q8, s_q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, 64, o, lse, nullptr, -1, -1, stream);
+                           causal, 64, 64, o, lse, nullptr, -1, -1, stream);
 }
 
 int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv, int d,
@@ -240,8 +275,8 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
   // logical work index of (tb, th, ti): longest query blocks first
   const int tr_L = (nb - 1 - ti) * B * Hq + tb * Hq + th;
   return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, 64, o, lse, static_cast<unsigned char*>(trace), tr_L, tj,
-                           stream);
+                           causal, 64, 64, o, lse, static_cast<unsigned char*>(trace), tr_L,
+                           tj, stream);
 }
 
 int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {

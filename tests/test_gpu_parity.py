@@ -164,36 +164,75 @@ def test_prefill_parity(orc, ta, dev, B, Hq, Hkv, N, causal):
 
 
 BLOCK_CASES = [
-    # B, Hq, Hkv, N, causal, block_rows
-    (2, 8, 2, 64 * 3 + 40, True, 32),
-    (2, 8, 2, 64 * 3 + 40, True, 128),
-    (1, 2, 1, 130, False, 32),
-    (1, 2, 1, 130, False, 128),
-    (1, 4, 4, 512, True, 128),
-    (1, 16, 1, 200, True, 128),
-    (1, 3, 3, 64 * 2 + 63, False, 128),
-    (1, 2, 2, 1, True, 32),
-    (1, 2, 2, 97, True, 128),
+    # B, Hq, Hkv, N, causal, (B_r, B_c)
+    (2, 8, 2, 64 * 3 + 40, True, (32, 64)),
+    (2, 8, 2, 64 * 3 + 40, True, (128, 64)),
+    (1, 2, 1, 130, False, (32, 64)),
+    (1, 2, 1, 130, False, (128, 64)),
+    (1, 4, 4, 512, True, (128, 64)),
+    (1, 16, 1, 200, True, (128, 64)),
+    (1, 3, 3, 64 * 2 + 63, False, (128, 64)),
+    (1, 2, 2, 1, True, (32, 64)),
+    (1, 2, 2, 97, True, (128, 64)),
+    # B_c = 32 and 128 (Table 3 pairs, plus (128, 32) and (32, 128))
+    (2, 8, 2, 64 * 3 + 40, True, (32, 32)),
+    (2, 8, 2, 64 * 3 + 40, True, (64, 32)),
+    (2, 8, 2, 64 * 3 + 40, True, (64, 128)),
+    (2, 8, 2, 64 * 3 + 40, True, (128, 128)),
+    (1, 4, 2, 64 * 5, True, (128, 32)),
+    (1, 4, 2, 64 * 5, True, (32, 128)),
+    (1, 4, 2, 64 * 5, True, (64, 128)),
+    (1, 2, 1, 130, False, (64, 32)),
+    (1, 2, 1, 130, False, (64, 128)),
+    (1, 3, 3, 64 * 2 + 63, False, (128, 128)),
+    (1, 16, 1, 200, True, (64, 32)),
+    (1, 2, 2, 17, True, (64, 128)),
+    (1, 2, 2, 33, True, (32, 32)),
 ]
 
 
-@pytest.mark.parametrize("B,Hq,Hkv,N,causal,br", BLOCK_CASES)
-def test_prefill_block_sizes(orc, ta, dev, B, Hq, Hkv, N, causal, br):
-    """Table 3's query block sizes: B_r = 32 (one wave per work-group) and
-    B_r = 128 (four waves sharing the Q scale and the P scale of the block)."""
-    _log(f"prefill B_r={br} B={B} Hq={Hq} Hkv={Hkv} N={N} causal={causal}")
+@pytest.mark.parametrize("B,Hq,Hkv,N,causal,blocks", BLOCK_CASES)
+def test_prefill_block_sizes(orc, ta, dev, B, Hq, Hkv, N, causal, blocks):
+    """Table 3's block sizes: B_r = 32 / 64 / 128 (one, two or four waves
+    sharing the Q scale and the P scale of the block) and B_c = 32 / 64 / 128
+    (the K/V step-1 blocks, the keys of each online step)."""
+    br, bc = blocks
+    _log(f"prefill B_r={br} B_c={bc} B={B} Hq={Hq} Hkv={Hkv} N={N} causal={causal}")
     q = _rand((B, Hq, N, 128), 310 + N)
     k = _rand((B, Hkv, N, 128), 410 + N)
     v = _rand((B, Hkv, N, 128), 510 + N)
     k[..., 3] *= 10
-    (k8, v8, sk, sv) = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
+    (k8, v8, sk, sv) = ta.turbo_quantize_kv(k.to(dev), v.to(dev), block_cols=bc)
     o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, 1 / np.sqrt(128), causal,
-                                   return_lse=True, block_rows=br)
+                                   return_lse=True, block_rows=br, block_cols=bc)
     torch.cuda.synchronize()
-    ro, rl = orc.attn_prefill(q, k, v, 1 / np.sqrt(128), causal, block_rows=br)
-    err = _cmp_o(o, ro, f"prefill B_r={br} O")
-    _cmp_lse(lse, rl, f"prefill B_r={br} lse")
+    ro, rl = orc.attn_prefill(q, k, v, 1 / np.sqrt(128), causal, block_rows=br, block_cols=bc)
+    err = _cmp_o(o, ro, f"prefill ({br},{bc}) O")
+    _cmp_lse(lse, rl, f"prefill ({br},{bc}) lse")
     _log(f"  vs oracle {err:.2e}")
+
+
+@pytest.mark.parametrize("bc", [32, 128])
+@pytest.mark.parametrize("B,H,N", [(1, 2, 64 * 3 + 40), (2, 3, 64 * 5), (1, 1, 17), (1, 2, 96),
+                                   (1, 1, 1), (2, 2, 64 * 8)])
+def test_quantize_kv_blocks_bit_exact(orc, ta, dev, B, H, N, bc):
+    _log(f"quantize_kv B_c={bc} B={B} H={H} N={N}")
+    k = _rand((B, H, N, 128), 120 + N)
+    v = _rand((B, H, N, 128), 220 + N)
+    k[..., 7] *= 10
+    if N >= 64:
+        v[:, 0, 32:40] *= 4   # scales that differ between the 32-token halves
+    nb = (N + 63) // 64
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev), block_cols=bc)
+    torch.cuda.synchronize()
+    ref = orc.quantize_kv_blocks(k, v, bc)
+    k8 = k8.cpu().numpy()
+    v8 = v8.cpu().numpy().transpose(0, 1, 2, 4, 3).reshape(B, H, nb * 64, 128)
+    assert np.array_equal(k8[:, :, :N], ref["k8"])
+    assert np.array_equal(v8[:, :, :N], ref["v8"])
+    assert not k8[:, :, N:].any() and not v8[:, :, N:].any()
+    assert np.array_equal(sk.cpu().numpy().view(np.int32), ref["sk"].view(np.int32))
+    assert np.array_equal(sv.cpu().numpy().view(np.int32), ref["sv"].view(np.int32))
 
 
 def test_prefill_zero_query_block(orc, ta, dev):
@@ -320,26 +359,28 @@ def test_full_size_prefill(orc, ta, dev, name, qblocks):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("br,qblocks", [(32, (126, 128)), (128, (30, 32)), (128, (0, 1))])
-def test_full_size_prefill_block_sizes(orc, ta, dev, br, qblocks):
-    """The Phi-3-medium prefill (4 x 4096, 40 / 10 heads) at B_r = 32 and 128,
-    run in full; one (sequence, KV head) unit's last or first query blocks
-    recomputed by the oracle."""
+@pytest.mark.parametrize("br,bc,qblocks", [(32, 64, (126, 128)), (128, 64, (30, 32)),
+                                           (128, 64, (0, 1)), (64, 32, (62, 64)),
+                                           (64, 128, (62, 64)), (128, 128, (31, 32))])
+def test_full_size_prefill_block_sizes(orc, ta, dev, br, bc, qblocks):
+    """The Phi-3-medium prefill (4 x 4096, 40 / 10 heads) at other block sizes
+    (B_r, B_c), run in full; one (sequence, KV head) unit's last or first
+    query blocks recomputed by the oracle."""
     from paper_2412_08585_amd import workloads as W
     w = W.WORKLOADS["phi3m-prefill-4k"]
-    _log(f"full-size prefill B_r={br} qblocks={qblocks}")
+    _log(f"full-size prefill B_r={br} B_c={bc} qblocks={qblocks}")
     q, k, v = W.prefill_inputs(w, device=dev)
-    k8, v8, sk, sv = ta.turbo_quantize_kv(k, v)
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k, v, block_cols=bc)
     o, lse = ta.turbo_attn_prefill(q, k8, v8, sk, sv, w.sm_scale, True, return_lse=True,
-                                   block_rows=br)
+                                   block_rows=br, block_cols=bc)
     torch.cuda.synchronize()
-    (b, h), = _sample_units(w, 1, seed=br + qblocks[0])
+    (b, h), = _sample_units(w, 1, seed=br + bc + qblocks[0])
     qs = q[b:b + 1, h * w.G:(h + 1) * w.G].cpu()
     ro, rl = orc.attn_prefill(qs, k[b:b + 1, h:h + 1].cpu(), v[b:b + 1, h:h + 1].cpu(),
-                              w.sm_scale, True, qblocks=qblocks, block_rows=br)
+                              w.sm_scale, True, qblocks=qblocks, block_rows=br, block_cols=bc)
     rows = slice(br * qblocks[0], br * qblocks[1])
-    _cmp_o(o[b:b + 1, h * w.G:(h + 1) * w.G, rows], ro[:, :, rows], f"B_r={br} O unit {b},{h}")
-    _cmp_lse(lse[b:b + 1, h * w.G:(h + 1) * w.G, rows], rl[:, :, rows], f"B_r={br} lse")
+    _cmp_o(o[b:b + 1, h * w.G:(h + 1) * w.G, rows], ro[:, :, rows], f"({br},{bc}) O unit {b},{h}")
+    _cmp_lse(lse[b:b + 1, h * w.G:(h + 1) * w.G, rows], rl[:, :, rows], f"({br},{bc}) lse")
     del q, k, v, k8, v8, o
     torch.cuda.empty_cache()
 

@@ -98,10 +98,15 @@ def test_invalid_arguments_rejected_before_launch(ta):
     # max_groups too small for N
     assert L.turbo_quantize_kv(dummy, dummy, 1, 1, 192, 128, dummy, dummy, dummy, dummy,
                                ctypes.byref(c), dummy, dummy, 2, None) == -1
-    # query block size outside {32, 64, 128}
-    for br in (0, 16, 96, 256):
+    # block sizes outside {32, 64, 128}
+    for br, bc in ((0, 64), (16, 64), (96, 64), (256, 64), (64, 0), (64, 16), (32, 256)):
         assert L.turbo_attn_prefill_blocks(dummy, dummy, dummy, dummy, dummy, 1, 4, 4, 64, 128,
-                                           0.1, 1, br, dummy, None, None) == -1
+                                           0.1, 1, br, bc, dummy, None, None) == -1
+    for bc in (0, 16, 48, 256):
+        assert L.turbo_quantize_kv_blocks(dummy, dummy, 1, 1, 64, 128, bc, dummy, dummy, dummy,
+                                          dummy, None) == -1
+    assert L.turbo_quantize_kv_blocks(None, None, 0, 1, 64, 128, 32, None, None, None, None,
+                                      None) == 0
     # SAS softmax: bad sizes and null pointers; zero rows is a no-op
     assert L.turbo_sas_softmax(dummy, dummy, -1, 8, None) == -1
     assert L.turbo_sas_softmax(dummy, dummy, 4, 0, None) == -1
