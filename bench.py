@@ -63,6 +63,20 @@ def decode_bytes_per_token(bits: int) -> float:
     return 2 * 128 * bits / 8 + 4 * 128 / 64 + 8 / 64
 
 
+def ramp_clocks(fn, seconds: float = 0.2):
+    """Untimed launches of the step until `seconds` of wall time have passed:
+    the GPU idles during input generation and its clocks fall; the warmup
+    steps proper (--warmup) and the timed steps (--steps) follow."""
+    import time
+
+    import torch
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,7 +141,7 @@ def main():
     od = torch.empty_like(qd)
     lse = torch.empty(B, Hq, N, dtype=torch.float32, device=dev)
     sl = torch.full((B,), N, dtype=torch.int32, device=dev)
-    split = ta.decode_split(B, Hkv, w.max_groups, 0)
+    split = ta.decode_split(B, Hq, Hkv, w.max_groups, 0)
     ws = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev)
 
     def run_quant():
@@ -154,6 +168,7 @@ def main():
         return
 
     # ---- whole-step timing ----------------------------------------------------
+    ramp_clocks(step)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -178,9 +193,26 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / iters
 
+    def time_after(prev, fn, iters):
+        """GPU time of fn launched behind prev: the events bracket fn alone,
+        and prev (about 1 ms) hides the host's launch overhead of fn, which
+        for the 15-us decode of this workload exceeds its GPU time."""
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(iters)]
+        prev()
+        fn()
+        torch.cuda.synchronize()
+        for a, b in ev:
+            prev()
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in ev) / iters
+
     ms_q = time_kernel(run_quant, args.kernel_iters)
     ms_p = time_kernel(run_prefill, args.kernel_iters)
-    ms_d = time_kernel(run_decode, args.kernel_iters)
+    ms_d = time_after(run_prefill, run_decode, args.kernel_iters)
     prio = torch.empty(Hkv, dtype=torch.float32, device=dev)
     ms_h = time_kernel(lambda: ta.binding.lib().turbo_head_priority(
         ta.binding._ptr(k), B, Hkv, N, d, ta.binding._ptr(prio), ta.binding._stream(dev)),
@@ -309,7 +341,7 @@ def bench_decode(args, w):
     torch.cuda.synchronize()
     q = W.decode_query(w, device=dev)
     sl = torch.full((B,), N, dtype=torch.int32, device=dev)
-    split = ta.decode_split(B, Hkv, w.max_groups, 0)
+    split = ta.decode_split(B, Hq, Hkv, w.max_groups, 0)
     ws = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev)
     o = torch.empty_like(q)
     it = [0]
@@ -325,6 +357,7 @@ def bench_decode(args, w):
         torch.cuda.synchronize()
         print(json.dumps({"only": "decode", "launches": args.warmup + args.steps}))
         return
+    ramp_clocks(run)
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
@@ -412,6 +445,7 @@ def bench_softmax(args, w):
     y = torch.empty_like(x)
     rows, cols = x.shape
     run = lambda: ta.turbo_sas_softmax(x, out=y)
+    ramp_clocks(run)
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
@@ -471,6 +505,7 @@ def bench_projection(args, w):
     stream = torch.cuda.current_stream()
 
     def time_loop(fn, iters):
+        ramp_clocks(fn)
         for _ in range(args.warmup):
             fn()
         torch.cuda.synchronize()

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define TURBO_ABI_VERSION 2
+#define TURBO_ABI_VERSION 3
 
 #define TURBO_HEAD_DIM 128       /* d */
 #define TURBO_BLOCK 64           /* B_r = B_c = step-2 group length (tokens) */
@@ -336,7 +336,7 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
  *                 is out of range is skipped (its memory is never read).
  * B, Hq           Hq % Hkv == 0, Hq / Hkv <= 16.
  * kv_split_groups groups per chunk, >= 1; 0 selects
- *                 turbo_decode_auto_split(B, Hkv, max_groups_per_seq) with
+ *                 turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq) with
  *                 Hkv = cache->num_kv_heads (see below).
  * workspace       device scratch of at least turbo_decode_workspace_bytes()
  *                 bytes (with_tail = tail != NULL; may be NULL when that is 0).
@@ -443,18 +443,21 @@ int turbo_append_kv(const void* k_new, const void* v_new, int B, int Hkv, int d,
 int turbo_sas_softmax(const float* x, float* y, int64_t rows, int cols, hipStream_t stream);
 
 /* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
- * a decode batch of B sequences, Hkv KV heads and max_groups_per_seq.  It
- * minimizes ceil(B*Hkv*chunks / 2048) * (chunk length + 2), the number of
- * rounds of resident decode waves (two per SIMD on 256 CUs) times a wave's
- * run time in group steps, preferring longer chunks on ties.  Since the
- * chunked result merges SAS-weighted partial states, the output depends on
- * the chunk length; pass an explicit kv_split_groups for results that do not
- * depend on the batch shape. */
-int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq);
+ * a decode batch of B sequences, Hq query and Hkv KV heads and
+ * max_groups_per_seq.  The decode kernel keeps three waves per SIMD resident
+ * when Hq / Hkv <= 4 and two otherwise (3072 or 2048 on 256 CUs); the
+ * fewest chunks n whose B * Hkv * n waves fill at least two thirds of those
+ * slots are chosen, with chunk length ceil(max_groups_per_seq / n) (the
+ * whole sequence when B * Hkv already fills them), but never fewer than two
+ * groups per chunk.  Since the chunked result merges SAS-weighted
+ * partial states, the output depends on the chunk length; pass an explicit
+ * kv_split_groups for results that do not depend on the batch shape.
+ * Returns 1 for arguments < 1. */
+int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq);
 
 /* Workspace bytes turbo_attn_decode needs for these arguments (0 when every
  * sequence fits one chunk and there is no tail).  kv_split_groups = 0 means
- * turbo_decode_auto_split(B, Hkv, max_groups_per_seq); with_tail != 0 adds
+ * turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq); with_tail != 0 adds
  * the buffer's chunk. */
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
                                     int kv_split_groups, int with_tail);

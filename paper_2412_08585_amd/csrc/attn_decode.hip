@@ -41,6 +41,7 @@ struct DecodeArgs {
   const int8_t* gmeta;       // [slots][Hkv][4][128]
   const float* gscale;       // [slots][Hkv][2]
   long num_pages, num_slots;
+  int npages32, nslots32;    // min(num_pages, INT_MAX), min(num_slots, INT_MAX)
   int page_bytes;
   unsigned long long int2_mask;
   const int* seq_lens;       // [B]
@@ -107,96 +108,118 @@ __device__ __forceinline__ int vpos(int j) {
   return 4 * (j & 3) + (j >> 2);
 }
 
+// Columns of the PV exchange: GP rows plus, for 4 <= GP < 16, four columns
+// that take the stores of the lanes holding unused rows (so no lane needs
+// its own branch around a store).
+template <int GP>
+constexpr int kObufCols = GP < 4 ? GP : (GP < 16 ? GP + 4 : GP);
+
 template <int GP>
 struct DecodeLds {
   float lut[8];
   float sq[16];
-  int sbuf[GP][64];             // scores, row-major
-  unsigned char pbuf[GP][64];   // Q(P~), per page in V-unpack order
-  int obuf[128][GP];            // PV accumulators, channel-major
-  float4 rowv[GP];              // per row: g = s_P s_V / beta, sum Q(P~), renorm, -
+  int sbuf[GP + 1][64];             // scores, row-major; row GP: stores of unused rows
+  unsigned char pbuf[GP + 1][64];   // Q(P~), per page in V-unpack order; row GP: read by
+                                    // unused rows (their products are never kept)
+  int obuf[128][kObufCols<GP>];     // PV accumulators, channel-major
+  float4 rowv[GP];                  // per row: g = s_P s_V / beta, sum Q(P~), renorm, -
 };
 
-// Everything one group needs from memory, loaded one group ahead.
+// Broadcast of lane I of each 16-lane row to the whole row (DPP row_newbcast).
+template <int I>
+__device__ __forceinline__ unsigned row_bcast(unsigned v) {
+  return (unsigned)__builtin_amdgcn_mov_dpp((int)v, 0x150 + I, 0xf, 0xf, false);
+}
+
+// K side of one group, loaded one group ahead of its step.  The table
+// entries, the slot and the float scales are wave-uniform.  A group that is
+// not live (past the chunk) or has an out-of-range entry (a caller error; it
+// is skipped) still issues every load, from page 0 and slot 0, so that the
+// number of memory operations in flight is the same on every path and the
+// waits before each use stay exact.
+//
+// A-operand row m of m-block mb holds token 16*mb + m, so each m-block reads
+// one page: its base address is wave-uniform and the lane adds its own
+// offset (token row m, channel block g4).
 template <int BITS>
-struct GroupData {
+struct GroupK {
   bool ok;
-  const uint8_t* krow;          // K codes of this lane's A-operand rows (page m>>2)
-  const uint8_t* vreg;          // V codes of page g4
-  const int8_t* meta;
-  float skg, svg;
-  unsigned kraw[4][BITS];       // K codes of the 4 A-operand rows (32 channels each)
-  unsigned ks4[8], kz4[8];      // K scale / zero of the lane's 32 channels
-  unsigned vraw[8][BITS / 2];   // V codes of channel 16*cb + n in page g4
-  unsigned vs4, vz4;            // V scales / zeros of channels 2L&~3 .. +3 (aligned dwords);
-                                // kept as loaded: arithmetic on them here would make the
-                                // loop wait for the prefetch of the next group
+  int pg[4];                // page of each 16-token quarter (clamped into range)
+  int vpg;                  // page of quarter g4 (this lane's PV K-chunk), clamped
+  int slot;                 // group slot (clamped)
+  float skg, svg;           // float scales s_K, s_V of the group
+  unsigned kraw[4][BITS];   // K codes of the lane's 4 A-operand rows (32 channels each)
+  unsigned kmeta;           // dword (lane & 15) of the s^int (8 dwords) and z^int (8 dwords)
+                            // bytes of the lane's 32 K channels; the row holds all 16
+};
+
+// V side of one group, loaded by the group's own step after its QK^T.
+template <int BITS>
+struct GroupV {
+  unsigned vraw[8][BITS / 2];  // V codes of channel 16*cb + n in page g4
+  unsigned vs4, vz4;           // V scales / zeros of channels 2L&~3 .. +3 (aligned dwords)
 };
 
 template <int BITS>
-__device__ __forceinline__ void load_group(const DecodeArgs& a, int kh, int head_off,
-                                           const int* bt, const int* gt, int g, bool live,
-                                           GroupData<BITS>& D) {
+__device__ __forceinline__ void load_k(const DecodeArgs& a, int kh, int head_off, const int* bt,
+                                       const int* gt, int g, bool live, GroupK<BITS>& K) {
   const int lane = threadIdx.x;
   const int n = lane & 15, g4 = lane >> 4, m = lane & 15;
   g = live ? g : 0;
-  const long p0 = bt[4 * g], p1 = bt[4 * g + 1], p2 = bt[4 * g + 2], p3 = bt[4 * g + 3];
-  bool ok = live && p0 >= 0 && p0 < a.num_pages && p1 >= 0 && p1 < a.num_pages && p2 >= 0 &&
-            p2 < a.num_pages && p3 >= 0 && p3 < a.num_pages;
-  const long slot = gt[g];
-  ok = ok && slot >= 0 && slot < a.num_slots;
-  D.ok = ok;
-  // The loads are issued on every path, so that the number of memory
-  // operations in flight is the same whatever the tables hold (and the wait
-  // counts before each use stay exact): a group that is not live (past the
-  // chunk) or has an out-of-range entry (a caller error; it is skipped) reads
-  // the first bytes of q instead.
-  const uint8_t* dummy = reinterpret_cast<const uint8_t*>(a.q);
-  D.meta = ok ? a.gmeta + (slot * a.Hkv + kh) * 512 : reinterpret_cast<const int8_t*>(dummy);
-  const float* gs = ok ? a.gscale + (slot * a.Hkv + kh) * 2 : reinterpret_cast<const float*>(dummy);
-  D.skg = gs[0];
-  D.svg = gs[1];
-  // lane-dependent page choice by selects (no dynamic indexing of an array)
-  const int pk = m >> 2;
-  const long pgk = pk == 0 ? p0 : pk == 1 ? p1 : pk == 2 ? p2 : p3;
-  const long pgv = g4 == 0 ? p0 : g4 == 1 ? p1 : g4 == 2 ? p2 : p3;
-  D.krow = ok ? a.pages + pgk * a.page_bytes + head_off + (m & 3) * 16 * BITS + 4 * BITS * g4
-              : dummy;
-  D.vreg = ok ? a.pages + pgv * a.page_bytes + head_off + 256 * BITS : dummy;
-  const int kstep = ok ? 4 * 16 * BITS : 0, vstep = ok ? 2 * BITS : 0;  // V: 16 codes per channel
-  const int mstep = ok ? 1 : 0;
+  bool ok = live;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int p = bt[4 * g + i];
+    ok = ok && p >= 0 && p < a.npages32;
+    K.pg[i] = p;
+  }
+  const int slot = gt[g];
+  ok = ok && slot >= 0 && slot < a.nslots32;
+  K.ok = ok;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) K.pg[i] = ok ? K.pg[i] : 0;
+  K.slot = ok ? slot : 0;
+  // this lane's V page, read by the lane itself (no per-lane choice among
+  // the four uniform values)
+  const int vp = bt[4 * g + g4];
+  K.vpg = ok ? vp : 0;
+  const int8_t* meta = a.gmeta + ((long)K.slot * a.Hkv + kh) * 512;
+  const float* gs = a.gscale + ((long)K.slot * a.Hkv + kh) * 2;
+  K.skg = gs[0];
+  K.svg = gs[1];
+  const int koff = head_off + m * 16 * BITS + 4 * BITS * g4;
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
-    const uint8_t* krow = D.krow + mb * kstep;
+    const uint8_t* krow = a.pages + (long)K.pg[mb] * a.page_bytes + koff;
     if constexpr (BITS == 4) {
       const uint4 x = *reinterpret_cast<const uint4*>(krow);
-      D.kraw[mb][0] = x.x; D.kraw[mb][1] = x.y; D.kraw[mb][2] = x.z; D.kraw[mb][3] = x.w;
+      K.kraw[mb][0] = x.x; K.kraw[mb][1] = x.y; K.kraw[mb][2] = x.z; K.kraw[mb][3] = x.w;
     } else {
       const uint2 x = *reinterpret_cast<const uint2*>(krow);
-      D.kraw[mb][0] = x.x; D.kraw[mb][1] = x.y;
+      K.kraw[mb][0] = x.x; K.kraw[mb][1] = x.y;
     }
   }
-  {
-    const uint4* ms = reinterpret_cast<const uint4*>(D.meta + (32 * g4) * mstep);
-    const uint4* mz = reinterpret_cast<const uint4*>(D.meta + (128 + 32 * g4) * mstep);
-    const uint4 t0 = ms[0], t1 = ms[mstep], z0 = mz[0], z1 = mz[mstep];
-    D.ks4[0] = t0.x; D.ks4[1] = t0.y; D.ks4[2] = t0.z; D.ks4[3] = t0.w;
-    D.ks4[4] = t1.x; D.ks4[5] = t1.y; D.ks4[6] = t1.z; D.ks4[7] = t1.w;
-    D.kz4[0] = z0.x; D.kz4[1] = z0.y; D.kz4[2] = z0.z; D.kz4[3] = z0.w;
-    D.kz4[4] = z1.x; D.kz4[5] = z1.y; D.kz4[6] = z1.z; D.kz4[7] = z1.w;
-  }
+  K.kmeta = *reinterpret_cast<const unsigned*>(meta + 32 * g4 + 4 * (n & 7) + 128 * (n >> 3));
+}
+
+template <int BITS>
+__device__ __forceinline__ void load_v(const DecodeArgs& a, int kh, int head_off,
+                                       const GroupK<BITS>& K, GroupV<BITS>& V) {
+  const int lane = threadIdx.x;
+  const int n = lane & 15;
+  const uint8_t* vrow = a.pages + (long)K.vpg * a.page_bytes + head_off + 256 * BITS + n * 2 * BITS;
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb) {
-    const int ch = 16 * cb + n;
     if constexpr (BITS == 4) {
-      const uint2 x = *reinterpret_cast<const uint2*>(D.vreg + ch * vstep);
-      D.vraw[cb][0] = x.x; D.vraw[cb][1] = x.y;
+      const uint2 x = *reinterpret_cast<const uint2*>(vrow + cb * 32 * BITS);
+      V.vraw[cb][0] = x.x; V.vraw[cb][1] = x.y;
     } else {
-      D.vraw[cb][0] = *reinterpret_cast<const unsigned*>(D.vreg + ch * vstep);
+      V.vraw[cb][0] = *reinterpret_cast<const unsigned*>(vrow + cb * 32 * BITS);
     }
   }
-  D.vs4 = *reinterpret_cast<const unsigned*>(D.meta + (256 + 4 * (lane >> 1)) * mstep);
-  D.vz4 = *reinterpret_cast<const unsigned*>(D.meta + (384 + 4 * (lane >> 1)) * mstep);
+  const int8_t* meta = a.gmeta + ((long)K.slot * a.Hkv + kh) * 512;
+  V.vs4 = *reinterpret_cast<const unsigned*>(meta + 256 + 4 * (lane >> 1));
+  V.vz4 = *reinterpret_cast<const unsigned*>(meta + 384 + 4 * (lane >> 1));
 }
 
 template <int GP, int BITS, bool kTrace>
@@ -209,6 +232,8 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   const int lane = threadIdx.x;
   const int n = lane & 15, g4 = lane >> 4;
   const int rr = lane / LPR, cc = lane % LPR;
+  const int nrow = min(n, GP);      // exchange row of this lane (GP: unused rows)
+  const int ocol = min(4 * g4, GP);  // PV exchange column (GP >= 4; GP..GP+3: unused rows)
 
   // 16-bit (q_ca, q_cb) pairs in the order the K codes unpack to: B-operand
   // dword j of k-step ks covers channels c0 + {0, d, 2d, 3d}; pair xy = 0 is
@@ -231,14 +256,23 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   const int* bt = a.block_table + (long)b * 4 * a.max_groups;
   const int* gt = a.group_table + (long)b * a.max_groups;
 
-  // Two prefetch buffers used alternately (a copy cur = nxt between groups
-  // would be a register move that waits for the prefetch to land).  Every
-  // prefetch is issued on every path so that the wait before each use covers
-  // exactly the loads that use needs.
-  GroupData<BITS> A, Bd;
-  load_group<BITS>(a, kh, head_off, bt, gt, g0, g0 < g1, A);
-  auto process = [&](const GroupData<BITS>& cur, int g) {
+  // Two K prefetch buffers used alternately (a copy cur = nxt between groups
+  // would be a register move that waits for the prefetch to land).  A step
+  // issues K of the next group first and V of its own group after its QK^T
+  // MFMAs (V is not held during the QK^T phase); the softmax covers the V
+  // latency.
+  GroupK<BITS> KA, KB;
+  load_k<BITS>(a, kh, head_off, bt, gt, g0, g0 < g1, KA);
+  auto process = [&](const GroupK<BITS>& cur, int g) {
     if (cur.ok) {
+      // the K scale / zero bytes of the lane's 32 channels, from its row
+      const unsigned km = cur.kmeta;
+      const unsigned ks4[8] = {row_bcast<0>(km), row_bcast<1>(km), row_bcast<2>(km),
+                               row_bcast<3>(km), row_bcast<4>(km), row_bcast<5>(km),
+                               row_bcast<6>(km), row_bcast<7>(km)};
+      const unsigned kz4[8] = {row_bcast<8>(km),  row_bcast<9>(km),  row_bcast<10>(km),
+                               row_bcast<11>(km), row_bcast<12>(km), row_bcast<13>(km),
+                               row_bcast<14>(km), row_bcast<15>(km)};
       // ---- hi/lo B-operands from w = q * s^int (this lane's 32 channels)
       v4i bhi[2], blo[2];
 #pragma unroll
@@ -254,7 +288,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
             // bytes [s_ca, 0, s_cb, 0]: the 16-bit pair (s_ca, s_cb)
             const unsigned selb = (cb >> 2) == (ca >> 2) ? (unsigned)(cb & 3) : 4u + (cb & 3);
             const unsigned sel = (unsigned)(ca & 3) | (0x0cu << 8) | (selb << 16) | (0x0cu << 24);
-            const unsigned spair = __builtin_amdgcn_perm(cur.ks4[cb >> 2], cur.ks4[ca >> 2], sel);
+            const unsigned spair = __builtin_amdgcn_perm(ks4[cb >> 2], ks4[ca >> 2], sel);
             const u16x2 w =
                 __builtin_bit_cast(u16x2, qpair[ks][j][xy]) * __builtin_bit_cast(u16x2, spair);
             hx[xy] = __builtin_bit_cast(unsigned, __builtin_bit_cast(s16x2, w) >> (short)7);
@@ -269,7 +303,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
       // zero-point term sum_c q_c z_c over the lane's channels, then over g4
       int bias = 0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) bias = __builtin_amdgcn_sdot4(q8w[i], (int)cur.kz4[i], bias, false);
+      for (int i = 0; i < 8; ++i) bias = __builtin_amdgcn_sdot4(q8w[i], (int)kz4[i], bias, false);
       bias = (int)add_xor32((float)bias);  // exact: |bias| < 2^24
       {
         const unsigned u = (unsigned)bias;
@@ -308,16 +342,17 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         sv[mb] = make_int4((hi[0] << 7) + lo[0], (hi[1] << 7) + lo[1], (hi[2] << 7) + lo[2],
                            (hi[3] << 7) + lo[3]);
       }
-      if (n < GP) {
+      GroupV<BITS> cv;
+      load_v<BITS>(a, kh, head_off, cur, cv);
+      // lane (n, g4), register r of m-block mb: row n, token 16*mb + 4*g4 + r
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-          *reinterpret_cast<int4*>(&L.sbuf[n < GP ? n : 0][16 * g4 + 4 * mb]) = sv[mb];
-      }
+      for (int mb = 0; mb < 4; ++mb)
+        *reinterpret_cast<int4*>(&L.sbuf[nrow][16 * mb + 4 * g4]) = sv[mb];
       const bool trace_g = kTrace && trow >= 0 && g == a.tr_g;  // wave-uniform
       if (trace_g && n == trow) {
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb)
-          reinterpret_cast<int4*>(a.trace + TURBO_TRACE_S)[4 * g4 + mb] = sv[mb];
+          reinterpret_cast<int4*>(a.trace + TURBO_TRACE_S)[4 * mb + g4] = sv[mb];
       }
       __syncthreads();
       // ---- compact softmax: lane (rr, cc) holds tokens cc*GP .. +GP-1 -----
@@ -376,22 +411,24 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         if (trace_g && rr == trow && cc == 0)
           *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
         const int psum = (int)row_sum<LPR>((float)ps);  // exact: < 2^24
-        const float gsc = ((pmax / kQmax) * cur.svg) * __builtin_amdgcn_rcpf(beta);
-        if (cc == 0) L.rowv[rr] = make_float4(gsc, __int_as_float(psum), rf, 0.0f);
+        // s_P s_V / beta scales the fp32 accumulator only (no integer depends
+        // on it): s_P as pmax times the binary32 1/119
+        const float gsc = ((pmax * (1.0f / kQmax)) * cur.svg) * __builtin_amdgcn_rcpf(beta);
+        // every lane of the row holds the same values
+        L.rowv[rr] = make_float4(gsc, __int_as_float(psum), rf, 0.0f);
       }
       __syncthreads();
       // ---- O = Q(P~) V on the raw codes (A = P rows, B = V codes) -------
-      const v4i pop = n < GP ? *reinterpret_cast<const v4i*>(&L.pbuf[n < GP ? n : 0][16 * g4])
-                             : v4i{0, 0, 0, 0};
+      const v4i pop = *reinterpret_cast<const v4i*>(&L.pbuf[nrow][16 * g4]);
 #pragma unroll
       for (int cb = 0; cb < 8; ++cb) {
         v4i vop;
         if (BITS == 4) {
-          const unsigned x0 = cur.vraw[cb][0], x1 = cur.vraw[cb][BITS / 2 - 1];
+          const unsigned x0 = cv.vraw[cb][0], x1 = cv.vraw[cb][BITS / 2 - 1];
           vop = v4i{(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
                     (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
         } else {
-          const unsigned x = cur.vraw[cb][0];
+          const unsigned x = cv.vraw[cb][0];
           vop = v4i{(int)(x & 0x03030303u), (int)((x >> 2) & 0x03030303u),
                     (int)((x >> 4) & 0x03030303u), (int)((x >> 6) & 0x03030303u)};
         }
@@ -399,9 +436,8 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         acc = mfma16x16x64(pop, vop, acc);
         // lane (n, g4), register r <-> row 4*g4 + r, channel 16*cb + n
         if (GP >= 4) {
-          if (4 * g4 < GP)
-            *reinterpret_cast<int4*>(&L.obuf[16 * cb + n][4 * g4 < GP ? 4 * g4 : 0]) =
-                make_int4(acc[0], acc[1], acc[2], acc[3]);
+          *reinterpret_cast<int4*>(&L.obuf[16 * cb + n][ocol]) =
+              make_int4(acc[0], acc[1], acc[2], acc[3]);
         } else if (g4 == 0) {
 #pragma unroll
           for (int r = 0; r < GP; ++r) L.obuf[16 * cb + n][r] = acc[r];
@@ -425,9 +461,9 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
           }
         }
         const int sh = 16 * (lane & 1);  // channels 2L, 2L+1 within the dword
-        const int s0 = (int)((cur.vs4 >> sh) & 0xffu), s1 = (int)((cur.vs4 >> (sh + 8)) & 0xffu);
-        const int z0 = (int)(int8_t)((cur.vz4 >> sh) & 0xffu);
-        const int z1 = (int)(int8_t)((cur.vz4 >> (sh + 8)) & 0xffu);
+        const int s0 = (int)((cv.vs4 >> sh) & 0xffu), s1 = (int)((cv.vs4 >> (sh + 8)) & 0xffu);
+        const int z0 = (int)(int8_t)((cv.vz4 >> sh) & 0xffu);
+        const int z1 = (int)(int8_t)((cv.vz4 >> (sh + 8)) & 0xffu);
 #pragma unroll
         for (int r = 0; r < GP; ++r) {
           const float4 rv = L.rowv[r];
@@ -436,28 +472,33 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
             O[r][0] *= rv.z;
             O[r][1] *= rv.z;
           }
-          // exact int32 PV of Algorithm 2: s * sum P*code + z * sum P
-          O[r][0] = __builtin_fmaf(rv.x, (float)(s0 * acc[0][r] + z0 * psum), O[r][0]);
-          O[r][1] = __builtin_fmaf(rv.x, (float)(s1 * acc[1][r] + z1 * psum), O[r][1]);
+          // exact int32 PV of Algorithm 2: s * sum P*code + z * sum P (every
+          // factor fits 24 bits: s <= 80, |z| <= 127, sum P <= 64*119,
+          // |sum P*code| <= 64*119*15)
+          const int pv0 = __mul24(s0, acc[0][r]) + __mul24(z0, psum);
+          const int pv1 = __mul24(s1, acc[1][r]) + __mul24(z1, psum);
+          O[r][0] = __builtin_fmaf(rv.x, (float)pv0, O[r][0]);
+          O[r][1] = __builtin_fmaf(rv.x, (float)pv1, O[r][1]);
           if (trace_g && r == trow)
-            reinterpret_cast<int2*>(a.trace + TURBO_TRACE_PV)[lane] =
-                make_int2(s0 * acc[0][r] + z0 * psum, s1 * acc[1][r] + z1 * psum);
+            reinterpret_cast<int2*>(a.trace + TURBO_TRACE_PV)[lane] = make_int2(pv0, pv1);
         }
       }
     }
   };
   for (int g = g0; g < g1; g += 2) {
-    load_group<BITS>(a, kh, head_off, bt, gt, g + 1, g + 1 < g1, Bd);
-    process(A, g);
-    load_group<BITS>(a, kh, head_off, bt, gt, g + 2, g + 2 < g1, A);
-    if (g + 1 < g1) process(Bd, g + 1);
+    load_k<BITS>(a, kh, head_off, bt, gt, g + 1, g + 1 < g1, KB);
+    process(KA, g);
+    if (g + 1 < g1) {
+      load_k<BITS>(a, kh, head_off, bt, gt, g + 2, g + 2 < g1, KA);
+      process(KB, g + 1);
+    }
   }
 }
 
 // kTrace = true only for the test hook that also stores one group's integers
 // (the production instances carry no trace code).
 template <int GP, bool kTrace>
-__global__ __launch_bounds__(64) void k_attn_decode(DecodeArgs a) {
+__global__ __launch_bounds__(64, (GP <= 4 && !kTrace) ? 3 : 2) void k_attn_decode(DecodeArgs a) {
   __shared__ DecodeLds<GP> L;
   constexpr int LPR = 64 / GP;
   const int lane = threadIdx.x;

@@ -1,6 +1,7 @@
 // C ABI of the gfx950 TurboAttention hot path: argument checks on the host,
 // then the kernel launches on the caller's stream.  No allocation, no
 // synchronization, no exception crosses the boundary.
+#include <algorithm>
 #include <atomic>
 #include <cstring>
 
@@ -279,35 +280,34 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
                            tj, stream);
 }
 
-int turbo_decode_auto_split(int B, int Hkv, int max_groups_per_seq) {
-  if (B < 1 || Hkv < 1 || max_groups_per_seq < 1) return 1;
-  // One wave per (sequence, KV head, chunk); every decode kernel variant holds
-  // two waves per SIMD, 2048 on the 256 CUs of gfx950.  A wave's run time is
-  // set by its per-group latency chain rather than by its bytes (int2 and int4
-  // chunks take the same time), about (groups + 2) group steps with the
-  // prologue and epilogue.  So take the chunk length minimizing
-  //   ceil(waves / 2048) * (chunk + 2),
-  // the longest chunk on ties (fewer partial states to merge).
-  constexpr long kSlots = 2048;
+int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || max_groups_per_seq < 1) return 1;
+  // One wave per (sequence, KV head, chunk).  The decode kernel holds three
+  // waves per SIMD when a KV head has at most 4 query heads and two
+  // otherwise: 3072 or 2048 resident waves on the 256 CUs of gfx950.  A
+  // wave's run time is set by its per-group latency chain, and the chunks of
+  // a sequence are merged afterwards, so take the fewest chunks whose waves
+  // fill at least two thirds of the resident slots (one chunk when the
+  // sequences alone do), with the groups spread evenly over them.  A chunk
+  // holds at least two groups: below that the fixed cost of a wave (query
+  // quantization, state write) and of the merge outweigh the parallelism.
+  const long slots = 1024L * ((Hq / Hkv) <= 4 ? 3 : 2);
+  const long want = (2 * slots + 2) / 3;
   const long units = (long)B * Hkv, G = max_groups_per_seq;
-  long best_split = G, best_cost = -1;
-  for (long split = G; split >= 1; --split) {
-    const long n = (G + split - 1) / split;
-    const long rounds = (units * n + kSlots - 1) / kSlots;
-    const long cost = rounds * (split + 2);
-    if (best_cost < 0 || cost < best_cost) {
-      best_cost = cost;
-      best_split = split;
-    }
+  const long min_split = G < 2 ? G : 2;
+  for (long n = 1; n <= G; ++n) {
+    const long split = (G + n - 1) / n;
+    if (split <= min_split || units * ((G + split - 1) / split) >= want)
+      return (int)(split > min_split ? split : min_split);
   }
-  return (int)best_split;
+  return (int)min_split;
 }
 
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
                                     int kv_split_groups, int with_tail) {
   if (B < 1 || Hq < 1 || Hkv < 1 || max_groups_per_seq < 1 || kv_split_groups < 0) return 0;
   const int split = kv_split_groups ? kv_split_groups
-                                    : turbo_decode_auto_split(B, Hkv, max_groups_per_seq);
+                                    : turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq);
   const long nws = (max_groups_per_seq + split - 1) / split + (with_tail ? 1 : 0);
   if (nws <= 1) return 0;
   return (size_t)B * Hq * nws * turbo::kWsStride * sizeof(float);
@@ -341,7 +341,7 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache,
   st = check_tail(tail, B, Hkv);
   if (st != TURBO_OK) return st;
   const int split = kv_split_groups ? kv_split_groups
-                                    : turbo_decode_auto_split(B, Hkv, max_groups_per_seq);
+                                    : turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq);
   const long nsplit = (max_groups_per_seq + split - 1) / split;
   if ((long)B * Hkv * nsplit > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
   const size_t need =
@@ -355,6 +355,8 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache,
   a.gscale = cache->group_scale;
   a.num_pages = cache->num_pages;
   a.num_slots = cache->num_group_slots;
+  a.npages32 = (int)std::min<long>(cache->num_pages, 0x7fffffffL);
+  a.nslots32 = (int)std::min<long>(cache->num_group_slots, 0x7fffffffL);
   a.seq_lens = seq_lens;
   a.block_table = block_table;
   a.group_table = group_table;

@@ -272,7 +272,7 @@ def test_decode_parity(orc, ta, dev, B, Hq, Hkv, Nc, bits, sl, split):
                                   return_lse=True)
     torch.cuda.synchronize()
     ref = orc.quantize_kv(k, v, bits)
-    used = ta.decode_split(B, Hkv, Nc // 64, split)
+    used = ta.decode_split(B, Hq, Hkv, Nc // 64, split)
     ro, rl = orc.attn_decode(q, ref, sl, 1 / np.sqrt(128), split=used)
     _cmp_o(o, ro, "decode O")
     _cmp_lse(lse, rl, "decode lse")
@@ -414,7 +414,7 @@ def test_full_size_decode(orc, ta, dev, name):
     sl = torch.full((w.B,), w.N, dtype=torch.int32, device=dev)
     o, lse = ta.turbo_attn_decode(q, cache, sl, btd, gtd, w.sm_scale, 0, return_lse=True)
     torch.cuda.synchronize()
-    split = ta.decode_split(w.B, w.Hkv, w.max_groups, 0)
+    split = ta.decode_split(w.B, w.Hq, w.Hkv, w.max_groups, 0)
     pages = cache.pages.cpu().numpy()
     gmeta = cache.group_meta.cpu().numpy()
     gscale = cache.group_scale.cpu().numpy()

@@ -204,7 +204,7 @@ def test_decode_with_buffer_parity(orc, ta, dev, B, Hq, Hkv, N, mg, bits, extra,
     o, lse = ta.turbo_attn_decode(q.to(dev), s.cache, sld, s.btd, s.gtd, SM, split,
                                   return_lse=True, tail=s.tail)
     torch.cuda.synchronize()
-    used = ta.decode_split(B, Hkv, mg, split)
+    used = ta.decode_split(B, Hq, Hkv, mg, split)
     ro, rl = orc.attn_decode(q, s.rcache, seq, SM, split=used, tail=s.rtail)
     _cmp_o(o, ro, "decode+buffer O")
     _cmp_lse(lse, rl, "decode+buffer lse")

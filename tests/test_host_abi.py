@@ -43,7 +43,7 @@ def test_exports_every_declared_function(ta):
 
 def test_version_and_strerror(ta):
     L = ta.lib()
-    assert L.turbo_abi_version() == 2
+    assert L.turbo_abi_version() == 3
     for st in (0, -1, -2, -3, -4, 7):
         assert L.turbo_strerror(st)
 
@@ -201,23 +201,28 @@ def test_int2_heads_rule_matches_the_oracle(ta, orc):
 
 def test_decode_split_and_workspace(ta):
     L = ta.lib()
-    # chunk minimizing ceil(waves / 2048) * (chunk + 2), longest on ties
-    assert L.turbo_decode_auto_split(64, 10, 128) == 43       # 3 chunks: 1920 waves, one round
-    assert L.turbo_decode_auto_split(256, 8, 512) == 512      # 2048 waves unsplit, one round
-    assert L.turbo_decode_auto_split(4096, 8, 4) == 4         # one chunk (16 rounds either way)
-    assert L.turbo_decode_auto_split(4, 10, 64) == 2          # 32 chunks: 1280 waves
-    assert L.turbo_decode_auto_split(1, 1, 1) == 1
+    # fewest (evenly filled) chunks whose waves fill two thirds of the
+    # resident slots: 3072 (3 waves per SIMD) for up to 4 query heads per KV
+    # head, else 2048
+    assert L.turbo_decode_auto_split(64, 40, 10, 128) == 32   # 4 chunks: 2560 waves >= 2048
+    assert L.turbo_decode_auto_split(256, 32, 8, 512) == 512  # 2048 waves unsplit
+    assert L.turbo_decode_auto_split(4096, 32, 8, 4) == 4     # one chunk
+    assert L.turbo_decode_auto_split(4, 40, 10, 64) == 2      # at least 2 groups a chunk
+    assert L.turbo_decode_auto_split(16, 128, 8, 64) == 6     # G = 16: 11 chunks, 1408 >= 1366
+    assert L.turbo_decode_auto_split(1, 1, 1, 1) == 1
+    assert L.turbo_decode_auto_split(1, 1, 1, 5) == 2
+    assert L.turbo_decode_auto_split(0, 1, 1, 1) == 1
 
-    def brute(B, Hkv, G):
-        best = None
-        for split in range(G, 0, -1):
-            n = -(-G // split)
-            cost = -(-(B * Hkv * n) // 2048) * (split + 2)
-            if best is None or cost < best[0]:
-                best = (cost, split)
-        return best[1]
-    for B, Hkv, G in [(1, 8, 256), (8, 8, 128), (32, 4, 300), (128, 16, 64), (3, 5, 7)]:
-        assert L.turbo_decode_auto_split(B, Hkv, G) == brute(B, Hkv, G)
+    def brute(B, Hq, Hkv, G):
+        want = -(-2 * 1024 * (3 if Hq // Hkv <= 4 else 2) // 3)
+        for n in range(1, G + 1):
+            split = -(-G // n)
+            if B * Hkv * -(-G // split) >= want:
+                return max(split, min(2, G))
+        return min(2, G)
+    for B, Hq, Hkv, G in [(1, 8, 8, 256), (8, 32, 8, 128), (32, 16, 4, 300), (128, 16, 16, 64),
+                          (3, 10, 5, 7), (2, 64, 4, 1000)]:
+        assert L.turbo_decode_auto_split(B, Hq, Hkv, G) == brute(B, Hq, Hkv, G)
     assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10, 0) == 0
     assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3, 0) == 4 * 8 * 4 * 132 * 4
     assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10, 1) == 4 * 8 * 2 * 132 * 4  # + buffer
