@@ -114,22 +114,25 @@ __device__ __forceinline__ int vpos(int j) {
 template <int GP>
 constexpr int kObufCols = GP < 4 ? GP : (GP < 16 ? GP + 4 : GP);
 
+// Rows of the w = q * s^int exchange: the GP query rows (at least 4, the
+// rows one writer pass covers).
+template <int GP>
+constexpr int kWRows = GP < 4 ? 4 : GP;
+
 template <int GP>
 struct DecodeLds {
   float lut[8];
   float sq[16];
+  __attribute__((aligned(16))) unsigned char whi[kWRows<GP>][128];  // hi bytes of w, B-operand order
+  __attribute__((aligned(16))) unsigned char wlo[kWRows<GP>][128];  // lo bytes of w
+  int wbias[kWRows<GP>];                // sum_c q_c z_c of each row
+  signed char qbuf[kWRows<GP>][128];    // the int8 query rows
   int sbuf[GP + 1][64];             // scores, row-major; row GP: stores of unused rows
   unsigned char pbuf[GP + 1][64];   // Q(P~), per page in V-unpack order; row GP: read by
                                     // unused rows (their products are never kept)
   int obuf[128][kObufCols<GP>];     // PV accumulators, channel-major
   float4 rowv[GP];                  // per row: g = s_P s_V / beta, sum Q(P~), renorm, -
 };
-
-// Broadcast of lane I of each 16-lane row to the whole row (DPP row_newbcast).
-template <int I>
-__device__ __forceinline__ unsigned row_bcast(unsigned v) {
-  return (unsigned)__builtin_amdgcn_mov_dpp((int)v, 0x150 + I, 0xf, 0xf, false);
-}
 
 // K side of one group, loaded one group ahead of its step.  The table
 // entries, the slot and the float scales are wave-uniform.  A group that is
@@ -149,8 +152,10 @@ struct GroupK {
   int slot;                 // group slot (clamped)
   float skg, svg;           // float scales s_K, s_V of the group
   unsigned kraw[4][BITS];   // K codes of the lane's 4 A-operand rows (32 channels each)
-  unsigned kmeta;           // dword (lane & 15) of the s^int (8 dwords) and z^int (8 dwords)
-                            // bytes of the lane's 32 K channels; the row holds all 16
+  // s^int and z^int bytes of the channels the lane writes w for (see
+  // decode_groups): int4: 8 channels (2 dwords each), int2: their 16-channel
+  // block (4 dwords each)
+  unsigned ws[BITS == 4 ? 2 : 4], wz[BITS == 4 ? 2 : 4];
 };
 
 // V side of one group, loaded by the group's own step after its QK^T.
@@ -199,7 +204,18 @@ __device__ __forceinline__ void load_k(const DecodeArgs& a, int kh, int head_off
       K.kraw[mb][0] = x.x; K.kraw[mb][1] = x.y;
     }
   }
-  K.kmeta = *reinterpret_cast<const unsigned*>(meta + 32 * g4 + 4 * (n & 7) + 128 * (n >> 3));
+  // the lane writes w for 16-channel block k >> 1, half k & 1 (k = lane & 15)
+  if constexpr (BITS == 4) {
+    const uint2 x = *reinterpret_cast<const uint2*>(meta + 8 * n);
+    const uint2 z = *reinterpret_cast<const uint2*>(meta + 128 + 8 * n);
+    K.ws[0] = x.x; K.ws[1] = x.y;
+    K.wz[0] = z.x; K.wz[1] = z.y;
+  } else {
+    const uint4 x = *reinterpret_cast<const uint4*>(meta + 16 * (n >> 1));
+    const uint4 z = *reinterpret_cast<const uint4*>(meta + 128 + 16 * (n >> 1));
+    K.ws[0] = x.x; K.ws[1] = x.y; K.ws[2] = x.z; K.ws[3] = x.w;
+    K.wz[0] = z.x; K.wz[1] = z.y; K.wz[2] = z.z; K.wz[3] = z.w;
+  }
 }
 
 template <int BITS>
@@ -224,8 +240,7 @@ __device__ __forceinline__ void load_v(const DecodeArgs& a, int kh, int head_off
 
 template <int GP, int BITS, bool kTrace>
 __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>& L, int b, int kh,
-                                              int g0, int g1, int head_off, const int (&q8w)[8],
-                                              float& mrow, float& lpart, float& beta,
+                                              int g0, int g1, int head_off, float& mrow, float& lpart, float& beta,
                                               float (&O)[GP][2], float sq_row, int trow) {
   constexpr int LPR = 64 / GP;  // lanes per compact softmax row
   constexpr int d = BITS == 4 ? 2 : 4;
@@ -235,23 +250,41 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   const int nrow = min(n, GP);      // exchange row of this lane (GP: unused rows)
   const int ocol = min(4 * g4, GP);  // PV exchange column (GP >= 4; GP..GP+3: unused rows)
 
-  // 16-bit (q_ca, q_cb) pairs in the order the K codes unpack to: B-operand
-  // dword j of k-step ks covers channels c0 + {0, d, 2d, 3d}; pair xy = 0 is
-  // (c0, c0+d), xy = 1 is (c0+2d, c0+3d).
-  unsigned qpair[2][4][2];
+  // ---- w = q * s^int, written by all lanes ------------------------------
+  // The QK^T B-operand of lane (n, g4), k-step ks, is 16 bytes: dword j, byte
+  // i holds channel 32*g4 + c0 + d*i with c0 = 16ks + 8(j>>1) + (j&1) (int4)
+  // or 16ks + j (int2), the order the K codes unpack to.  Only GP of the 16
+  // rows n are real, so instead of every lane building its own 32 values,
+  // lane L builds those of unit U = L + 64t: row U >> 4, 8 channels given by
+  // k = U & 15 -- dwords j = 2h, 2h+1 (h = k & 1) of block (g4 = k >> 2,
+  // ks = (k >> 1) & 1) -- and writes their hi/lo bytes to byte 8k of the row.
+  constexpr int kU = GP <= 4 ? 1 : GP / 4;  // writer units per lane
+  const int k = lane & 15;
+  const int cA = BITS == 4 ? 8 * k : 16 * (k >> 1) + 2 * (k & 1);  // channel of dword 2h, byte 0
+  unsigned wq[kU][4];  // 16-bit q pairs (A0,A1) (A2,A3) (B0,B1) (B2,B3)
+  int wqn[kU][2];      // the q bytes of dword A (= 2h) and B (= 2h + 1)
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
+  for (int t = 0; t < kU; ++t) {
+    const int r = (lane >> 4) + 4 * t;
+    int qa[4], qb[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c0 = BITS == 4 ? 16 * ks + 8 * (j >> 1) + (j & 1) : 16 * ks + j;
-#pragma unroll
-      for (int xy = 0; xy < 2; ++xy) {
-        const int ca = c0 + 2 * d * xy, cb = ca + d;
-        const int qa = (int)(int8_t)(q8w[ca >> 2] >> (8 * (ca & 3)));
-        const int qb = (int)(int8_t)(q8w[cb >> 2] >> (8 * (cb & 3)));
-        qpair[ks][j][xy] = ((unsigned)qa & 0xffffu) | ((unsigned)qb << 16);
-      }
+    for (int i = 0; i < 4; ++i) {
+      qa[i] = L.qbuf[r][cA + d * i];
+      qb[i] = L.qbuf[r][cA + 1 + d * i];
     }
+    wq[t][0] = ((unsigned)qa[0] & 0xffffu) | ((unsigned)qa[1] << 16);
+    wq[t][1] = ((unsigned)qa[2] & 0xffffu) | ((unsigned)qa[3] << 16);
+    wq[t][2] = ((unsigned)qb[0] & 0xffffu) | ((unsigned)qb[1] << 16);
+    wq[t][3] = ((unsigned)qb[2] & 0xffffu) | ((unsigned)qb[3] << 16);
+    wqn[t][0] = pack4(qa[0], qa[1], qa[2], qa[3]);
+    wqn[t][1] = pack4(qb[0], qb[1], qb[2], qb[3]);
+  }
+  // int2: byte selectors of channel 2h (+1) in the four dwords of the block
+  const unsigned h2 = 2u * (unsigned)(k & 1);
+  const unsigned selA = h2 | (0x0cu << 8) | ((4u + h2) << 16) | (0x0cu << 24);
+  const unsigned selZ1 = h2 | ((4u + h2) << 8) | 0x0c0c0000u;
+  const unsigned selZ2 = 0x00000c0cu | (h2 << 16) | ((4u + h2) << 24);
+  const int wrow = min(n, kWRows<GP> - 1);  // row this lane reads (unused rows: any)
 
   const int* bt = a.block_table + (long)b * 4 * a.max_groups;
   const int* gt = a.group_table + (long)b * a.max_groups;
@@ -265,51 +298,57 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   load_k<BITS>(a, kh, head_off, bt, gt, g0, g0 < g1, KA);
   auto process = [&](const GroupK<BITS>& cur, int g) {
     if (cur.ok) {
-      // the K scale / zero bytes of the lane's 32 channels, from its row
-      const unsigned km = cur.kmeta;
-      const unsigned ks4[8] = {row_bcast<0>(km), row_bcast<1>(km), row_bcast<2>(km),
-                               row_bcast<3>(km), row_bcast<4>(km), row_bcast<5>(km),
-                               row_bcast<6>(km), row_bcast<7>(km)};
-      const unsigned kz4[8] = {row_bcast<8>(km),  row_bcast<9>(km),  row_bcast<10>(km),
-                               row_bcast<11>(km), row_bcast<12>(km), row_bcast<13>(km),
-                               row_bcast<14>(km), row_bcast<15>(km)};
-      // ---- hi/lo B-operands from w = q * s^int (this lane's 32 channels)
+      // s^int pairs matching wq and z^int bytes matching wqn (see above)
+      unsigned sA01, sA23, sB01, sB23, zA, zB;
+      if constexpr (BITS == 4) {
+        sA01 = __builtin_amdgcn_perm(0u, cur.ws[0], 0x0c020c00u);
+        sA23 = __builtin_amdgcn_perm(0u, cur.ws[1], 0x0c020c00u);
+        sB01 = __builtin_amdgcn_perm(0u, cur.ws[0], 0x0c030c01u);
+        sB23 = __builtin_amdgcn_perm(0u, cur.ws[1], 0x0c030c01u);
+        zA = __builtin_amdgcn_perm(cur.wz[1], cur.wz[0], 0x06040200u);
+        zB = __builtin_amdgcn_perm(cur.wz[1], cur.wz[0], 0x07050301u);
+      } else {
+        sA01 = __builtin_amdgcn_perm(cur.ws[1], cur.ws[0], selA);
+        sA23 = __builtin_amdgcn_perm(cur.ws[3], cur.ws[2], selA);
+        sB01 = __builtin_amdgcn_perm(cur.ws[1], cur.ws[0], selA + 0x00010001u);
+        sB23 = __builtin_amdgcn_perm(cur.ws[3], cur.ws[2], selA + 0x00010001u);
+        zA = __builtin_amdgcn_perm(cur.wz[1], cur.wz[0], selZ1) |
+             __builtin_amdgcn_perm(cur.wz[3], cur.wz[2], selZ2);
+        zB = __builtin_amdgcn_perm(cur.wz[1], cur.wz[0], selZ1 + 0x0101u) |
+             __builtin_amdgcn_perm(cur.wz[3], cur.wz[2], selZ2 + 0x01010000u);
+      }
+#pragma unroll
+      for (int t = 0; t < kU; ++t) {
+        const int r = (lane >> 4) + 4 * t;
+        const unsigned sp[4] = {sA01, sA23, sB01, sB23};
+        unsigned hx[4], lx[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const u16x2 w = __builtin_bit_cast(u16x2, wq[t][u]) * __builtin_bit_cast(u16x2, sp[u]);
+          hx[u] = __builtin_bit_cast(unsigned, __builtin_bit_cast(s16x2, w) >> (short)7);
+          lx[u] = __builtin_bit_cast(unsigned, w) & 0x007F007Fu;
+        }
+        *reinterpret_cast<uint2*>(&L.whi[r][8 * k]) =
+            make_uint2(__builtin_amdgcn_perm(hx[1], hx[0], 0x06040200u),
+                       __builtin_amdgcn_perm(hx[3], hx[2], 0x06040200u));
+        *reinterpret_cast<uint2*>(&L.wlo[r][8 * k]) =
+            make_uint2(__builtin_amdgcn_perm(lx[1], lx[0], 0x06040200u),
+                       __builtin_amdgcn_perm(lx[3], lx[2], 0x06040200u));
+        // zero-point term sum_c q_c z_c of row r: the unit's 8 channels, then
+        // the 16 units of the row (one DPP row; exact: |sum| < 2^24)
+        const int bp = __builtin_amdgcn_sdot4(wqn[t][0], (int)zA,
+                                              __builtin_amdgcn_sdot4(wqn[t][1], (int)zB, 0, false),
+                                              false);
+        L.wbias[r] = (int)row_sum<16>((float)bp);  // every lane of the row: the same value
+      }
+      __syncthreads();
       v4i bhi[2], blo[2];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        int hw[4], lw[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int c0 = BITS == 4 ? 16 * ks + 8 * (j >> 1) + (j & 1) : 16 * ks + j;
-          unsigned hx[2], lx[2];
-#pragma unroll
-          for (int xy = 0; xy < 2; ++xy) {
-            const int ca = c0 + 2 * d * xy, cb = ca + d;
-            // bytes [s_ca, 0, s_cb, 0]: the 16-bit pair (s_ca, s_cb)
-            const unsigned selb = (cb >> 2) == (ca >> 2) ? (unsigned)(cb & 3) : 4u + (cb & 3);
-            const unsigned sel = (unsigned)(ca & 3) | (0x0cu << 8) | (selb << 16) | (0x0cu << 24);
-            const unsigned spair = __builtin_amdgcn_perm(ks4[cb >> 2], ks4[ca >> 2], sel);
-            const u16x2 w =
-                __builtin_bit_cast(u16x2, qpair[ks][j][xy]) * __builtin_bit_cast(u16x2, spair);
-            hx[xy] = __builtin_bit_cast(unsigned, __builtin_bit_cast(s16x2, w) >> (short)7);
-            lx[xy] = __builtin_bit_cast(unsigned, w) & 0x007F007Fu;
-          }
-          hw[j] = (int)__builtin_amdgcn_perm(hx[1], hx[0], 0x06040200u);
-          lw[j] = (int)__builtin_amdgcn_perm(lx[1], lx[0], 0x06040200u);
-        }
-        bhi[ks] = v4i{hw[0], hw[1], hw[2], hw[3]};
-        blo[ks] = v4i{lw[0], lw[1], lw[2], lw[3]};
+        bhi[ks] = *reinterpret_cast<const v4i*>(&L.whi[wrow][32 * g4 + 16 * ks]);
+        blo[ks] = *reinterpret_cast<const v4i*>(&L.wlo[wrow][32 * g4 + 16 * ks]);
       }
-      // zero-point term sum_c q_c z_c over the lane's channels, then over g4
-      int bias = 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) bias = __builtin_amdgcn_sdot4(q8w[i], (int)kz4[i], bias, false);
-      bias = (int)add_xor32((float)bias);  // exact: |bias| < 2^24
-      {
-        const unsigned u = (unsigned)bias;
-        auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-        bias = (int)r[0] + (int)r[1];
-      }
+      const int bias = L.wbias[wrow];
       // ---- S^T = K^{q1} q^T on the MFMA, scores to LDS -----------------
       int4 sv[4];
 #pragma unroll
@@ -551,6 +590,10 @@ __global__ __launch_bounds__(64, (GP <= 4 && !kTrace) ? 3 : 2) void k_attn_decod
       q8w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
     }
     if (g4 == 0) L.sq[n] = sq;
+    if (n < kWRows<GP>) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) *reinterpret_cast<int*>(&L.qbuf[n][32 * g4 + 4 * i]) = q8w[i];
+    }
   }
   // traced row of this wave (-1: none); the wave whose chunk holds group tr_g
   const int trow = kTrace && b == a.tr_b && kh == a.tr_h / G && g0 <= a.tr_g && a.tr_g < g1
@@ -568,9 +611,9 @@ __global__ __launch_bounds__(64, (GP <= 4 && !kTrace) ? 3 : 2) void k_attn_decod
   for (int r = 0; r < GP; ++r) O[r][0] = O[r][1] = 0.0f;
   float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
   if (bits == 4)
-    decode_groups<GP, 4, kTrace>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row, trow);
+    decode_groups<GP, 4, kTrace>(a, L, b, kh, g0, g1, head_off, mrow, lpart, beta, O, sq_row, trow);
   else
-    decode_groups<GP, 2, kTrace>(a, L, b, kh, g0, g1, head_off, q8w, mrow, lpart, beta, O, sq_row, trow);
+    decode_groups<GP, 2, kTrace>(a, L, b, kh, g0, g1, head_off, mrow, lpart, beta, O, sq_row, trow);
 
   // ---- epilogue: per-row (m, l, beta) from the softmax lanes -------------
   const float l = row_sum<LPR>(lpart);
