@@ -445,7 +445,7 @@ int turbo_sas_softmax(const float* x, float* y, int64_t rows, int cols, hipStrea
 /* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
  * a decode batch of B sequences, Hq query and Hkv KV heads and
  * max_groups_per_seq.  The decode kernel keeps three waves per SIMD resident
- * when Hq / Hkv <= 4 and two otherwise (3072 or 2048 on 256 CUs); the
+ * when Hq / Hkv <= 8 and two otherwise (3072 or 2048 on 256 CUs); the
  * fewest chunks n whose B * Hkv * n waves fill at least two thirds of those
  * slots are chosen, with chunk length ceil(max_groups_per_seq / n) (the
  * whole sequence when B * Hkv already fills them), but never fewer than two

@@ -537,7 +537,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
 // kTrace = true only for the test hook that also stores one group's integers
 // (the production instances carry no trace code).
 template <int GP, bool kTrace>
-__global__ __launch_bounds__(64, (GP <= 4 && !kTrace) ? 3 : 2) void k_attn_decode(DecodeArgs a) {
+__global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decode(DecodeArgs a) {
   __shared__ DecodeLds<GP> L;
   constexpr int LPR = 64 / GP;
   const int lane = threadIdx.x;

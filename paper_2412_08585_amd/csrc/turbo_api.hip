@@ -283,7 +283,7 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
 int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq) {
   if (B < 1 || Hq < 1 || Hkv < 1 || max_groups_per_seq < 1) return 1;
   // One wave per (sequence, KV head, chunk).  The decode kernel holds three
-  // waves per SIMD when a KV head has at most 4 query heads and two
+  // waves per SIMD when a KV head has at most 8 query heads and two
   // otherwise: 3072 or 2048 resident waves on the 256 CUs of gfx950.  A
   // wave's run time is set by its per-group latency chain, and the chunks of
   // a sequence are merged afterwards, so take the fewest chunks whose waves
@@ -291,7 +291,7 @@ int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq) {
   // sequences alone do), with the groups spread evenly over them.  A chunk
   // holds at least two groups: below that the fixed cost of a wave (query
   // quantization, state write) and of the merge outweigh the parallelism.
-  const long slots = 1024L * ((Hq / Hkv) <= 4 ? 3 : 2);
+  const long slots = 1024L * ((Hq / Hkv) <= 8 ? 3 : 2);
   const long want = (2 * slots + 2) / 3;
   const long units = (long)B * Hkv, G = max_groups_per_seq;
   const long min_split = G < 2 ? G : 2;

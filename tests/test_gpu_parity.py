@@ -255,6 +255,7 @@ DECODE_CASES = [
     (3, 8, 2, 64 * 6, [4, 2], [384, 200, 63], 0),
     (2, 4, 4, 64 * 4, [2, 4, 4, 2], [256, 256], 1),
     (1, 16, 1, 64 * 8, [4], [512], 3),
+    (2, 16, 2, 64 * 6, [2, 4], [384, 250], 2),   # 8 query heads per KV head
     (2, 2, 1, 64 * 5, [2], [320, 128], 100),
 ]
 

@@ -202,19 +202,20 @@ def test_int2_heads_rule_matches_the_oracle(ta, orc):
 def test_decode_split_and_workspace(ta):
     L = ta.lib()
     # fewest (evenly filled) chunks whose waves fill two thirds of the
-    # resident slots: 3072 (3 waves per SIMD) for up to 4 query heads per KV
+    # resident slots: 3072 (3 waves per SIMD) for up to 8 query heads per KV
     # head, else 2048
     assert L.turbo_decode_auto_split(64, 40, 10, 128) == 32   # 4 chunks: 2560 waves >= 2048
     assert L.turbo_decode_auto_split(256, 32, 8, 512) == 512  # 2048 waves unsplit
     assert L.turbo_decode_auto_split(4096, 32, 8, 4) == 4     # one chunk
     assert L.turbo_decode_auto_split(4, 40, 10, 64) == 2      # at least 2 groups a chunk
     assert L.turbo_decode_auto_split(16, 128, 8, 64) == 6     # G = 16: 11 chunks, 1408 >= 1366
+    assert L.turbo_decode_auto_split(16, 64, 8, 64) == 4      # G = 8: 16 chunks, 2048 >= 2048
     assert L.turbo_decode_auto_split(1, 1, 1, 1) == 1
     assert L.turbo_decode_auto_split(1, 1, 1, 5) == 2
     assert L.turbo_decode_auto_split(0, 1, 1, 1) == 1
 
     def brute(B, Hq, Hkv, G):
-        want = -(-2 * 1024 * (3 if Hq // Hkv <= 4 else 2) // 3)
+        want = -(-2 * 1024 * (3 if Hq // Hkv <= 8 else 2) // 3)
         for n in range(1, G + 1):
             split = -(-G // n)
             if B * Hkv * -(-G // split) >= want:
