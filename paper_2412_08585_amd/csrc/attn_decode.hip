@@ -537,7 +537,16 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
 // kTrace = true only for the test hook that also stores one group's integers
 // (the production instances carry no trace code).
 template <int GP, bool kTrace>
+__device__ void decode_tail_body(const DecodeArgs& a, int bx);  // kv_tail.hip
+
+template <int GP, bool kTrace>
 __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decode(DecodeArgs a) {
+  // the last B * Hkv work-groups (when there is a buffer): its chunk
+  const int nmain = a.B * a.Hkv * a.nsplit;
+  if ((int)blockIdx.x >= nmain) {
+    decode_tail_body<GP, kTrace>(a, (int)blockIdx.x - nmain);
+    return;
+  }
   __shared__ DecodeLds<GP> L;
   constexpr int LPR = 64 / GP;
   const int lane = threadIdx.x;
@@ -719,10 +728,9 @@ __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
   if (a.lse && lane == 0) a.lse[bh] = L;
 }
 
-hipError_t launch_decode_tail(const DecodeArgs& a, hipStream_t stream);  // kv_tail.hip
-
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
-  const int total = a.B * a.Hkv * a.nsplit;
+  // group chunks, then one work-group per (sequence, KV head) for the buffer
+  const int total = a.B * a.Hkv * a.nsplit + (a.tk ? a.B * a.Hkv : 0);
   const int gp = a.G <= 1 ? 1 : a.G <= 2 ? 2 : a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
   if (a.trace) {
     switch (gp) {
@@ -743,10 +751,6 @@ hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.direct) return e;
-  if (a.tk) {
-    e = launch_decode_tail(a, stream);
-    if (e != hipSuccess) return e;
-  }
   hipLaunchKernelGGL(k_decode_combine, dim3(a.B * a.Hq), dim3(64), 0, stream, a);
   return hipGetLastError();
 }

@@ -191,10 +191,13 @@ hipError_t launch_append_kv(const AppendArgs& a, int B, hipStream_t stream) {
 // buffer holds at most 63 tokens, so the integer products run on the VALU
 // (v_dot4): lane t scores token t, then lane L accumulates channels 2L, 2L+1.
 // The result is the buffer's chunk state (m, l, O) in workspace slot
-// ceil(ng / split), merged by k_decode_combine.
+// ceil(ng / split), merged by k_decode_combine.  It runs as the last B * Hkv
+// work-groups of the k_attn_decode launch (work-group index bx among them),
+// so it needs no launch of its own and fills the slots the group chunks
+// leave free at the end.
 
 template <int GP, bool kTrace>
-__global__ __launch_bounds__(64) void k_decode_tail(DecodeArgs a) {
+__device__ void decode_tail_body(const DecodeArgs& a, int bx) {
   __shared__ float lut[8];
   __shared__ int q8s[GP][32];        // int8 query codes, 4 per word
   __shared__ float sqs[GP];
@@ -202,7 +205,7 @@ __global__ __launch_bounds__(64) void k_decode_tail(DecodeArgs a) {
   __shared__ float4 rowv[GP];        // m, l, g = s_P s_V, -
   const int lane = threadIdx.x;
   if (lane < 8) lut[lane] = kLut[lane];
-  const int b = blockIdx.x / a.Hkv, kh = blockIdx.x % a.Hkv;
+  const int b = bx / a.Hkv, kh = bx % a.Hkv;
   const int G = a.G;
   int ng = a.seq_lens[b] / 64;
   ng = min(max(ng, 0), a.max_groups);
@@ -312,27 +315,5 @@ __global__ __launch_bounds__(64) void k_decode_tail(DecodeArgs a) {
   }
 }
 
-hipError_t launch_decode_tail(const DecodeArgs& a, hipStream_t stream) {
-  const int gp = a.G <= 1 ? 1 : a.G <= 2 ? 2 : a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
-  const dim3 grid(a.B * a.Hkv);
-  if (a.trace) {
-    switch (gp) {
-      case 1: hipLaunchKernelGGL((k_decode_tail<1, true>), grid, dim3(64), 0, stream, a); break;
-      case 2: hipLaunchKernelGGL((k_decode_tail<2, true>), grid, dim3(64), 0, stream, a); break;
-      case 4: hipLaunchKernelGGL((k_decode_tail<4, true>), grid, dim3(64), 0, stream, a); break;
-      case 8: hipLaunchKernelGGL((k_decode_tail<8, true>), grid, dim3(64), 0, stream, a); break;
-      default: hipLaunchKernelGGL((k_decode_tail<16, true>), grid, dim3(64), 0, stream, a); break;
-    }
-  } else {
-    switch (gp) {
-      case 1: hipLaunchKernelGGL((k_decode_tail<1, false>), grid, dim3(64), 0, stream, a); break;
-      case 2: hipLaunchKernelGGL((k_decode_tail<2, false>), grid, dim3(64), 0, stream, a); break;
-      case 4: hipLaunchKernelGGL((k_decode_tail<4, false>), grid, dim3(64), 0, stream, a); break;
-      case 8: hipLaunchKernelGGL((k_decode_tail<8, false>), grid, dim3(64), 0, stream, a); break;
-      default: hipLaunchKernelGGL((k_decode_tail<16, false>), grid, dim3(64), 0, stream, a); break;
-    }
-  }
-  return hipGetLastError();
-}
 
 }  // namespace turbo

@@ -343,7 +343,7 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache,
   const int split = kv_split_groups ? kv_split_groups
                                     : turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq);
   const long nsplit = (max_groups_per_seq + split - 1) / split;
-  if ((long)B * Hkv * nsplit > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
+  if ((long)B * Hkv * (nsplit + (tail ? 1 : 0)) > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
   const size_t need =
       turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups_per_seq, split, tail != nullptr);
   if (need > 0 && (!workspace || workspace_bytes < need)) return TURBO_ERR_WORKSPACE_TOO_SMALL;
