@@ -108,11 +108,19 @@ __device__ __forceinline__ int vpos(int j) {
   return 4 * (j & 3) + (j >> 2);
 }
 
-// Columns of the PV exchange: GP rows plus, for 4 <= GP < 16, four columns
-// that take the stores of the lanes holding unused rows (so no lane needs
-// its own branch around a store).
+// LDS row strides (in ints) chosen for the bank pattern of the exchanges
+// (64 banks of 4 bytes):
+//  * scores: one row per MFMA column n (16), 68 ints apart, so the 16 lanes
+//    of a column block store to 16 different banks;
+//  * PV accumulators: GP + 2 ints per channel (an odd number of 8-byte
+//    pairs), so lanes L = 0..15 reading channel rows 2L (+1) hit distinct
+//    banks.  Lanes whose MFMA rows are unused (4*g4 >= GP) store to a
+//    separate area instead, at one address for every channel block.
+constexpr int kSbufStride = 68;
 template <int GP>
-constexpr int kObufCols = GP < 4 ? GP : (GP < 16 ? GP + 4 : GP);
+constexpr int kObufStride = GP < 4 ? GP : GP + 2;
+template <int GP>
+constexpr int kOdumRows = GP < 4 ? 1 : (GP < 16 ? 64 - 4 * GP : 1);
 
 // Rows of the w = q * s^int exchange: the GP query rows (at least 4, the
 // rows one writer pass covers).
@@ -127,10 +135,11 @@ struct DecodeLds {
   __attribute__((aligned(16))) unsigned char wlo[kWRows<GP>][128];  // lo bytes of w
   int wbias[kWRows<GP>];                // sum_c q_c z_c of each row
   signed char qbuf[kWRows<GP>][128];    // the int8 query rows
-  int sbuf[GP + 1][64];             // scores, row-major; row GP: stores of unused rows
+  __attribute__((aligned(16))) int sbuf[16][kSbufStride];  // scores, row n; rows >= GP unused
   unsigned char pbuf[GP + 1][64];   // Q(P~), per page in V-unpack order; row GP: read by
                                     // unused rows (their products are never kept)
-  int obuf[128][kObufCols<GP>];     // PV accumulators, channel-major
+  __attribute__((aligned(16))) int obuf[128][kObufStride<GP>];  // PV accumulators, channel-major
+  __attribute__((aligned(16))) int odum[kOdumRows<GP>][4];     // stores of unused MFMA rows
   float4 rowv[GP];                  // per row: g = s_P s_V / beta, sum Q(P~), renorm, -
 };
 
@@ -172,13 +181,18 @@ __device__ __forceinline__ void load_k(const DecodeArgs& a, int kh, int head_off
   const int n = lane & 15, g4 = lane >> 4, m = lane & 15;
   g = live ? g : 0;
   bool ok = live;
+  // the tables are read-only here: read them through the constant address
+  // space, which keeps these wave-uniform reads on the scalar unit
+  typedef const __attribute__((address_space(4))) int cint;
+  const cint* btc = (const cint*)bt;
+  const cint* gtc = (const cint*)gt;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int p = bt[4 * g + i];
+    const int p = btc[4 * g + i];
     ok = ok && p >= 0 && p < a.npages32;
     K.pg[i] = p;
   }
-  const int slot = gt[g];
+  const int slot = gtc[g];
   ok = ok && slot >= 0 && slot < a.nslots32;
   K.ok = ok;
 #pragma unroll
@@ -189,7 +203,8 @@ __device__ __forceinline__ void load_k(const DecodeArgs& a, int kh, int head_off
   const int vp = bt[4 * g + g4];
   K.vpg = ok ? vp : 0;
   const int8_t* meta = a.gmeta + ((long)K.slot * a.Hkv + kh) * 512;
-  const float* gs = a.gscale + ((long)K.slot * a.Hkv + kh) * 2;
+  typedef const __attribute__((address_space(4))) float cfloat;
+  const cfloat* gs = (const cfloat*)(a.gscale + ((long)K.slot * a.Hkv + kh) * 2);
   K.skg = gs[0];
   K.svg = gs[1];
   const int koff = head_off + m * 16 * BITS + 4 * BITS * g4;
@@ -247,8 +262,13 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   const int lane = threadIdx.x;
   const int n = lane & 15, g4 = lane >> 4;
   const int rr = lane / LPR, cc = lane % LPR;
-  const int nrow = min(n, GP);      // exchange row of this lane (GP: unused rows)
-  const int ocol = min(4 * g4, GP);  // PV exchange column (GP >= 4; GP..GP+3: unused rows)
+  const int nrow = min(n, GP);  // P~ row this lane reads (GP: unused rows)
+  // PV store target of this lane (GP >= 4): its 4 MFMA rows of channel
+  // 16*cb + n, or (rows 4*g4.. unused) one spare slot for every cb
+  const bool orows = 4 * g4 < GP;
+  const int odi = min(max((g4 * 16 + n) - 4 * GP, 0), kOdumRows<GP> - 1);
+  int* const obase = orows ? &L.obuf[n][4 * g4] : &L.odum[odi][0];
+  const int ostep = orows ? 16 * kObufStride<GP> : 0;
 
   // ---- w = q * s^int, written by all lanes ------------------------------
   // The QK^T B-operand of lane (n, g4), k-step ks, is 16 bytes: dword j, byte
@@ -386,7 +406,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
       // lane (n, g4), register r of m-block mb: row n, token 16*mb + 4*g4 + r
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
-        *reinterpret_cast<int4*>(&L.sbuf[nrow][16 * mb + 4 * g4]) = sv[mb];
+        *reinterpret_cast<int4*>(&L.sbuf[n][16 * mb + 4 * g4]) = sv[mb];
       const bool trace_g = kTrace && trow >= 0 && g == a.tr_g;  // wave-uniform
       if (trace_g && n == trow) {
 #pragma unroll
@@ -475,8 +495,9 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         acc = mfma16x16x64(pop, vop, acc);
         // lane (n, g4), register r <-> row 4*g4 + r, channel 16*cb + n
         if (GP >= 4) {
-          *reinterpret_cast<int4*>(&L.obuf[16 * cb + n][ocol]) =
-              make_int4(acc[0], acc[1], acc[2], acc[3]);
+          int* dst = obase + cb * ostep;
+          *reinterpret_cast<int2*>(dst) = make_int2(acc[0], acc[1]);
+          *reinterpret_cast<int2*>(dst + 2) = make_int2(acc[2], acc[3]);
         } else if (g4 == 0) {
 #pragma unroll
           for (int r = 0; r < GP; ++r) L.obuf[16 * cb + n][r] = acc[r];
@@ -490,9 +511,9 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         for (int c2 = 0; c2 < 2; ++c2) {
           if (GP >= 4) {
 #pragma unroll
-            for (int r = 0; r < GP; r += 4) {
-              const int4 t = *reinterpret_cast<const int4*>(&L.obuf[2 * lane + c2][r]);
-              acc[c2][r] = t.x; acc[c2][r + 1] = t.y; acc[c2][r + 2] = t.z; acc[c2][r + 3] = t.w;
+            for (int r = 0; r < GP; r += 2) {
+              const int2 t = *reinterpret_cast<const int2*>(&L.obuf[2 * lane + c2][r]);
+              acc[c2][r] = t.x; acc[c2][r + 1] = t.y;
             }
           } else {
 #pragma unroll
