@@ -40,7 +40,11 @@ def measured_traffic(kernel: str, workload: str):
     import hashlib
     srcs = {"k_attn_prefill": ["paper_2412_08585_amd/csrc/attn_prefill.hip",
                                "paper_2412_08585_amd/csrc/turbo_common.h",
-                               "paper_2412_08585_amd/build.py"]}.get(kernel)
+                               "paper_2412_08585_amd/build.py"],
+            "k_attn_decode": ["paper_2412_08585_amd/csrc/attn_decode.hip",
+                              "paper_2412_08585_amd/csrc/kv_tail.hip",
+                              "paper_2412_08585_amd/csrc/turbo_common.h",
+                              "paper_2412_08585_amd/build.py"]}.get(kernel)
     path = os.path.join(ROOT, "profiles", "traffic.txt")
     if not srcs or not os.path.exists(path):
         return None
@@ -75,6 +79,22 @@ def ramp_clocks(fn, seconds: float = 0.2):
         for _ in range(4):
             fn()
         torch.cuda.synchronize()
+
+
+CPU_SAMPLE_SECONDS = 10.0
+
+
+def cpu_sample(run_chunk, n_total: int, chunk: int, seconds: float = CPU_SAMPLE_SECONDS):
+    """Runs the oracle over consecutive chunks of the workload, run_chunk(lo,
+    hi), until `seconds` of oracle time have passed or the whole workload is
+    done; returns (items done, oracle seconds).  Copies to the host are not
+    timed."""
+    done, dt = 0, 0.0
+    while done < n_total and dt < seconds:
+        hi = min(n_total, done + chunk)
+        dt += run_chunk(done, hi)
+        done = hi
+    return done, dt
 
 
 def parse():
@@ -268,22 +288,30 @@ def main():
     if not args.no_cpu_baseline:
         import oracle
         threads = oracle.num_threads()
-        n_units = max(1, min(B * Hkv, math.ceil(threads * 5 / G)))
         rng = np.random.default_rng(0)
-        units = [divmod(int(u), Hkv) for u in rng.choice(B * Hkv, n_units, replace=False)]
-        qs = torch.stack([q[b, h * G:(h + 1) * G] for b, h in units])[:, :, :, :].cpu()
-        ks = torch.stack([k[b, h] for b, h in units])[:, None].cpu()
-        vs = torch.stack([v[b, h] for b, h in units])[:, None].cpu()
-        # one sampled unit = one sequence with one KV head and its G query heads
-        qs = qs.reshape(n_units, G, N, d)
-        qds = torch.stack([qd[b, h * G:(h + 1) * G] for b, h in units]).cpu()
-        t0 = time.perf_counter()
-        ref = oracle.quantize_kv(ks.reshape(n_units, 1, N, d), vs.reshape(n_units, 1, N, d),
-                                 [4])
-        ro, _ = oracle.attn_prefill(qs, ks.reshape(n_units, 1, N, d), vs.reshape(n_units, 1, N, d),
-                                    w.sm_scale, True)
-        oracle.attn_decode(qds, ref, [N] * n_units, w.sm_scale, split=split)
-        dt = time.perf_counter() - t0
+        order = [divmod(int(u), Hkv) for u in rng.permutation(B * Hkv)]
+        ros = []
+
+        def run_units(lo, hi):
+            # one unit = one sequence with one KV head and its G query heads
+            us, n = order[lo:hi], hi - lo
+            qs = torch.stack([q[b, h * G:(h + 1) * G] for b, h in us]).cpu()
+            ks = torch.stack([k[b, h] for b, h in us])[:, None].cpu()
+            vs = torch.stack([v[b, h] for b, h in us])[:, None].cpu()
+            qds = torch.stack([qd[b, h * G:(h + 1) * G] for b, h in us]).cpu()
+            t0 = time.perf_counter()
+            ref = oracle.quantize_kv(ks, vs, [4])
+            ro, _ = oracle.attn_prefill(qs, ks, vs, w.sm_scale, True)
+            oracle.attn_decode(qds, ref, [N] * n, w.sm_scale, split=split)
+            t = time.perf_counter() - t0
+            ros.append(ro)
+            return t
+
+        n_units, dt = cpu_sample(run_units, B * Hkv, max(1, math.ceil(threads / G)))
+        units, ro = order[:n_units], np.concatenate(ros)
+        qs = torch.stack([q[b, h * G:(h + 1) * G] for b, h in units[:1]]).cpu()
+        ks = k[units[0][0], units[0][1]][None, None].cpu()
+        vs = v[units[0][0], units[0][1]][None, None].cpu()
         sample_ops = (prefill_ops + decode_ops) * n_units / (B * Hkv)
         result["cpu_baseline"] = {
             "value": round(sample_ops / dt / 1e12, 6), "unit": "TOPS",
@@ -293,7 +321,6 @@ def main():
         # parity and error of the sampled units (reported, not gated here)
         got = torch.stack([o[b, h * G:(h + 1) * G] for b, h in units]).float().cpu().numpy()
         rowmax = np.abs(ro).max(axis=-1, keepdims=True)
-        b0, h0 = units[0]
         ex, _ = oracle.attn_exact(qs[:1], ks[:1].reshape(1, 1, N, d), vs[:1].reshape(1, 1, N, d),
                                   float(np.float32(w.sm_scale)), True)
         rel = lambda a, r: float(np.linalg.norm(a - r) / np.linalg.norm(r))
@@ -421,7 +448,8 @@ def bench_decode(args, w):
         "attention_TOPS": round(ops / (ms * 1e-3) / 1e12, 3),
         "roofline": {"kernel": "k_attn_decode+k_decode_combine", "bound": "hbm",
                      "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                     "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": measured_traffic("k_attn_decode", w.name),
                      "per_launch_bytes": kv_bytes + qo_bytes},
         "buffer_step": {
             "note": "Sec. 3.3 decoding step: turbo_append_kv of the new token, then "
@@ -429,6 +457,38 @@ def bench_decode(args, w):
             "append_ms": round(ms_app, 4), "step_ms": round(ms_buf, 4),
             "GB/s": round((kv_bytes + qo_bytes) / (ms_buf * 1e-3) / 1e9, 1)},
     }
+
+    # ---- CPU oracle: the oracle's caches of the first sequences (built
+    # untimed, like the GPU cache), attended until the sample time is spent ----
+    if not args.no_cpu_baseline:
+        import oracle
+        qc = q.cpu()
+        run()                       # o of the plain decode (the buffer step overwrote it)
+        got = o.float().cpu().numpy()
+        refs, t0 = [], time.perf_counter()
+        while len(refs) < B and time.perf_counter() - t0 < 15.0:
+            b = len(refs)
+            kv = [W.unit_kv(w, b, h, device=dev) for h in range(Hkv)]
+            ref = oracle.quantize_kv(torch.stack([a for a, _ in kv])[None].cpu(),
+                                     torch.stack([c for _, c in kv])[None].cpu(), bits)
+            del ref["k8"], ref["v8"], kv
+            refs.append(ref)
+        passes, dt, err = 0, 0.0, 0.0
+        while passes == 0 or dt < CPU_SAMPLE_SECONDS:
+            for b, ref in enumerate(refs):
+                t1 = time.perf_counter()
+                ro, _ = oracle.attn_decode(qc[b:b + 1], ref, [N], w.sm_scale, split=split)
+                dt += time.perf_counter() - t1
+                rowmax = np.abs(ro[0]).max(axis=-1, keepdims=True)
+                err = max(err, float(np.max(np.abs(got[b] - ro[0]) / rowmax)))
+            passes += 1
+        nseq = len(refs) * passes
+        result["cpu_baseline"] = {
+            "value": round((kv_bytes + qo_bytes) * nseq / B / dt / 1e9, 3), "unit": "GB/s",
+            "cores": min(oracle.num_threads(), Hq), "kind": "oracle",
+            "sample": f"{len(refs)} of {B} sequences (oracle cache built untimed), each attended "
+                      f"{passes} times, {dt:.1f} s"}
+        result["parity"] = {"max_err_vs_oracle_rel_rowmax": err, "sample_sequences": len(refs)}
     print(json.dumps(result), flush=True)
 
 
@@ -472,11 +532,14 @@ def bench_softmax(args, w):
     }
     if not args.no_cpu_baseline:
         import oracle
-        n = 4096
-        xs = x[:n].cpu().numpy()
-        t0 = time.perf_counter()
-        oracle.sas_softmax_rows(xs)
-        dt = time.perf_counter() - t0
+
+        def run_rows(lo, hi):
+            xs = x[lo:hi].cpu().numpy()
+            t0 = time.perf_counter()
+            oracle.sas_softmax_rows(xs)
+            return time.perf_counter() - t0
+
+        n, dt = cpu_sample(run_rows, rows, 4096)
         result["cpu_baseline"] = {"value": round(n * cols * 8 / dt / 1e9, 3), "unit": "GB/s",
                                   "cores": 1, "kind": "oracle",
                                   "sample": f"{n} of {rows} rows, {dt:.1f} s"}
@@ -543,12 +606,16 @@ def bench_projection(args, w):
     }
     if not args.no_cpu_baseline:
         import oracle
-        n = 512
-        xs = x[0, :n].float().cpu().numpy()[None]
         ws = wt.float().cpu().numpy()
-        t0 = time.perf_counter()
-        oracle.qkv_project(xs, ws, Hq, Hkv, bits)
-        dt = time.perf_counter() - t0
+        xt = x.reshape(B * N, D)
+
+        def run_tokens(lo, hi):
+            xs = xt[lo:hi].float().cpu().numpy()[None]
+            t0 = time.perf_counter()
+            oracle.qkv_project(xs, ws, Hq, Hkv, bits)
+            return time.perf_counter() - t0
+
+        n, dt = cpu_sample(run_tokens, B * N, 1024)
         result["cpu_baseline"] = {"value": round(2.0 * n * D * F / dt / 1e12, 5), "unit": "TFLOP/s",
                                   "cores": oracle.num_threads(), "kind": "oracle",
                                   "sample": f"{n} of {B * N} tokens, {dt:.1f} s"}
