@@ -394,6 +394,330 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
   }
 }
 
+// ---------------------------------------------------------------------------
+// B_r = B_c = 64 (the paper's setting): four waves of 16 query rows.
+//
+// A 16-row wave holds half the accumulators of a 32-row one, which brings the
+// kernel under 128 VGPRs: a SIMD then keeps four waves resident instead of
+// two.  The softmax is bound by VALU issue, and one wave alone issues a VALU
+// instruction only every few clocks, so more resident waves raise the rate.
+// The work-group loads each K and V tile once into LDS (double-buffered) and
+// the waves read their MFMA operands from there.
+//
+// v_mfma_i32_16x16x64_i8: output lane (n + 16g), register r = row 4g + r,
+// column n.  S^T = K Q^T per 16-key block mb: A-operand row m holds key
+// 16(m >> 2) + 4mb + (m & 3), so lane (n, g), register r of block mb is the
+// score of query n and key 16g + 4mb + r.  The lane's 16 keys 16g .. 16g + 15
+// are, byte for byte, its B-operand of O^T = V^T P^T with contraction slot
+// (g, byte i) = key 16g + i, and the matching V^T bytes are 16 contiguous
+// bytes of a channel row of the channel-major V block.  A query's 64 scores
+// lie in lanes n, n + 16, n + 32, n + 48 (two exchanges per row reduction).
+//
+// LDS tiles without padding: 16-byte chunk c of K row t is stored at chunk
+// c ^ kswz(t), chunk c of V row ch at c ^ vswz(ch), so that the lanes of
+// each ds_read_b128 / ds_write_b128 pass hit distinct 4-bank groups.
+//
+// Per tile j (one barrier): QK_j from K buffer j&1; K_{j+1} (loaded a tile
+// earlier) into K buffer (j+1)&1, whose last readers (QK_{j-1}) all finished
+// before the previous barrier; softmax; tile maximum exchange + barrier; PV_j
+// from V buffer j&1; V_{j+1} into V buffer (j+1)&1, whose last readers
+// (PV_{j-1}) all finished before this tile's barrier.
+constexpr int kP16Waves = 4;
+
+// (conflict-free with 32 banks served 8 lanes per pass and with 64 banks
+// served 16 lanes per pass; they depend only on key bits 0, 1, 4, 5 and
+// channel bits 1 .. 3, so they are the same for every block mb and cb)
+__device__ __forceinline__ int kswz(int t) {
+  return ((t >> 1) & 1) | (((t >> 4) & 1) << 1) | ((((t >> 5) ^ t) & 1) << 2);
+}
+__device__ __forceinline__ int vswz(int ch) {
+  return (((ch >> 1) ^ (ch >> 3)) & 1) | (((ch >> 2) & 1) << 1);
+}
+
+struct Prefill16Lds {
+  __attribute__((aligned(16))) int8_t k[2][64 * 128];   // [key][128 channels], swizzled
+  __attribute__((aligned(16))) int8_t v[2][128 * 64];   // [channel][64 keys], swizzled
+  float lut[8];
+  float xmax[2][kP16Waves];
+  float xq[kP16Waves];
+};
+
+template <bool kTrace, bool kQ8>
+__global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArgs a) {
+  __shared__ Prefill16Lds L;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int n = lane & 15, g = lane >> 4;
+  if (tid < 8) L.lut[tid] = kLut[tid];
+
+  const int BH = a.B * a.Hq;
+  const int Lx = prefill_order(blockIdx.x, BH * a.nbq, a.Hq / a.Hkv);
+  const int i = a.nbq - 1 - Lx / BH;  // longest causal rows first
+  const int b = (Lx % BH) / a.Hq, h = Lx % a.Hq;
+  const int G = a.Hq / a.Hkv, kh = h / G;
+  const int N = a.N;
+  const int row0 = 64 * i + 16 * w;  // first query row of this wave
+  const int qrow = row0 + n;
+  const long kvu = (long)b * a.Hkv + kh;
+  const float* skp = a.sk + kvu * a.nbc;
+  const float* svp = a.sv + kvu * a.nbc;
+  const int jend = a.causal ? i : a.nbc - 1;
+
+  // ---- tile copies: thread tid moves 16-byte chunks tid and tid + 256 -----
+  const uint4* kg = reinterpret_cast<const uint4*>(a.k8 + kvu * a.nb * 8192) + tid;
+  const uint4* vg = reinterpret_cast<const uint4*>(a.v8 + kvu * a.nb * 8192) + tid;
+  const int c0 = tid, c1 = tid + 256;
+  const int kdst0 = (c0 >> 3) * 128 + 16 * ((c0 & 7) ^ kswz(c0 >> 3));
+  const int kdst1 = (c1 >> 3) * 128 + 16 * ((c1 & 7) ^ kswz(c1 >> 3));
+  const int vdst0 = (c0 >> 2) * 64 + 16 * ((c0 & 3) ^ vswz(c0 >> 2));
+  const int vdst1 = (c1 >> 2) * 64 + 16 * ((c1 & 3) ^ vswz(c1 >> 2));
+  // K_{j+1} and V_{j+1} in flight (registers)
+  uint4 kp0 = kg[0], kp1 = kg[256], vp0 = vg[0], vp1 = vg[256];
+  *reinterpret_cast<uint4*>(&L.k[0][kdst0]) = kp0;
+  *reinterpret_cast<uint4*>(&L.k[0][kdst1]) = kp1;
+  *reinterpret_cast<uint4*>(&L.v[0][vdst0]) = vp0;
+  *reinterpret_cast<uint4*>(&L.v[0][vdst1]) = vp1;
+  {
+    const long o1 = (long)min(1, jend) * 512;
+    kp0 = kg[o1];
+    kp1 = kg[o1 + 256];
+    vp0 = vg[o1];
+    vp1 = vg[o1 + 256];
+  }
+
+  // ---- Q_i -> int8 (eq. step1bpq; scale over the 64-row block) ----------
+  // lane (n, g), k-step ks: channels 64ks + 16g .. +15 of query qrow
+  v4i qop[2];
+  float sq;
+  if (kQ8) {
+    const int8_t* src = a.q8 + (((long)b * a.Hq + h) * a.nb * 64 + qrow) * 128 + 16 * g;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) qop[ks] = *reinterpret_cast<const v4i*>(src + 64 * ks);
+    sq = a.sq[((long)b * a.Hq + h) * a.nb + i];
+    __syncthreads();
+  } else {
+    uint4 raw[2][2];
+    float amax = 0.0f;
+    const uint4* src = a.q + (((long)b * a.Hq + h) * N + qrow) * 16 + 2 * g;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        raw[ks][u] = qrow < N ? src[8 * ks + u] : make_uint4(0, 0, 0, 0);
+        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[ks][u]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
+      }
+    amax = wave_max_fast(amax);
+    if (lane == 0) L.xq[w] = amax;
+    __syncthreads();
+    amax = fmaxf(fmaxf(L.xq[0], L.xq[1]), fmaxf(L.xq[2], L.xq[3]));
+    float inv = 0.0f;
+    sq = 0.0f;
+    if (amax > 0.0f) {
+      sq = amax / kQmax;
+      inv = kQmax / amax;
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      int wd[4];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[ks][u]);
+        int qv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
+        wd[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
+        wd[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
+      }
+      qop[ks] = v4i{wd[0], wd[1], wd[2], wd[3]};
+    }
+  }
+  // wave-uniform; a key block the loop never reaches traces nothing
+  const bool traced = kTrace && Lx == a.tr_L && a.tr_j <= jend;
+  if constexpr (kTrace) {
+    if (traced) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_Q8 + (16 * w + n) * 128 + 64 * ks +
+                                16 * g) = qop[ks];
+      if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = sq;
+    }
+  }
+
+  // operand addresses in the tiles: K row 16(n>>2) + (n&3) (+ 4mb), chunk
+  // 4ks + g; V row n (+ 16cb), chunk g
+  const int kf = kswz(16 * (n >> 2) + (n & 3));  // the same for every block mb
+  const int kbase0 = (16 * (n >> 2) + (n & 3)) * 128 + 16 * (g ^ kf);
+  const int kbase1 = (16 * (n >> 2) + (n & 3)) * 128 + 16 * ((4 + g) ^ kf);
+  const int vbase = n * 64 + 16 * (g ^ vswz(n));
+
+  float O[8][4];
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) O[cb][r] = 0.0f;
+  float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
+  float skj = skp[0], svj = svp[0];
+  // sm_scale 2^26: (sq s_K) * (sm_scale 2^26) = ((sq s_K) * sm_scale) 2^26
+  // exactly (a power-of-two factor; c cannot be subnormal for fp16 inputs)
+  const float sm26 = a.sm_scale * 0x1p26f;
+
+  for (int j = 0; j <= jend; ++j) {
+    const int buf = j & 1;
+    const float skn = skp[min(j + 1, jend)], svn = svp[min(j + 1, jend)];
+    // ---- S^T_j = K_j Q^T on the MFMA -----------------------------------
+    v4i S[4];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const v4i k0 = *reinterpret_cast<const v4i*>(&L.k[buf][kbase0 + 512 * mb]);
+      const v4i k1 = *reinterpret_cast<const v4i*>(&L.k[buf][kbase1 + 512 * mb]);
+      v4i acc = {kAccSeed, kAccSeed, kAccSeed, kAccSeed};
+      acc = mfma16x16x64(k0, qop[0], acc);
+      acc = mfma16x16x64(k1, qop[1], acc);
+      S[mb] = acc;
+    }
+    *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst0]) = kp0;
+    *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst1]) = kp1;
+    const long o2 = (long)min(j + 2, jend) * 512;
+    kp0 = kg[o2];
+    kp1 = kg[o2 + 256];
+    const bool trace_tile = traced && j == a.tr_j;
+    if constexpr (kTrace) {
+      if (trace_tile) {
+        int* ts = reinterpret_cast<int*>(a.trace + TURBO_TRACE_S) + (16 * w + n) * 64 + 16 * g;
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) ts[4 * mb + r] = S[mb][r] - kAccSeed;
+      }
+    }
+    // ---- scores, online max, SAS (Algorithm 1, statistics step) --------
+    // (S read as float - seed) * (c 2^26) = float(S) * c, rounded once
+    const float c26 = (sq * skj) * sm26;
+    float P[4][4];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) P[mb][r] = acc_unseed(S[mb][r]) * c26;
+    // masking on the diagonal tile and where keys or rows reach past N
+    if ((a.causal && 64 * j + 63 > row0) || (64 * j + 64 > N) || (row0 + 16 > N)) {
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = 64 * j + 16 * g + 4 * mb + r;
+          const bool vis = key < N && qrow < N && (!a.causal || key <= qrow);
+          P[mb][r] = vis ? P[mb][r] : -INFINITY;
+        }
+    }
+    float smax = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) smax = fmaxf(smax, P[mb][r]);
+    smax = max_xor32(max_xor16_nn(smax));
+    const float mold = mrow;
+    const float mnew = fmaxf(mold, smax);
+    float rs, pmax;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = sas_y(mnew - P[mb][r], L.lut);
+        P[mb][r] = p;
+        rs = (mb | r) ? rs + p : p;
+        pmax = (mb | r) ? fmaxf(pmax, p) : p;
+      }
+    const float alpha = sas_y(mnew - mold, L.lut);  // 0 when mold = -inf
+    lpart = alpha * lpart + rs;
+    mrow = mnew;
+    // ---- tile maximum of P~ over the four waves ------------------------
+    pmax = wave_max_pos(pmax);  // P~ >= 0
+    if (lane == 0) L.xmax[buf][w] = pmax;
+    __syncthreads();
+    pmax = __int_as_float(max(max(__float_as_int(L.xmax[buf][0]), __float_as_int(L.xmax[buf][1])),
+                              max(__float_as_int(L.xmax[buf][2]), __float_as_int(L.xmax[buf][3]))));
+    // ---- rescale factor: O = beta * Ost --------------------------------
+    float nbeta = beta * alpha;
+    if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) O[cb][r] *= nbeta;
+      nbeta = 1.0f;
+    }
+    beta = nbeta;
+    // ---- Q(P~) with scale pmax/119 over the 64 x 64 tile ----------------
+    const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
+    // s_P = pmax / 119 only scales O (no code depends on it): the product
+    // with the rounded reciprocal is within one ulp of the quotient; the
+    // factor 2^26 undoes the accumulator seed
+    const float g26 = ((pmax * (0x1p26f / kQmax)) * svj) * __builtin_amdgcn_rcpf(beta);
+    v4i pop;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+      pop[mb] = pack_lo4(rne_bits(P[mb][0], inv), rne_bits(P[mb][1], inv),
+                         rne_bits(P[mb][2], inv), rne_bits(P[mb][3], inv));
+    if constexpr (kTrace) {
+      if (trace_tile) {
+        *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_P + (16 * w + n) * 64 + 16 * g) = pop;
+        if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
+      }
+    }
+    // ---- PV_j on the MFMA; Ost += (s_P s_V / beta) V_j^T Q(P~)^T --------
+    v4i acc[8];
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      const v4i vop = *reinterpret_cast<const v4i*>(&L.v[buf][vbase + 1024 * cb]);
+      const v4i z = {kAccSeed, kAccSeed, kAccSeed, kAccSeed};
+      acc[cb] = mfma16x16x64(vop, pop, z);
+    }
+    if constexpr (kTrace) {
+      if (trace_tile) {
+        // register r of channel block cb <-> channel 16cb + 4g + r
+        int* tp = reinterpret_cast<int*>(a.trace + TURBO_TRACE_PV) + (16 * w + n) * 128 + 4 * g;
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tp[16 * cb + r] = acc[cb][r] - kAccSeed;
+      }
+    }
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) O[cb][r] = __builtin_fmaf(g26, acc_unseed(acc[cb][r]), O[cb][r]);
+    *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst0]) = vp0;
+    *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst1]) = vp1;
+    vp0 = vg[o2];
+    vp1 = vg[o2 + 256];
+    skj = skn;
+    svj = svn;
+  }
+
+  // ---- epilogue: O / l (fp16), L = m + ln l ----------------------------
+  float l = lpart;
+  {
+    const unsigned u = __float_as_uint(l);
+    auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    l = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  }
+  l = add_xor32(l);
+  if (qrow < N) {
+    const float f = beta / l;
+    uint2* orow = a.o + (((long)b * a.Hq + h) * N + qrow) * 32;
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      f16x4_t hv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][e] * f);
+      orow[(16 * cb + 4 * g) / 4] = __builtin_bit_cast(uint2, hv);
+    }
+    if (a.lse && g == 0) a.lse[((long)b * a.Hq + h) * N + qrow] = mrow + logf(l);
+  }
+}
+
 template <int kWaves>
 static void launch_bc(const PrefillArgs& a, int total, hipStream_t stream) {
   const dim3 grid(total), block(64 * kWaves);
@@ -407,10 +731,13 @@ static void launch_bc(const PrefillArgs& a, int total, hipStream_t stream) {
 
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hq * a.nbq;
+  const dim3 b16(64 * kP16Waves);
   if (a.trace)  // test hook: B_r = B_c = 64 only
-    hipLaunchKernelGGL((k_attn_prefill<true, false, 2, 64>), dim3(total), dim3(128), 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill16<true, false>), dim3(total), b16, 0, stream, a);
   else if (a.q8)  // B_r = B_c = 64 only
-    hipLaunchKernelGGL((k_attn_prefill<false, true, 2, 64>), dim3(total), dim3(128), 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill16<false, true>), dim3(total), b16, 0, stream, a);
+  else if (a.waves == 2 && a.bc == 64)
+    hipLaunchKernelGGL((k_attn_prefill16<false, false>), dim3(total), b16, 0, stream, a);
   else if (a.waves == 1)
     launch_bc<1>(a, total, stream);
   else if (a.waves == 4)

@@ -24,6 +24,19 @@ constexpr float kQmax = 119.0f;
 constexpr float kMagic = 12582912.0f;
 constexpr int kMagicBits = 0x4B400000;
 
+// Accumulator seed of the i8 MFMAs: the bits of binary32 1/(2 pi) =
+// 0x1.45f306p-3, one of the instruction set's inline constants.  An int32
+// result seed + s with -2292099 <= s <= 6096508 stays in the binade of the
+// seed (whose mantissa field is 2292099), so read as a float it is
+// 0x1.45f306p-3 + s * 2^-26, and subtracting the seed gives s * 2^-26
+// exactly: a full-rate subtraction replaces the half-rate int -> float
+// conversion.  Every product sum here is within |s| <= 128 * 128 * 128 = 2^21.
+constexpr int kAccSeed = 0x3E22F983;
+constexpr float kAccSeedF = 0x1.45f306p-3f;
+
+// s * 2^-26 of a seeded accumulator entry (exact).
+__device__ __forceinline__ float acc_unseed(int r) { return __int_as_float(r) - kAccSeedF; }
+
 // SAS (Sec. 4): e^{-y} ~ LUT[floor y] * POLY(y - floor y) for y = m - s in
 // [0, 6]; zero for y > 6 (n_r = -6, Sec. 5.2).  LUT[k] = e^{-k} rounded to
 // binary32; POLY coefficients as printed in Sec. 4, rounded to binary32.
@@ -111,6 +124,36 @@ __device__ __forceinline__ float row16_max(float v) {
   v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xf, 0xf, false)));
   v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xf, 0xf, false)));
   return v;
+}
+
+// Maxima without NaN canonicalization (the compiler quiets both inputs of a
+// max whose operands come from a lane exchange): one v_max_f32 for values
+// that are never NaN, and the max of non-negative floats on their bits
+// (integer order = float order), which also lets the DPP moves fuse into the
+// max.
+__device__ __forceinline__ float max_nn(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+__device__ __forceinline__ float max_xor16_nn(float v) {
+  const unsigned u = __float_as_uint(v);
+  auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return max_nn(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// max over the 64 lanes of a non-negative float (result in every lane)
+__device__ __forceinline__ float wave_max_pos(float v) {
+  int x = __float_as_int(v);
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xf, 0xf, true));
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xf, 0xf, true));
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x124, 0xf, 0xf, true));
+  x = max(x, __builtin_amdgcn_mov_dpp(x, 0x128, 0xf, 0xf, true));
+  auto r = __builtin_amdgcn_permlane16_swap((unsigned)x, (unsigned)x, false, false);
+  x = max((int)r[0], (int)r[1]);
+  r = __builtin_amdgcn_permlane32_swap((unsigned)x, (unsigned)x, false, false);
+  return __int_as_float(max((int)r[0], (int)r[1]));
 }
 
 // max over the 64 lanes of the wave (result in every lane).
