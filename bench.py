@@ -38,9 +38,9 @@ def measured_traffic(kernel: str, workload: str):
     summary (profiles/traffic.txt), or None if the kernel's sources changed
     since the counters were taken."""
     import hashlib
-    srcs = {"k_attn_prefill": ["paper_2412_08585_amd/csrc/attn_prefill.hip",
-                               "paper_2412_08585_amd/csrc/turbo_common.h",
-                               "paper_2412_08585_amd/build.py"],
+    srcs = {"k_attn_prefill16": ["paper_2412_08585_amd/csrc/attn_prefill.hip",
+                                 "paper_2412_08585_amd/csrc/turbo_common.h",
+                                 "paper_2412_08585_amd/build.py"],
             "k_attn_decode": ["paper_2412_08585_amd/csrc/attn_decode.hip",
                               "paper_2412_08585_amd/csrc/kv_tail.hip",
                               "paper_2412_08585_amd/csrc/turbo_common.h",
@@ -277,10 +277,10 @@ def main():
                             "frac_hbm": round(decode_bytes / ms_d / 1e6 / PEAK_HBM_GBS, 4),
                             "note": "cache of this workload (22 MB) may sit in the 256 MB MALL"},
         },
-        "roofline": {"kernel": "k_attn_prefill", "bound": "mfma",
+        "roofline": {"kernel": "k_attn_prefill16", "bound": "mfma",
                      "achieved": round(prefill_tops, 2), "peak": PEAK_INT8_TOPS,
                      "unit": "TOP/s", "frac": round(prefill_tops / PEAK_INT8_TOPS, 4),
-                     "traffic": measured_traffic("k_attn_prefill", w.name),
+                     "traffic": measured_traffic("k_attn_prefill16", w.name),
                      "per_launch_ops": prefill_ops},
     }
 

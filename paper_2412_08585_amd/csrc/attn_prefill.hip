@@ -465,25 +465,26 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
   const int jend = a.causal ? i : a.nbc - 1;
 
   // ---- tile copies: thread tid moves 16-byte chunks tid and tid + 256 -----
-  const uint4* kg = reinterpret_cast<const uint4*>(a.k8 + kvu * a.nb * 8192) + tid;
-  const uint4* vg = reinterpret_cast<const uint4*>(a.v8 + kvu * a.nb * 8192) + tid;
+  // wave-uniform tile bases; the lane adds its chunk index tid (+256)
+  const uint4* kg = reinterpret_cast<const uint4*>(a.k8 + kvu * a.nb * 8192);
+  const uint4* vg = reinterpret_cast<const uint4*>(a.v8 + kvu * a.nb * 8192);
   const int c0 = tid, c1 = tid + 256;
   const int kdst0 = (c0 >> 3) * 128 + 16 * ((c0 & 7) ^ kswz(c0 >> 3));
   const int kdst1 = (c1 >> 3) * 128 + 16 * ((c1 & 7) ^ kswz(c1 >> 3));
   const int vdst0 = (c0 >> 2) * 64 + 16 * ((c0 & 3) ^ vswz(c0 >> 2));
   const int vdst1 = (c1 >> 2) * 64 + 16 * ((c1 & 3) ^ vswz(c1 >> 2));
   // K_{j+1} and V_{j+1} in flight (registers)
-  uint4 kp0 = kg[0], kp1 = kg[256], vp0 = vg[0], vp1 = vg[256];
+  uint4 kp0 = kg[tid], kp1 = kg[tid + 256], vp0 = vg[tid], vp1 = vg[tid + 256];
   *reinterpret_cast<uint4*>(&L.k[0][kdst0]) = kp0;
   *reinterpret_cast<uint4*>(&L.k[0][kdst1]) = kp1;
   *reinterpret_cast<uint4*>(&L.v[0][vdst0]) = vp0;
   *reinterpret_cast<uint4*>(&L.v[0][vdst1]) = vp1;
   {
     const long o1 = (long)min(1, jend) * 512;
-    kp0 = kg[o1];
-    kp1 = kg[o1 + 256];
-    vp0 = vg[o1];
-    vp1 = vg[o1 + 256];
+    kp0 = kg[o1 + tid];
+    kp1 = kg[o1 + tid + 256];
+    vp0 = vg[o1 + tid];
+    vp1 = vg[o1 + tid + 256];
   }
 
   // ---- Q_i -> int8 (eq. step1bpq; scale over the 64-row block) ----------
@@ -491,7 +492,7 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
   v4i qop[2];
   float sq;
   if (kQ8) {
-    const int8_t* src = a.q8 + (((long)b * a.Hq + h) * a.nb * 64 + qrow) * 128 + 16 * g;
+    const int8_t* src = a.q8 + (((long)b * a.Hq + h) * a.nb * 64 + row0) * 128 + (n * 128 + 16 * g);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) qop[ks] = *reinterpret_cast<const v4i*>(src + 64 * ks);
     sq = a.sq[((long)b * a.Hq + h) * a.nb + i];
@@ -499,7 +500,9 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
   } else {
     uint4 raw[2][2];
     float amax = 0.0f;
-    const uint4* src = a.q + (((long)b * a.Hq + h) * N + qrow) * 16 + 2 * g;
+    // wave-uniform row base + a small lane offset: nothing per lane and
+    // 64-bit stays live across the tile loop
+    const uint4* src = a.q + (((long)b * a.Hq + h) * N + row0) * 16 + (n * 16 + 2 * g);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
@@ -581,8 +584,8 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
     *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst0]) = kp0;
     *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst1]) = kp1;
     const long o2 = (long)min(j + 2, jend) * 512;
-    kp0 = kg[o2];
-    kp1 = kg[o2 + 256];
+    kp0 = kg[o2 + tid];
+    kp1 = kg[o2 + tid + 256];
     const bool trace_tile = traced && j == a.tr_j;
     if constexpr (kTrace) {
       if (trace_tile) {
@@ -667,31 +670,38 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
       }
     }
     // ---- PV_j on the MFMA; Ost += (s_P s_V / beta) V_j^T Q(P~)^T --------
-    v4i acc[8];
+    // in two halves of four channel blocks (operands and accumulators of
+    // all eight at once would not fit beside O in 128 VGPRs)
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) {
-      const v4i vop = *reinterpret_cast<const v4i*>(&L.v[buf][vbase + 1024 * cb]);
-      const v4i z = {kAccSeed, kAccSeed, kAccSeed, kAccSeed};
-      acc[cb] = mfma16x16x64(vop, pop, z);
-    }
-    if constexpr (kTrace) {
-      if (trace_tile) {
-        // register r of channel block cb <-> channel 16cb + 4g + r
-        int* tp = reinterpret_cast<int*>(a.trace + TURBO_TRACE_PV) + (16 * w + n) * 128 + 4 * g;
+    for (int hv = 0; hv < 2; ++hv) {
+      v4i acc[4];
 #pragma unroll
-        for (int cb = 0; cb < 8; ++cb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) tp[16 * cb + r] = acc[cb][r] - kAccSeed;
+      for (int c = 0; c < 4; ++c) {
+        const v4i vop = *reinterpret_cast<const v4i*>(&L.v[buf][vbase + 1024 * (4 * hv + c)]);
+        const v4i z = {kAccSeed, kAccSeed, kAccSeed, kAccSeed};
+        acc[c] = mfma16x16x64(vop, pop, z);
       }
+      if constexpr (kTrace) {
+        if (trace_tile) {
+          // register r of channel block cb <-> channel 16cb + 4g + r
+          int* tp = reinterpret_cast<int*>(a.trace + TURBO_TRACE_PV) + (16 * w + n) * 128 + 4 * g;
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) tp[16 * (4 * hv + c) + r] = acc[c][r] - kAccSeed;
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          O[4 * hv + c][r] = __builtin_fmaf(g26, acc_unseed(acc[c][r]), O[4 * hv + c][r]);
+      __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int cb = 0; cb < 8; ++cb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) O[cb][r] = __builtin_fmaf(g26, acc_unseed(acc[cb][r]), O[cb][r]);
     *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst0]) = vp0;
     *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst1]) = vp1;
-    vp0 = vg[o2];
-    vp1 = vg[o2 + 256];
+    vp0 = vg[o2 + tid];
+    vp1 = vg[o2 + tid + 256];
     skj = skn;
     svj = svn;
   }
@@ -706,7 +716,7 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
   l = add_xor32(l);
   if (qrow < N) {
     const float f = beta / l;
-    uint2* orow = a.o + (((long)b * a.Hq + h) * N + qrow) * 32;
+    uint2* orow = a.o + (((long)b * a.Hq + h) * N + row0) * 32 + n * 32;
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
       f16x4_t hv;
@@ -714,7 +724,7 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
       for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][e] * f);
       orow[(16 * cb + 4 * g) / 4] = __builtin_bit_cast(uint2, hv);
     }
-    if (a.lse && g == 0) a.lse[((long)b * a.Hq + h) * N + qrow] = mrow + logf(l);
+    if (a.lse && g == 0) a.lse[(((long)b * a.Hq + h) * N + row0) + n] = mrow + logf(l);
   }
 }
 
