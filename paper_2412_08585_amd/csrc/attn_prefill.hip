@@ -567,8 +567,10 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
   // exactly (a power-of-two factor; c cannot be subnormal for fp16 inputs)
   const float sm26 = a.sm_scale * 0x1p26f;
 
-  for (int j = 0; j <= jend; ++j) {
-    const int buf = j & 1;
+  // The tile step, unrolled by two over the LDS buffer index so that every
+  // LDS address is a register plus an immediate offset.
+  auto tile = [&](const int j, auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
     const float skn = skp[min(j + 1, jend)], svn = svp[min(j + 1, jend)];
     // ---- S^T_j = K_j Q^T on the MFMA -----------------------------------
     v4i S[4];
@@ -704,6 +706,10 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
     vp1 = vg[o2 + tid + 256];
     skj = skn;
     svj = svn;
+  };
+  for (int j = 0; j <= jend; j += 2) {
+    tile(j, std::integral_constant<int, 0>{});
+    if (j + 1 <= jend) tile(j + 1, std::integral_constant<int, 1>{});
   }
 
   // ---- epilogue: O / l (fp16), L = m + ln l ----------------------------
