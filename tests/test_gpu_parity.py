@@ -319,6 +319,65 @@ def test_prefill_tiles_with_empty_p(orc, ta, dev):
     _cmp_lse(lse, rl, "prefill empty tiles lse")
 
 
+def _rowmax_path(q, k, sm, causal):
+    """fp64 running maxima of the scaled scores per 64-key tile (no
+    quantization): the per-tile drops m_old - m_new and the product of
+    e^(m_old - m_new) over the tiles, per row."""
+    s = np.einsum("bhnd,bktd->bhnt", q.double().numpy(), k.double().numpy()) * sm
+    N = s.shape[-1]
+    if causal:
+        s = np.where(np.tril(np.ones((N, N), bool)), s, -np.inf)
+    m = np.full(s.shape[:-1], -np.inf)
+    logbeta = np.zeros(s.shape[:-1])
+    jump = np.zeros(s.shape[:-1])
+    for j in range(0, N, 64):
+        mn = np.maximum(m, s[..., j:j + 64].max(-1))
+        d = np.where(np.isfinite(m), mn - m, 0.0)
+        jump = np.maximum(jump, d)
+        logbeta -= d
+        m = mn
+    return jump, logbeta
+
+
+@pytest.mark.parametrize("case", ["jump", "decay"])
+@pytest.mark.parametrize("causal", [True, False])
+def test_prefill_rescale_paths(orc, ta, dev, case, causal):
+    """The accumulator rescale of Algorithm 1 at its extremes.  "jump": one
+    key block whose scores exceed everything before by more than 6, so the
+    factor SAS(m_old - m_new) is 0 and the kernel renormalizes its kept
+    accumulator (O = beta * Ost with beta = 0).  "decay": scores that rise
+    steadily along the keys, so the per-tile factors multiply beta below
+    2^-64 and the renormalization runs mid-sequence."""
+    sm = 1 / np.sqrt(128)
+    g = torch.Generator().manual_seed(77)
+    u = torch.randn(128, generator=g, dtype=torch.float64)
+    u /= u.norm()
+    if case == "jump":
+        N = 64 * 5
+        q = (torch.randn(1, 2, N, 128, generator=g, dtype=torch.float64) + 3.0 * u).half()
+        k = (torch.randn(1, 1, N, 128, generator=g, dtype=torch.float64) * 0.2).half()
+        k[0, 0, 200] = (40.0 * u).half()
+    else:
+        N = 64 * 64
+        q = (torch.randn(1, 2, N, 128, generator=g, dtype=torch.float64) + 3.0 * u).half()
+        t = torch.arange(N, dtype=torch.float64)[:, None] / 64.0
+        k = (torch.randn(1, 1, N, 128, generator=g, dtype=torch.float64) * 0.1
+             + 5.0 * t * u).half()
+    v = _rand((1, 1, N, 128), 931)
+    jump, logbeta = _rowmax_path(q, k, sm, causal)
+    if case == "jump":
+        assert (jump > 8.0).sum() > 100, "the planted key must raise many rows' maximum by > 6"
+    else:
+        assert (logbeta < -80.0).sum() > 100, "beta must underflow 2^-64 in many rows"
+    _log(f"prefill rescale {case} causal={causal}: max jump {jump.max():.1f}, "
+         f"min log beta {logbeta.min():.1f}")
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
+    o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, sm, causal, return_lse=True)
+    ro, rl = orc.attn_prefill(q, k, v, sm, causal)
+    _cmp_o(o, ro, f"prefill rescale {case} O")
+    _cmp_lse(lse, rl, f"prefill rescale {case} lse")
+
+
 def test_determinism(ta, dev):
     N = 64 * 4 + 9
     q, k, v = _rand((2, 4, N, 128), 1), _rand((2, 2, N, 128), 2), _rand((2, 2, N, 128), 3)
