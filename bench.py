@@ -33,11 +33,30 @@ PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, 8 TB/s
 PEAK_FP16_TFLOPS = 2500.0  # MI355X dense fp16 MFMA, 2.5 PFLOP/s
 
 
+def source_digest(paths) -> str:
+    """First 16 hex digits of the sha256 of the given source files with their
+    comments, leading/trailing blanks and empty lines removed, so that an edit
+    of the prose alone keeps the digest (and the counters taken under it)."""
+    import hashlib
+    import re
+    m = hashlib.sha256()
+    for f in paths:
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+            text = fh.read()
+        if f.endswith(".py"):
+            text = re.sub(r"(?m)^\s*#.*$", "", text)
+        else:
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            text = re.sub(r"//[^\n]*", "", text)
+        lines = [ln.strip() for ln in text.splitlines()]
+        m.update("\n".join(ln for ln in lines if ln).encode())
+    return m.hexdigest()[:16]
+
+
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
     summary (profiles/traffic.txt), or None if the kernel's sources changed
     since the counters were taken."""
-    import hashlib
     srcs = {"k_attn_prefill16": ["paper_2412_08585_amd/csrc/attn_prefill.hip",
                                  "paper_2412_08585_amd/csrc/turbo_common.h",
                                  "paper_2412_08585_amd/build.py"],
@@ -48,11 +67,7 @@ def measured_traffic(kernel: str, workload: str):
     path = os.path.join(ROOT, "profiles", "traffic.txt")
     if not srcs or not os.path.exists(path):
         return None
-    m = hashlib.sha256()
-    for f in srcs:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            m.update(fh.read())
-    digest = m.hexdigest()[:16]
+    digest = source_digest(srcs)
     for line in open(path):
         parts = line.split()
         if len(parts) == 4 and parts[0] == kernel and parts[1] == workload and parts[2] == digest:

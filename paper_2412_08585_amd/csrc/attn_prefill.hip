@@ -1,11 +1,16 @@
 // TurboAttention prefill on gfx950 (Algorithm 1): int8 QK^T and PV on the
-// 32x32x32 i8 MFMA, SAS online softmax in fp32 on the VALU.
+// i8 MFMA, SAS online softmax in fp32 on the VALU.  Two kernels:
+//   * k_attn_prefill16 (further below): B_r = B_c = 64, the paper's setting,
+//     with four waves of 16 query rows -- the default, the pre-quantized-Q
+//     path and the test hook;
+//   * k_attn_prefill (this one): waves of 32 query rows, templated over
+//     B_r in {32, 64, 128} and B_c in {32, 64, 128} for the other block sizes
+//     of Table 3.
 //
-// A workgroup of B_r / 32 waves owns one (sequence b, query head h, query
-// block i of B_r rows); wave qh holds queries B_r i + 32qh .. +31 and all run
-// over the key blocks j (those with a key at or before the block's last row
-// when causal).  B_r = 64 (two waves) is the paper's setting; 32 and 128 are
-// its Table 3 variants.  The Q scale and the P scale of Algorithm 1 cover the
+// k_attn_prefill: a workgroup of B_r / 32 waves owns one (sequence b, query
+// head h, query block i of B_r rows); wave qh holds queries B_r i + 32qh ..
+// +31 and all run over the key blocks j (those with a key at or before the
+// block's last row when causal).  The Q scale and the P scale of Algorithm 1 cover the
 // whole B_r x 64 tile, so the waves exchange their partial maxima through LDS
 // (once for Q, once per tile for P).  32 queries per wave keep a wave under
 // 256 VGPRs (two waves per SIMD, MFMA results in VGPRs).  With B_r = 128 the
