@@ -567,6 +567,8 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
 #pragma unroll
     for (int r = 0; r < 4; ++r) O[cb][r] = 0.0f;
   float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
+  // 119 / pmax of the last tile that computed it, as wave-uniform bits
+  unsigned pmax_prev = 0xffffffffu, inv_prev = 0u;
   float skj = skp[0], svj = svp[0];
   // sm_scale 2^26: (sq s_K) * (sm_scale 2^26) = ((sq s_K) * sm_scale) 2^26
   // exactly (a power-of-two factor; c cannot be subnormal for fp16 inputs)
@@ -640,7 +642,12 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
         rs = (mb | r) ? rs + p : p;
         pmax = (mb | r) ? fmaxf(pmax, p) : p;
       }
-    const float alpha = sas_y(mnew - mold, L.lut);  // 0 when mold = -inf
+    // SAS(m_old - m_new); 0 when m_old = -inf.  When no row of the wave moved
+    // its maximum the argument is 0 in every lane (rows past N, which see no
+    // key, also take this branch: they are never written) and SAS(0) is
+    // LUT[0] * POLY(0) = c0 exactly -- the common case away from the diagonal.
+    float alpha = kC0;
+    if (__builtin_amdgcn_ballot_w64(mnew > mold) != 0) alpha = sas_y(mnew - mold, L.lut);
     lpart = alpha * lpart + rs;
     mrow = mnew;
     // ---- tile maximum of P~ over the four waves ------------------------
@@ -660,7 +667,15 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
     }
     beta = nbeta;
     // ---- Q(P~) with scale pmax/119 over the 64 x 64 tile ----------------
-    const float inv = pmax > 0.0f ? kQmax / pmax : 0.0f;
+    // tile-uniform (scalar registers); the same pmax as the last tile (often
+    // SAS(0), when a row sets its maximum in the tile) reuses the quotient
+    const unsigned pbits = __builtin_amdgcn_readfirstlane(__float_as_uint(pmax));
+    pmax = __uint_as_float(pbits);
+    if (pbits != pmax_prev) {
+      inv_prev = __builtin_amdgcn_readfirstlane(__float_as_uint(pmax > 0.0f ? kQmax / pmax : 0.0f));
+      pmax_prev = pbits;
+    }
+    const float inv = __uint_as_float(inv_prev);
     // s_P = pmax / 119 only scales O (no code depends on it): the product
     // with the rounded reciprocal is within one ulp of the quotient; the
     // factor 2^26 undoes the accumulator seed
