@@ -740,17 +740,23 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
     l = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
   }
   l = add_xor32(l);
-  if (qrow < N) {
+  // the lane index again, from an instruction the compiler cannot merge with
+  // the prologue's: nothing lane-derived stays live across the tile loop
+  // only for the epilogue (which kept three registers spilled)
+  int lane_e;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane_e));
+  const int ne = lane_e & 15, ge = lane_e >> 4;
+  if (row0 + ne < N) {
     const float f = beta / l;
-    uint2* orow = a.o + (((long)b * a.Hq + h) * N + row0) * 32 + n * 32;
+    uint2* orow = a.o + (((long)b * a.Hq + h) * N + row0) * 32 + ne * 32;
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
       f16x4_t hv;
 #pragma unroll
       for (int e = 0; e < 4; ++e) hv[e] = (_Float16)(O[cb][e] * f);
-      orow[(16 * cb + 4 * g) / 4] = __builtin_bit_cast(uint2, hv);
+      orow[(16 * cb + 4 * ge) / 4] = __builtin_bit_cast(uint2, hv);
     }
-    if (a.lse && g == 0) a.lse[(((long)b * a.Hq + h) * N + row0) + n] = mrow + logf(l);
+    if (a.lse && ge == 0) a.lse[(((long)b * a.Hq + h) * N + row0) + ne] = mrow + logf(l);
   }
 }
 
