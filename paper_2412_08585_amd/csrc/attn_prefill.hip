@@ -427,7 +427,6 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
 // before the previous barrier; softmax; tile maximum exchange + barrier; PV_j
 // from V buffer j&1; V_{j+1} into V buffer (j+1)&1, whose last readers
 // (PV_{j-1}) all finished before this tile's barrier.
-constexpr int kP16Waves = 4;
 
 // (conflict-free with 32 banks served 8 lanes per pass and with 64 banks
 // served 16 lanes per pass; they depend only on key bits 0, 1, 4, 5 and
@@ -439,17 +438,21 @@ __device__ __forceinline__ int vswz(int ch) {
   return (((ch >> 1) ^ (ch >> 3)) & 1) | (((ch >> 2) & 1) << 1);
 }
 
+template <int kW>
 struct Prefill16Lds {
   __attribute__((aligned(16))) int8_t k[2][64 * 128];   // [key][128 channels], swizzled
   __attribute__((aligned(16))) int8_t v[2][128 * 64];   // [channel][64 keys], swizzled
   float lut[8];
-  float xmax[2][kP16Waves];
-  float xq[kP16Waves];
+  float xmax[2][kW];
+  float xq[kW];
 };
 
-template <bool kTrace, bool kQ8>
-__global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArgs a) {
-  __shared__ Prefill16Lds L;
+// kW waves of 16 rows: B_r = 16 kW (4: the paper's 64; 8: Table 3's 128).
+template <bool kTrace, bool kQ8, int kW>
+__global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
+  static_assert(kW == 4 || kW == 8, "B_r = 64 or 128");
+  constexpr int kBr = 16 * kW;
+  __shared__ Prefill16Lds<kW> L;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -462,15 +465,18 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
   const int b = (Lx % BH) / a.Hq, h = Lx % a.Hq;
   const int G = a.Hq / a.Hkv, kh = h / G;
   const int N = a.N;
-  const int row0 = 64 * i + 16 * w;  // first query row of this wave
+  const int row0 = kBr * i + 16 * w;  // first query row of this wave
   const int qrow = row0 + n;
   const long kvu = (long)b * a.Hkv + kh;
   const float* skp = a.sk + kvu * a.nbc;
   const float* svp = a.sv + kvu * a.nbc;
-  const int jend = a.causal ? i : a.nbc - 1;
+  // last key tile: the one holding the block's last row when causal
+  const int jend = a.causal ? min(a.nbc - 1, (kBr * i + kBr - 1) / 64) : a.nbc - 1;
 
-  // ---- tile copies: thread tid moves 16-byte chunks tid and tid + 256 -----
-  // wave-uniform tile bases; the lane adds its chunk index tid (+256)
+  // ---- tile copies: the 512 16-byte chunks of a K (V) tile, one (kW = 8)
+  // or two (kW = 4: tid and tid + 256) per thread --------------------------
+  // wave-uniform tile bases; the lane adds its chunk index
+  constexpr bool kTwo = kW == 4;
   const uint4* kg = reinterpret_cast<const uint4*>(a.k8 + kvu * a.nb * 8192);
   const uint4* vg = reinterpret_cast<const uint4*>(a.v8 + kvu * a.nb * 8192);
   const int c0 = tid, c1 = tid + 256;
@@ -479,17 +485,25 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
   const int vdst0 = (c0 >> 2) * 64 + 16 * ((c0 & 3) ^ vswz(c0 >> 2));
   const int vdst1 = (c1 >> 2) * 64 + 16 * ((c1 & 3) ^ vswz(c1 >> 2));
   // K_{j+1} and V_{j+1} in flight (registers)
-  uint4 kp0 = kg[tid], kp1 = kg[tid + 256], vp0 = vg[tid], vp1 = vg[tid + 256];
+  uint4 kp0 = kg[tid], vp0 = vg[tid], kp1 = {}, vp1 = {};
+  if constexpr (kTwo) {
+    kp1 = kg[tid + 256];
+    vp1 = vg[tid + 256];
+  }
   *reinterpret_cast<uint4*>(&L.k[0][kdst0]) = kp0;
-  *reinterpret_cast<uint4*>(&L.k[0][kdst1]) = kp1;
   *reinterpret_cast<uint4*>(&L.v[0][vdst0]) = vp0;
-  *reinterpret_cast<uint4*>(&L.v[0][vdst1]) = vp1;
+  if constexpr (kTwo) {
+    *reinterpret_cast<uint4*>(&L.k[0][kdst1]) = kp1;
+    *reinterpret_cast<uint4*>(&L.v[0][vdst1]) = vp1;
+  }
   {
     const long o1 = (long)min(1, jend) * 512;
     kp0 = kg[o1 + tid];
-    kp1 = kg[o1 + tid + 256];
     vp0 = vg[o1 + tid];
-    vp1 = vg[o1 + tid + 256];
+    if constexpr (kTwo) {
+      kp1 = kg[o1 + tid + 256];
+      vp1 = vg[o1 + tid + 256];
+    }
   }
 
   // ---- Q_i -> int8 (eq. step1bpq; scale over the 64-row block) ----------
@@ -520,7 +534,9 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
     amax = wave_max_fast(amax);
     if (lane == 0) L.xq[w] = amax;
     __syncthreads();
-    amax = fmaxf(fmaxf(L.xq[0], L.xq[1]), fmaxf(L.xq[2], L.xq[3]));
+    amax = L.xq[0];
+#pragma unroll
+    for (int u = 1; u < kW; ++u) amax = fmaxf(amax, L.xq[u]);
     float inv = 0.0f;
     sq = 0.0f;
     if (amax > 0.0f) {
@@ -591,10 +607,10 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
       S[mb] = acc;
     }
     *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst0]) = kp0;
-    *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst1]) = kp1;
+    if constexpr (kTwo) *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst1]) = kp1;
     const long o2 = (long)min(j + 2, jend) * 512;
     kp0 = kg[o2 + tid];
-    kp1 = kg[o2 + tid + 256];
+    if constexpr (kTwo) kp1 = kg[o2 + tid + 256];
     const bool trace_tile = traced && j == a.tr_j;
     if constexpr (kTrace) {
       if (trace_tile) {
@@ -648,14 +664,23 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
     // LUT[0] * POLY(0) = c0 exactly -- the common case away from the diagonal.
     float alpha = kC0;
     if (__builtin_amdgcn_ballot_w64(mnew > mold) != 0) alpha = sas_y(mnew - mold, L.lut);
+    // with B_r = 128 a wave can see no key of the tile (its rows all precede
+    // it): the rows are not processed, so nothing is rescaled (factor 1)
+    if constexpr (kW > 4) {
+      if (a.causal && 64 * j > row0 + 15) alpha = 1.0f;
+    }
     lpart = alpha * lpart + rs;
     mrow = mnew;
     // ---- tile maximum of P~ over the four waves ------------------------
     pmax = wave_max_pos(pmax);  // P~ >= 0
     if (lane == 0) L.xmax[buf][w] = pmax;
     __syncthreads();
-    pmax = __int_as_float(max(max(__float_as_int(L.xmax[buf][0]), __float_as_int(L.xmax[buf][1])),
-                              max(__float_as_int(L.xmax[buf][2]), __float_as_int(L.xmax[buf][3]))));
+    {
+      int pm = __float_as_int(L.xmax[buf][0]);
+#pragma unroll
+      for (int u = 1; u < kW; ++u) pm = max(pm, __float_as_int(L.xmax[buf][u]));
+      pmax = __int_as_float(pm);
+    }
     // ---- rescale factor: O = beta * Ost --------------------------------
     float nbeta = beta * alpha;
     if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
@@ -721,9 +746,9 @@ __global__ __launch_bounds__(64 * kP16Waves, 4) void k_attn_prefill16(PrefillArg
       __builtin_amdgcn_sched_barrier(0);
     }
     *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst0]) = vp0;
-    *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst1]) = vp1;
+    if constexpr (kTwo) *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst1]) = vp1;
     vp0 = vg[o2 + tid];
-    vp1 = vg[o2 + tid + 256];
+    if constexpr (kTwo) vp1 = vg[o2 + tid + 256];
     skj = skn;
     svj = svn;
   };
@@ -773,13 +798,15 @@ static void launch_bc(const PrefillArgs& a, int total, hipStream_t stream) {
 
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
   const int total = a.B * a.Hq * a.nbq;
-  const dim3 b16(64 * kP16Waves);
+  const dim3 b16(256);
   if (a.trace)  // test hook: B_r = B_c = 64 only
-    hipLaunchKernelGGL((k_attn_prefill16<true, false>), dim3(total), b16, 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill16<true, false, 4>), dim3(total), b16, 0, stream, a);
   else if (a.q8)  // B_r = B_c = 64 only
-    hipLaunchKernelGGL((k_attn_prefill16<false, true>), dim3(total), b16, 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill16<false, true, 4>), dim3(total), b16, 0, stream, a);
   else if (a.waves == 2 && a.bc == 64)
-    hipLaunchKernelGGL((k_attn_prefill16<false, false>), dim3(total), b16, 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill16<false, false, 4>), dim3(total), b16, 0, stream, a);
+  else if (a.waves == 4 && a.bc == 64)  // (B_r, B_c) = (128, 64)
+    hipLaunchKernelGGL((k_attn_prefill16<false, false, 8>), dim3(total), dim3(512), 0, stream, a);
   else if (a.waves == 1)
     launch_bc<1>(a, total, stream);
   else if (a.waves == 4)
