@@ -130,8 +130,8 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding "
-                          "is described in DESIGN.md but not implemented"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU only (--gpus 1); the "
+                          "library has no multi-GPU sharding"}))
         sys.exit(2)
     import torch
 
