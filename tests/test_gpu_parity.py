@@ -341,7 +341,8 @@ def _rowmax_path(q, k, sm, causal):
 
 @pytest.mark.parametrize("case", ["jump", "decay"])
 @pytest.mark.parametrize("causal", [True, False])
-def test_prefill_rescale_paths(orc, ta, dev, case, causal):
+@pytest.mark.parametrize("br", [64, 128])
+def test_prefill_rescale_paths(orc, ta, dev, case, causal, br):
     """The accumulator rescale of Algorithm 1 at its extremes.  "jump": one
     key block whose scores exceed everything before by more than 6, so the
     factor SAS(m_old - m_new) is 0 and the kernel renormalizes its kept
@@ -369,11 +370,12 @@ def test_prefill_rescale_paths(orc, ta, dev, case, causal):
         assert (jump > 8.0).sum() > 100, "the planted key must raise many rows' maximum by > 6"
     else:
         assert (logbeta < -80.0).sum() > 100, "beta must underflow 2^-64 in many rows"
-    _log(f"prefill rescale {case} causal={causal}: max jump {jump.max():.1f}, "
+    _log(f"prefill rescale {case} causal={causal} B_r={br}: max jump {jump.max():.1f}, "
          f"min log beta {logbeta.min():.1f}")
     k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
-    o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, sm, causal, return_lse=True)
-    ro, rl = orc.attn_prefill(q, k, v, sm, causal)
+    o, lse = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, sm, causal, return_lse=True,
+                                   block_rows=br)
+    ro, rl = orc.attn_prefill(q, k, v, sm, causal, block_rows=br)
     _cmp_o(o, ro, f"prefill rescale {case} O")
     _cmp_lse(lse, rl, f"prefill rescale {case} lse")
 
