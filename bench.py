@@ -278,8 +278,8 @@ def main():
         "dtype": "int8",
         "data": "synthetic (seeded N(0,1) fp16 with 4 K outlier channels x10; no weights)",
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "seq_len": N,
-                   "head_dim": d, "causal": True, "kv_cache": w.bits, "decode_tokens": 1,
-                   "decode_kv_split_groups": split},
+                   "head_dim": d, "causal": True, "kv_cache": w.bits, "block_rows": 64,
+                   "block_cols": 64, "decode_tokens": 1, "decode_kv_split_groups": split},
         "kernels": {
             "quantize_kv": {"ms": round(ms_q, 4), "GB/s": round(quant_bytes / ms_q / 1e6, 1),
                             "frac_hbm": round(quant_bytes / ms_q / 1e6 / PEAK_HBM_GBS, 4)},
