@@ -226,6 +226,22 @@ static double or_e(const or_opts* o, double hi, double lo) {
   return o->sas ? (double)or_sas_y((float)y) : exp(-y);
 }
 
+/* Factor that rescales a running state (l, O of Algorithms 1 and 2; the
+ * weight of a chunk in the split-KV merge) when the maximum it was taken
+ * against moves from lo to hi >= lo.  Reading: SAS stands in for e^x; where
+ * the maximum has not moved the exponent is exactly 0 and the factor is
+ * e^0 = 1, so the state is left as it is.  Evaluating SAS there would give
+ * the fit error POLY(0) = 0.9996 of Sec. 4, compounded once per online step,
+ * which makes the result depend on how many steps (tiles, chunks) the keys
+ * are cut into.  A moved maximum takes SAS (or exp) of the difference, and
+ * lo = -inf (an empty state) gives 0.  The SAS value of an individual score
+ * (P~ = SAS(0) for the row's maximum) is not a rescale and keeps POLY(0). */
+static double or_rescale(const or_opts* o, double hi, double lo) {
+  if (lo == -INFINITY) return 0.0;
+  if (hi == lo) return 1.0;
+  return or_e(o, hi, lo);
+}
+
 /* Running state of one query row: m (binary32-valued when FlashQ is on),
  * l and O (double). */
 typedef struct or_row {
@@ -260,9 +276,10 @@ typedef struct or_trace {
  *                   FlashQ off), row t at vq/vf + t*d.
  * Steps, in the order of Algorithm 1:
  *   m_new = max(m_old, rowmax S);  P~ = SAS(S - m_new);
- *   l = SAS(m_old - m_new) l + rowsum P~;
+ *   alpha = SAS(m_old - m_new), 1 when m_new = m_old (or_rescale);
+ *   l = alpha l + rowsum P~;
  *   s_P = max P~ / 119 over the tile, Q(P~) = round(P~ / s_P) (FlashQ on);
- *   O = SAS(m_old - m_new) O + s_P s_V Q(P~) V^{q1}.
+ *   O = alpha O + s_P s_V Q(P~) V^{q1}.
  * A row with no visible key is left untouched.  P scale granularity: the
  * whole tile (all processed rows and visible keys) for prefill (B_r x B_c,
  * Algorithm 1) and one row for decode (1 x B_c, Algorithm 2).
@@ -293,7 +310,7 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
       rowsum += e;
       if ((float)e > pmax) pmax = (float)e;
     }
-    alpha[r] = (mold == -INFINITY) ? 0.0 : or_e(o, mnew, mold);
+    alpha[r] = or_rescale(o, mnew, mold);
     rows[r].l = alpha[r] * rows[r].l + rowsum;
     rows[r].m = mnew;
     for (int e = 0; e < d; ++e) rows[r].O[e] *= alpha[r];
@@ -343,7 +360,7 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
  * accumulator update with the inverse of diag(SAS(m_old - m_new)), which
  * would not compute a softmax and disagrees with the l update next to it, so
  * O is multiplied by that factor; when the maximum does not move the factor
- * is SAS(0) as written.
+ * is e^0 = 1 (or_rescale).
  * Block sizes (Table 3 varies them): Q is quantized per br rows of a head
  * (br = B_r in {32, 64, 128}); K and V are quantized per bc tokens (bc = B_c
  * in {32, 64, 128}), each online step covers bc keys and the P scale covers
@@ -456,7 +473,7 @@ void or_attn_prefill(const float* q, const float* k, const float* v, int B, int 
  * the online SAS step with the P scale taken over the row's 64 keys.
  * Split-KV extension (not in the paper): chunks of `split` groups each run
  * the loop from m = -inf; with more than one chunk the states are merged in
- * ascending order with m* = max m_s, w_s = SAS(m_s - m*),
+ * ascending order with m* = max m_s, w_s = SAS(m_s - m*) (1 for m_s = m*),
  * O = sum w_s O_s / sum w_s l_s, L = m* + ln(sum w_s l_s).
  * No group: o = 0, lse = -inf.  Outputs o double [B][Hq][d], lse [B][Hq].
  * With the int8 buffer of Sec. 3.3 (tk != NULL): the seq_len - 64 ng newest
@@ -592,7 +609,7 @@ void or_attn_decode(const float* q, const uint8_t* kc, const uint8_t* vc, const 
           lse[orow] = ms[0] + log(ls[0]);
         } else {
           for (int s = 0; s < nsplit; ++s) {
-            const double w = or_e(&opts, mstar, ms[s]);
+            const double w = or_rescale(&opts, mstar, ms[s]);
             den += w * ls[s];
             for (int e = 0; e < d; ++e) num[e] += w * Oall[(size_t)s * d + e];
           }

@@ -3,8 +3,8 @@
 - With FlashQ and SAS switched off the online loop must reduce to exact softmax
   attention (eq. stdattn) — checked against torch's CPU attention in float64.
 - Integer contractions of a traced tile equal brute-force matrix products.
-- Uniform scores reduce the loop to a closed form that exposes the tile order,
-  the per-tile P scale and the rescale factor SAS(0) of an unchanged maximum.
+- Uniform scores reduce the loop to a closed form that exposes the per-tile P
+  scale and the rescale factor 1 of an unchanged maximum.
 - Invariants: causality per key block, GQA = MHA with repeated KV heads,
   decode with one chunk = unsplit decode, split merge exact under exp.
 """
@@ -64,9 +64,11 @@ def test_traced_tile_integers_are_matrix_products(orc):
 @pytest.mark.parametrize("causal", [True, False])
 def test_uniform_scores_closed_form(orc, causal):
     """Q = 0 makes every score 0, so every kept P~ is SAS(0) = a, every tile
-    quantizes P~ to 119 with s_P = a/119, and the maximum never moves, so each
-    later tile multiplies the history by a.  Row r then averages the dequantized
-    V rows with weight a^(age of the tile) — a closed form."""
+    quantizes P~ to 119 with s_P = a/119, and the maximum never moves, so the
+    rescale factor is e^0 = 1 on every tile after the first (it is not the
+    fit value SAS(0) = 0.9996, which would weight tile j by a^(age of the
+    tile)).  Row r is then the plain average of its visible dequantized V rows,
+    each tile's rows weighted by s_P s_V * 119, a closed form."""
     N = 64 * 3 + 21
     q = torch.zeros(1, 1, N, D, dtype=torch.float16)
     k, v = _rand((1, 1, N, D), 7), _rand((1, 1, N, D), 8)
@@ -86,9 +88,8 @@ def test_uniform_scores_closed_form(orc, causal):
         den = 0.0
         for j in range(last + 1):
             keys = v8[j] if (not causal or j < i) else v8[j][: r % 64 + 1]
-            w = a ** (last - j)
-            num += w * np.float64(np.float32(sp * sv[j])) * 119 * keys.sum(axis=0)
-            den += w * a * keys.shape[0]
+            num += np.float64(np.float32(sp * sv[j])) * 119 * keys.sum(axis=0)
+            den += a * keys.shape[0]
         assert np.allclose(o[0, 0, r], num / den, rtol=1e-12, atol=1e-15), r
         assert abs(lse[0, 0, r] - np.log(den)) < 1e-12
 

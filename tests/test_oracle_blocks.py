@@ -29,9 +29,8 @@ def test_one_block_is_the_same_for_every_block_size(orc, causal):
 @pytest.mark.parametrize("br", [32, 128])
 @pytest.mark.parametrize("causal", [True, False])
 def test_without_quantization_the_block_size_does_not_matter(orc, br, causal):
-    """With FlashQ off no scale depends on the block partition; SAS stays on,
-    so a row of a 128-row block that were processed with a tile it sees no
-    key of would pick up a factor SAS(0) in l (its L would move by ln 0.9996)."""
+    """With FlashQ off no scale depends on the block partition (SAS stays on),
+    so the query block size changes nothing but the summation order."""
     q, k, v = _qkv(1, 2, 4, 2, 64 * 3 + 41)
     o64, l64 = orc.attn_prefill(q, k, v, SM, causal, quant=False)
     o, lse = orc.attn_prefill(q, k, v, SM, causal, quant=False, block_rows=br)
