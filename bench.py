@@ -119,6 +119,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="phi3m-prefill-4k")
     ap.add_argument("--kernel-iters", type=int, default=30)
+    ap.add_argument("--kv-split-groups", type=int, default=0,
+                    help="decode workloads: chunk length of the split-KV decode (0: the "
+                         "library's default, each sequence by its own length; -1: the "
+                         "occupancy-fitted turbo_decode_auto_split)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["quantize", "prefill", "decode", "copy"], default=None,
                     help="launch only this kernel --steps times (for profiler passes); "
@@ -176,7 +180,9 @@ def main():
     od = torch.empty_like(qd)
     lse = torch.empty(B, Hq, N, dtype=torch.float32, device=dev)
     sl = torch.full((B,), N, dtype=torch.int32, device=dev)
-    split = ta.decode_split(B, Hq, Hkv, w.max_groups, 0)
+    # the decode of this batch (B * Hkv = 40 units of 64 groups) takes the
+    # occupancy-fitted chunk length; the decode workloads use the default
+    split = ta.decode_auto_split(B, Hq, Hkv, w.max_groups)
     ws = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev)
 
     def run_quant():
@@ -383,7 +389,9 @@ def bench_decode(args, w):
     torch.cuda.synchronize()
     q = W.decode_query(w, device=dev)
     sl = torch.full((B,), N, dtype=torch.int32, device=dev)
-    split = ta.decode_split(B, Hq, Hkv, w.max_groups, 0)
+    split = args.kv_split_groups
+    if split < 0:
+        split = ta.decode_auto_split(B, Hq, Hkv, w.max_groups)
     ws = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev)
     o = torch.empty_like(q)
     it = [0]
@@ -459,9 +467,9 @@ def bench_decode(args, w):
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "kv_len": N,
                    "head_dim": 128, "kv_cache": w.bits,
                    "head_bits": [int(x) for x in bits], "page_tokens": 16,
-                   "kv_split_groups": split, "cache_copies": ncopy},
+                   "kv_split_groups": ta.decode_split(N, split), "cache_copies": ncopy},
         "attention_TOPS": round(ops / (ms * 1e-3) / 1e12, 3),
-        "roofline": {"kernel": "k_attn_decode+k_decode_combine", "bound": "hbm",
+        "roofline": {"kernel": "k_attn_decode", "bound": "hbm",
                      "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "traffic": measured_traffic("k_attn_decode", w.name),
@@ -492,7 +500,8 @@ def bench_decode(args, w):
         while passes == 0 or dt < CPU_SAMPLE_SECONDS:
             for b, ref in enumerate(refs):
                 t1 = time.perf_counter()
-                ro, _ = oracle.attn_decode(qc[b:b + 1], ref, [N], w.sm_scale, split=split)
+                ro, _ = oracle.attn_decode(qc[b:b + 1], ref, [N], w.sm_scale,
+                                           split=ta.decode_split(N, split))
                 dt += time.perf_counter() - t1
                 rowmax = np.abs(ro[0]).max(axis=-1, keepdims=True)
                 err = max(err, float(np.max(np.abs(got[b] - ro[0]) / rowmax)))

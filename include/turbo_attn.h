@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define TURBO_ABI_VERSION 3
+#define TURBO_ABI_VERSION 4
 
 #define TURBO_HEAD_DIM 128       /* d */
 #define TURBO_BLOCK 64           /* B_r = B_c = step-2 group length (tokens) */
@@ -202,7 +202,8 @@ int turbo_quantize_kv_blocks(const void* k, const void* v, int B, int Hkv, int N
  * s_Q * s_K * sm_scale, online row maximum, SAS in place of exp, running sum
  * of the unquantized SAS values, int8 quantization of the 64x64 SAS tile with
  * scale max/119, int8 PV scaled by s_P * s_V, and the rescale of the
- * accumulator by SAS(m_old - m_new); finally O / l and L = m + ln l.
+ * accumulator by SAS(m_old - m_new) (exactly 1, e^0, for a row whose maximum
+ * did not move); finally O / l and L = m + ln l.
  *
  * q           fp16 [B][Hq][N][128].
  * k8, v8, s_k, s_v  as written by turbo_quantize_kv for the same B, Hkv, N.
@@ -308,12 +309,20 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
  * code * s^int + z^int, and the same SAS online softmax as prefill runs with
  * one query row (P scale per row and group).
  *
+ * The rescale factor SAS(m_old - m_new) of the online step is exactly 1
+ * (e^0) when a row's maximum does not move (reading: SAS stands in for e^x,
+ * and the exponent is exactly 0 there).
+ *
  * Split-KV extension (not in the paper): the groups of a sequence are cut
- * into chunks of kv_split_groups groups.  Each chunk runs the online loop
- * from m = -inf; with more than one chunk the partial states are merged with
- * m* = max m_s, w_s = SAS(m_s - m*), O = sum w_s O_s / sum w_s l_s,
- * L = m* + ln(sum w_s l_s), chunks in ascending order.  With one chunk the
- * result is the unsplit Algorithm 2.
+ * into chunks of kv_split_groups groups (0: turbo_decode_default_split of
+ * the sequence's own group count, so that a sequence's result does not
+ * depend on the batch).  Each chunk runs the online loop from m = -inf; with
+ * more than one chunk the partial states are merged with m* = max m_s,
+ * w_s = SAS(m_s - m*) (1 for m_s = m*), O = sum w_s O_s / sum w_s l_s,
+ * L = m* + ln(sum w_s l_s), chunks in ascending order (a second launch on
+ * the same stream).  With one chunk the result is the unsplit Algorithm 2.
+ * Different chunkings give different results (the n_r threshold drops
+ * scores against the running maximum of each chunk).
  *
  * int8 buffer (Sec. 3.3): with tail != NULL the seq_len mod 64 newest tokens
  * (rows of the buffer) are attended as well.  Reading: the buffer is one more
@@ -335,11 +344,16 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
  * group_table     as for turbo_quantize_kv.  A group whose page or slot entry
  *                 is out of range is skipped (its memory is never read).
  * B, Hq           Hq % Hkv == 0, Hq / Hkv <= 16.
- * kv_split_groups groups per chunk, >= 1; 0 selects
- *                 turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq) with
- *                 Hkv = cache->num_kv_heads (see below).
+ * kv_split_groups groups per chunk, >= 1, for every sequence; 0 selects
+ *                 turbo_decode_default_split(ng) for each sequence of ng
+ *                 cached groups.  turbo_decode_auto_split offers a chunk
+ *                 length fitted to the batch's occupancy instead (pass it
+ *                 explicitly; results then depend on the batch shape).
  * workspace       device scratch of at least turbo_decode_workspace_bytes()
- *                 bytes (with_tail = tail != NULL; may be NULL when that is 0).
+ *                 bytes (with_tail = tail != NULL; may be NULL when that is
+ *                 0): the chunk states, fully written before they are
+ *                 read (no initialization needed).  Calls that share a
+ *                 workspace must not overlap.
  * o               fp16 [B][Hq][128];  lse fp32 [B][Hq] or NULL.
  */
 int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const turbo_kv_tail* tail,
@@ -442,23 +456,29 @@ int turbo_append_kv(const void* k_new, const void* v_new, int B, int Hkv, int d,
  */
 int turbo_sas_softmax(const float* x, float* y, int64_t rows, int cols, hipStream_t stream);
 
-/* The chunk length (in 64-token groups) that kv_split_groups = 0 selects for
- * a decode batch of B sequences, Hq query and Hkv KV heads and
- * max_groups_per_seq.  The decode kernel keeps three waves per SIMD resident
+/* The chunk length (in 64-token groups) that kv_split_groups = 0 gives a
+ * sequence with ng cached groups: ng itself (one chunk) up to 32 groups,
+ * 32 up to 128 groups (2 to 4 chunks), ceil(ng / 4) beyond (4 chunks).  It
+ * depends on the sequence only.  Returns 1 for ng < 1. */
+int turbo_decode_default_split(int ng);
+
+/* A chunk length fitted to the occupancy of a decode batch of B sequences,
+ * Hq query and Hkv KV heads and max_groups_per_seq (to be passed explicitly
+ * as kv_split_groups).  The decode kernel keeps three waves per SIMD resident
  * when Hq / Hkv <= 8 and two otherwise (3072 or 2048 on 256 CUs); the
  * fewest chunks n whose B * Hkv * n waves fill at least two thirds of those
  * slots are chosen, with chunk length ceil(max_groups_per_seq / n) (the
  * whole sequence when B * Hkv already fills them), but never fewer than two
  * groups per chunk.  Since the chunked result merges SAS-weighted
- * partial states, the output depends on the chunk length; pass an explicit
- * kv_split_groups for results that do not depend on the batch shape.
+ * partial states, the output then depends on the batch shape.
  * Returns 1 for arguments < 1. */
 int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq);
 
 /* Workspace bytes turbo_attn_decode needs for these arguments (0 when every
- * sequence fits one chunk and there is no tail).  kv_split_groups = 0 means
- * turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq); with_tail != 0 adds
- * the buffer's chunk. */
+ * sequence fits one chunk and there is no tail): fp32 chunk states
+ * [B][Hq][n][132] with n the most chunks a sequence of max_groups_per_seq
+ * groups can have, plus one with_tail.  kv_split_groups as for
+ * turbo_attn_decode. */
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
                                     int kv_split_groups, int with_tail);
 

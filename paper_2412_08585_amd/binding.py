@@ -68,6 +68,7 @@ def lib() -> ctypes.CDLL:
             "turbo_quantize_kv_blocks": ([P, P, I, I, I, I, I, P, P, P, P, P], I),
             "turbo_qkv_project": ([P, P, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P], I),
             "turbo_decode_auto_split": ([I, I, I, I], I),
+            "turbo_decode_default_split": ([I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
         }
         for name, (args, res) in sig.items():
@@ -281,8 +282,14 @@ def turbo_attn_prefill_trace(q: torch.Tensor, k8, v8, s_k, s_v, tile, sm_scale=N
     return o, _trace_dict(buf)
 
 
-def decode_split(B: int, Hq: int, Hkv: int, max_groups: int, kv_split_groups: int = 0) -> int:
-    return kv_split_groups or int(lib().turbo_decode_auto_split(B, Hq, Hkv, max_groups))
+def decode_split(seq_len: int, kv_split_groups: int = 0) -> int:
+    """Chunk length turbo_attn_decode uses for a sequence of seq_len tokens."""
+    return kv_split_groups or int(lib().turbo_decode_default_split(int(seq_len) // 64))
+
+
+def decode_auto_split(B: int, Hq: int, Hkv: int, max_groups: int) -> int:
+    """Chunk length fitted to a batch's occupancy (turbo_decode_auto_split)."""
+    return int(lib().turbo_decode_auto_split(B, Hq, Hkv, max_groups))
 
 
 def decode_workspace(B: int, Hq: int, Hkv: int, max_groups: int, kv_split_groups: int = 0,

@@ -50,11 +50,10 @@ struct DecodeArgs {
   int max_groups;
   int B, Hq, Hkv, G;
   float sm_scale;
-  int split;                 // groups per chunk
-  int nsplit;                // group chunks per sequence (grid dimension)
+  int split;                 // groups per chunk; 0: decode_default_split of each sequence
+  int nsplit;                // group chunks per (sequence, KV head) in the grid
   int nws;                   // workspace slots per row: nsplit, plus one with a tail
-  int direct;                // one chunk and no tail: write o and lse directly
-  float* ws;                 // [B][Hq][nws][132] unless direct: m, l, -, -, O[128]
+  float* ws;                 // [B][Hq][nws][132]: m, l, -, -, O[128] of each chunk
   const int8_t* tk;          // Sec. 3.3 buffer (null: none): [B][Hkv][64][128]
   const int8_t* tv;          //   [B][Hkv][128][64]
   const float* tscale;       //   [B][Hkv][2]
@@ -66,6 +65,56 @@ struct DecodeArgs {
 
 constexpr int kWsStride = 132;  // m, l, two pad words, O[128] (16-byte aligned)
 constexpr int kWsO = 4;
+
+
+// Chunk length (groups) that kv_split_groups = 0 gives a sequence of ng
+// cached groups: one chunk up to 32 groups, chunks of 32 up to 128 groups,
+// four equal chunks beyond.  It depends on the sequence alone, so a
+// sequence's result does not depend on the batch it is decoded in.
+__host__ __device__ constexpr int decode_default_split(int ng) {
+  return ng <= 32 ? (ng > 0 ? ng : 1) : (ng <= 128 ? 32 : (ng + 3) / 4);
+}
+
+// Chunks of a sequence with ng groups (chunk length split > 0 or the
+// default rule), and the most any sequence of at most max_groups groups has.
+__host__ __device__ constexpr int decode_chunks(int ng, int split) {
+  return ng <= 0 ? 0 : (ng + (split > 0 ? split : decode_default_split(ng)) - 1) /
+                           (split > 0 ? split : decode_default_split(ng));
+}
+__host__ __device__ constexpr int decode_max_chunks(int max_groups, int split) {
+  return split > 0 ? (max_groups + split - 1) / split
+                   : (max_groups <= 32 ? 1 : (max_groups <= 128 ? (max_groups + 31) / 32 : 4));
+}
+
+// The cached groups and buffered tokens decode attends for sequence b.
+struct DecodeSeq {
+  int ng;      // cached groups
+  int split;   // chunk length
+  int nchunk;  // group chunks
+  int nt;      // buffered tokens (0 without a buffer)
+  int nparts;  // nchunk + (nt > 0): states to merge
+};
+
+__device__ __forceinline__ DecodeSeq decode_seq(const DecodeArgs& a, int b) {
+  DecodeSeq q;
+  const int len = a.seq_lens[b];
+  q.ng = min(max(len / 64, 0), a.max_groups);
+  q.split = a.split > 0 ? a.split : decode_default_split(q.ng);
+  q.nchunk = decode_chunks(q.ng, a.split);
+  q.nt = a.tk ? min(max(len - 64 * q.ng, 0), 63) : 0;
+  q.nparts = q.nchunk + (q.nt > 0);
+  return q;
+}
+
+// o = 0 and lse = -inf for the G rows of (b, kh): a sequence with nothing to
+// attend.
+__device__ void decode_write_empty(const DecodeArgs& a, int b, int kh) {
+  for (int r = 0; r < a.G; ++r) {
+    const long bh = (long)b * a.Hq + kh * a.G + r;
+    reinterpret_cast<unsigned*>(a.o)[bh * 64 + threadIdx.x] = 0u;
+    if (a.lse && threadIdx.x == 0) a.lse[bh] = -INFINITY;
+  }
+}
 
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x2 __attribute__((ext_vector_type(2)));
@@ -445,7 +494,9 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
           rs += p[e];
           pmax = fmaxf(pmax, p[e]);
         }
-        const float alpha = sas_y(mnew - mrow, L.lut);  // 0 when mrow = -inf
+        // SAS(m_old - m_new): 0 when m_old = -inf, exactly 1 (e^0) when the
+        // row's maximum did not move
+        const float alpha = mnew > mrow ? sas_y(mnew - mrow, L.lut) : 1.0f;
         lpart = alpha * lpart + rs;
         mrow = mnew;
         pmax = row_max<LPR>(pmax);
@@ -580,10 +631,13 @@ __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decod
   const int rr = lane / LPR, cc = lane % LPR;
   const int G = a.G;
 
-  int ng = a.seq_lens[b] / 64;
-  ng = min(max(ng, 0), a.max_groups);
-  const int g0 = s * a.split;
-  const int g1 = min(ng, g0 + a.split);
+  const DecodeSeq sq_ = decode_seq(a, b);
+  const int g0 = s * sq_.split;
+  const int g1 = min(sq_.ng, g0 + sq_.split);
+  if (g1 <= g0) {  // no group of this sequence in the chunk
+    if (s == 0 && sq_.nparts == 0) decode_write_empty(a, b, kh);
+    return;
+  }
 
   const int bits = ((a.int2_mask >> kh) & 1ull) ? 2 : 4;
   const int head_off = 512 * (4 * kh - 2 * __popcll(a.int2_mask & ((1ull << kh) - 1ull)));
@@ -650,22 +704,19 @@ __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decod
   __syncthreads();
   if (cc == 0) L.rowv[rr] = make_float4(mrow, l, beta, 0.0f);
   __syncthreads();
-  const bool empty = g1 <= g0;
-  if (a.direct) {
+  if (sq_.nparts == 1) {  // the only state: O / l and L directly
 #pragma unroll
     for (int r = 0; r < GP; ++r) {
       if (r >= G) break;
       const float4 rv = L.rowv[r];
       const float f = rv.z / rv.y;
-      _Float16 h2[2] = {empty ? (_Float16)0.0f : (_Float16)(O[r][0] * f),
-                        empty ? (_Float16)0.0f : (_Float16)(O[r][1] * f)};
+      _Float16 h2[2] = {(_Float16)(O[r][0] * f), (_Float16)(O[r][1] * f)};
       reinterpret_cast<unsigned*>(a.o)[((long)b * a.Hq + kh * G + r) * 64 + lane] =
           __builtin_bit_cast(unsigned, h2);
     }
     if (a.lse && cc == 0 && rr < G)
-      a.lse[(long)b * a.Hq + kh * G + rr] = empty ? -INFINITY : mrow + logf(l);
+      a.lse[(long)b * a.Hq + kh * G + rr] = mrow + logf(l);
   } else {
-    if (empty) return;  // chunk beyond this sequence: never read by the merge
 #pragma unroll
     for (int r = 0; r < GP; ++r) {
       if (r >= G) break;
@@ -681,72 +732,61 @@ __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decod
   }
 }
 
-// Merge of the chunk states of one (b, query head): lane handles channels
-// 2*lane, 2*lane + 1.
+// Merge of the chunk states of one (b, query head) with more than one state
+// (split-KV extension): m* = max m_s, w_s = SAS(m_s - m*) (exactly 1 for
+// m_s = m*), O = sum w_s O_s / sum w_s l_s, L = m* + ln sum w_s l_s, chunks
+// in ascending order (the buffer's state last).  A separate launch: the
+// kernel boundary makes every chunk's state visible across the XCDs' L2
+// caches.  Lane L handles channels 2L, 2L + 1.
 __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
   __shared__ float lut[8];
   __shared__ float cwt[64], cl[64];  // merge weights and l of up to 64 chunks
   const int lane = threadIdx.x;
-  if (lane < 8) lut[lane] = kLut[lane];
-  __syncthreads();
   const int bh = blockIdx.x;
   const int b = bh / a.Hq;
-  int ng = a.seq_lens[b] / 64;
-  ng = min(max(ng, 0), a.max_groups);
-  // group chunks, then the buffer's chunk when there is one
-  const int nt = a.tk ? min(max(a.seq_lens[b] - 64 * ng, 0), 63) : 0;
-  const int ns = (ng + a.split - 1) / a.split + (nt > 0);
+  const int ns = decode_seq(a, b).nparts;
+  if (ns < 2) return;  // written by the decode launch itself
+  if (lane < 8) lut[lane] = kLut[lane];
   const float* w = a.ws + (long)bh * a.nws * kWsStride;
-  float o0 = 0.0f, o1 = 0.0f, L = -INFINITY;
-  if (ns == 1) {
-    const float l = w[1];
-    o0 = w[kWsO + 2 * lane] / l;
-    o1 = w[kWsO + 1 + 2 * lane] / l;
-    L = w[0] + logf(l);
-  } else if (ns > 1) {
-    // m* over the chunks, lane s reading chunk s (and s + 64, ...)
-    float mstar = -INFINITY;
-    for (int s = lane; s < ns; s += 64) mstar = fmaxf(mstar, w[(long)s * kWsStride]);
-    mstar = wave_max(mstar);
-    // ascending accumulation of w_s l_s and w_s O_s; the weights of 64 chunks
-    // at a time go through LDS and four chunks' O loads are in flight at once
-    float den = 0.0f, n0 = 0.0f, n1 = 0.0f;
-    for (int s0 = 0; s0 < ns; s0 += 64) {
-      const int cnt = min(64, ns - s0);
-      __syncthreads();
-      if (lane < cnt) {
-        const float* ws = w + (long)(s0 + lane) * kWsStride;
-        cwt[lane] = sas_y(mstar - ws[0], lut);
-        cl[lane] = ws[1];
-      }
-      __syncthreads();
-      const float* wo = w + (long)s0 * kWsStride + kWsO + 2 * lane;
-      int t = 0;
-      for (; t + 4 <= cnt; t += 4) {
-        float2 x[4];
+  // m* over the chunks, lane s reading chunk s (and s + 64, ...)
+  float mstar = -INFINITY;
+  for (int s = lane; s < ns; s += 64) mstar = fmaxf(mstar, w[(long)s * kWsStride]);
+  mstar = wave_max(mstar);
+  // ascending accumulation of w_s l_s and w_s O_s; the weights of 64 chunks
+  // at a time go through LDS and four chunks' O loads are in flight at once
+  float den = 0.0f, n0 = 0.0f, n1 = 0.0f;
+  for (int s0 = 0; s0 < ns; s0 += 64) {
+    const int cnt = min(64, ns - s0);
+    __syncthreads();
+    if (lane < cnt) {
+      const float* ws = w + (long)(s0 + lane) * kWsStride;
+      cwt[lane] = ws[0] < mstar ? sas_y(mstar - ws[0], lut) : 1.0f;  // e^0 for m_s = m*
+      cl[lane] = ws[1];
+    }
+    __syncthreads();
+    const float* wo = w + (long)s0 * kWsStride + kWsO + 2 * lane;
+    int t = 0;
+    for (; t + 4 <= cnt; t += 4) {
+      float2 x[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) x[u] = *reinterpret_cast<const float2*>(wo + (t + u) * kWsStride);
+      for (int u = 0; u < 4; ++u) x[u] = *reinterpret_cast<const float2*>(wo + (t + u) * kWsStride);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          den = __builtin_fmaf(cwt[t + u], cl[t + u], den);
-          n0 = __builtin_fmaf(cwt[t + u], x[u].x, n0);
-          n1 = __builtin_fmaf(cwt[t + u], x[u].y, n1);
-        }
-      }
-      for (; t < cnt; ++t) {
-        const float2 x = *reinterpret_cast<const float2*>(wo + t * kWsStride);
-        den = __builtin_fmaf(cwt[t], cl[t], den);
-        n0 = __builtin_fmaf(cwt[t], x.x, n0);
-        n1 = __builtin_fmaf(cwt[t], x.y, n1);
+      for (int u = 0; u < 4; ++u) {
+        den = __builtin_fmaf(cwt[t + u], cl[t + u], den);
+        n0 = __builtin_fmaf(cwt[t + u], x[u].x, n0);
+        n1 = __builtin_fmaf(cwt[t + u], x[u].y, n1);
       }
     }
-    o0 = n0 / den;
-    o1 = n1 / den;
-    L = mstar + logf(den);
+    for (; t < cnt; ++t) {
+      const float2 x = *reinterpret_cast<const float2*>(wo + t * kWsStride);
+      den = __builtin_fmaf(cwt[t], cl[t], den);
+      n0 = __builtin_fmaf(cwt[t], x.x, n0);
+      n1 = __builtin_fmaf(cwt[t], x.y, n1);
+    }
   }
-  _Float16 h2[2] = {(_Float16)o0, (_Float16)o1};
+  _Float16 h2[2] = {(_Float16)(n0 / den), (_Float16)(n1 / den)};
   reinterpret_cast<unsigned*>(a.o)[(long)bh * 64 + lane] = __builtin_bit_cast(unsigned, h2);
-  if (a.lse && lane == 0) a.lse[bh] = L;
+  if (a.lse && lane == 0) a.lse[bh] = mstar + logf(den);
 }
 
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
@@ -771,7 +811,7 @@ hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
     }
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.direct) return e;
+  if (e != hipSuccess || a.nws < 2) return e;  // no sequence has two states to merge
   hipLaunchKernelGGL(k_decode_combine, dim3(a.B * a.Hq), dim3(64), 0, stream, a);
   return hipGetLastError();
 }

@@ -15,7 +15,7 @@
 // (once for Q, once per tile for P).  32 queries per wave keep a wave under
 // 256 VGPRs (two waves per SIMD, MFMA results in VGPRs).  With B_r = 128 the
 // first waves of a diagonal block see no key of its last tile; their rows
-// keep m and l unchanged there (factor 1, not SAS(0)).
+// keep m and l unchanged there.
 //
 // Register layout.  The scores are computed transposed, S^T = K Q^T, so that
 // each lane holds one query column:  for the 32x32 output block kb (32-key
@@ -287,12 +287,11 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
         rs += p;
         pmax = fmaxf(pmax, p);
       }
-    float alpha = sas_y(mnew - mold, lut);  // 0 when mold = -inf
-    // with B_r > B_c a wave can see no key of the tile (its rows all precede
-    // it): the rows are not processed, so nothing is rescaled
-    if constexpr (kBr > kBc) {
-      if (a.causal && kBc * j > row0 + 31) alpha = 1.0f;
-    }
+    // SAS(m_old - m_new), 0 when m_old = -inf, and exactly 1 (e^0) for a row
+    // whose maximum did not move.  A row that sees no key of the tile (with
+    // B_r > B_c its keys can all follow the row) has only -inf scores, keeps
+    // its maximum and adds nothing: it is left as it is.
+    const float alpha = mnew > mold ? sas_y(mnew - mold, lut) : 1.0f;
     lhalf = alpha * lhalf + rs;
     mrow = mnew;
     // ---- tile maximum of P~ over the waves -----------------------------
@@ -582,7 +581,7 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
   for (int cb = 0; cb < 8; ++cb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) O[cb][r] = 0.0f;
-  float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
+  float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f, rbeta = 1.0f;  // rbeta ~ 1 / beta
   // 119 / pmax of the last tile that computed it, as wave-uniform bits
   unsigned pmax_prev = 0xffffffffu, inv_prev = 0u;
   float skj = skp[0], svj = svp[0];
@@ -658,18 +657,16 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
         rs = (mb | r) ? rs + p : p;
         pmax = (mb | r) ? fmaxf(pmax, p) : p;
       }
-    // SAS(m_old - m_new); 0 when m_old = -inf.  When no row of the wave moved
-    // its maximum the argument is 0 in every lane (rows past N, which see no
-    // key, also take this branch: they are never written) and SAS(0) is
-    // LUT[0] * POLY(0) = c0 exactly -- the common case away from the diagonal.
-    float alpha = kC0;
-    if (__builtin_amdgcn_ballot_w64(mnew > mold) != 0) alpha = sas_y(mnew - mold, L.lut);
-    // with B_r = 128 a wave can see no key of the tile (its rows all precede
-    // it): the rows are not processed, so nothing is rescaled (factor 1)
-    if constexpr (kW > 4) {
-      if (a.causal && 64 * j > row0 + 15) alpha = 1.0f;
-    }
-    lpart = alpha * lpart + rs;
+    // Rescale by SAS(m_old - m_new): 0 when m_old = -inf, exactly 1 (e^0)
+    // for a row whose maximum did not move.  When no row of the wave moved
+    // its maximum -- the common case away from the diagonal -- l, beta and
+    // the accumulator stay as they are (wave-uniform branch).  Rows that see
+    // no key of the tile (past N, or with B_r = 128 all before its keys) have
+    // only -inf scores, keep their maximum and add nothing.
+    const bool moved = __builtin_amdgcn_ballot_w64(mnew > mold) != 0;
+    float alpha = 1.0f;
+    if (moved) alpha = mnew > mold ? sas_y(mnew - mold, L.lut) : 1.0f;
+    lpart = moved ? alpha * lpart + rs : lpart + rs;
     mrow = mnew;
     // ---- tile maximum of P~ over the four waves ------------------------
     pmax = wave_max_pos(pmax);  // P~ >= 0
@@ -682,15 +679,18 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
       pmax = __int_as_float(pm);
     }
     // ---- rescale factor: O = beta * Ost --------------------------------
-    float nbeta = beta * alpha;
-    if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
+    if (moved) {
+      float nbeta = beta * alpha;
+      if (__builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0) {  // rare: renormalize
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb)
+        for (int cb = 0; cb < 8; ++cb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) O[cb][r] *= nbeta;
-      nbeta = 1.0f;
+          for (int r = 0; r < 4; ++r) O[cb][r] *= nbeta;
+        nbeta = 1.0f;
+      }
+      beta = nbeta;
+      rbeta = __builtin_amdgcn_rcpf(beta);
     }
-    beta = nbeta;
     // ---- Q(P~) with scale pmax/119 over the 64 x 64 tile ----------------
     // tile-uniform (scalar registers); the same pmax as the last tile (often
     // SAS(0), when a row sets its maximum in the tile) reuses the quotient
@@ -704,7 +704,7 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     // s_P = pmax / 119 only scales O (no code depends on it): the product
     // with the rounded reciprocal is within one ulp of the quotient; the
     // factor 2^26 undoes the accumulator seed
-    const float g26 = ((pmax * (0x1p26f / kQmax)) * svj) * __builtin_amdgcn_rcpf(beta);
+    const float g26 = ((pmax * (0x1p26f / kQmax)) * svj) * rbeta;
     v4i pop;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)

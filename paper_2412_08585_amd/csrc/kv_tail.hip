@@ -191,7 +191,8 @@ hipError_t launch_append_kv(const AppendArgs& a, int B, hipStream_t stream) {
 // buffer holds at most 63 tokens, so the integer products run on the VALU
 // (v_dot4): lane t scores token t, then lane L accumulates channels 2L, 2L+1.
 // The result is the buffer's chunk state (m, l, O) in workspace slot
-// ceil(ng / split), merged by k_decode_combine.  It runs as the last B * Hkv
+// nchunk (after the group chunks), merged by k_decode_combine like the
+// others (or written as the output when the sequence has no cached group).  It runs as the last B * Hkv
 // work-groups of the k_attn_decode launch (work-group index bx among them),
 // so it needs no launch of its own and fills the slots the group chunks
 // leave free at the end.
@@ -207,11 +208,10 @@ __device__ void decode_tail_body(const DecodeArgs& a, int bx) {
   if (lane < 8) lut[lane] = kLut[lane];
   const int b = bx / a.Hkv, kh = bx % a.Hkv;
   const int G = a.G;
-  int ng = a.seq_lens[b] / 64;
-  ng = min(max(ng, 0), a.max_groups);
-  const int nt = min(max(a.seq_lens[b] - 64 * ng, 0), 63);
+  const DecodeSeq sq_ = decode_seq(a, b);
+  const int ng = sq_.ng, nt = sq_.nt;
   if (nt == 0) return;
-  const int sslot = (ng + a.split - 1) / a.split;  // after the group chunks
+  const int sslot = sq_.nchunk;  // after the group chunks
   const long u = (long)b * a.Hkv + kh;
   const float sK = a.tscale[2 * u], sV = a.tscale[2 * u + 1];
   const int trow = kTrace && b == a.tr_b && kh == a.tr_h / G && a.tr_g == ng ? a.tr_h % G : -1;
@@ -304,12 +304,19 @@ __device__ void decode_tail_body(const DecodeArgs& a, int bx) {
       if (r == trow)
         reinterpret_cast<int2*>(a.trace + TURBO_TRACE_PV)[lane] = make_int2(acc0, acc1);
       const float4 rv = rowv[r];
-      float* w = a.ws + (((long)b * a.Hq + kh * G + r) * a.nws + sslot) * kWsStride;
-      *reinterpret_cast<float2*>(w + kWsO + 2 * lane) =
-          make_float2(rv.z * (float)acc0, rv.z * (float)acc1);
-      if (lane == 0) {
-        w[0] = rv.x;
-        w[1] = rv.y;
+      const long bh = (long)b * a.Hq + kh * G + r;
+      if (sq_.nparts == 1) {  // no cached group: the buffer's state is the result
+        _Float16 h2[2] = {(_Float16)(rv.z * (float)acc0 / rv.y), (_Float16)(rv.z * (float)acc1 / rv.y)};
+        reinterpret_cast<unsigned*>(a.o)[bh * 64 + lane] = __builtin_bit_cast(unsigned, h2);
+        if (a.lse && lane == 0) a.lse[bh] = rv.x + logf(rv.y);
+      } else {
+        float* w = a.ws + (bh * a.nws + sslot) * kWsStride;
+        *reinterpret_cast<float2*>(w + kWsO + 2 * lane) =
+            make_float2(rv.z * (float)acc0, rv.z * (float)acc1);
+        if (lane == 0) {
+          w[0] = rv.x;
+          w[1] = rv.y;
+        }
       }
     }
   }

@@ -280,6 +280,8 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
                            tj, stream);
 }
 
+int turbo_decode_default_split(int ng) { return turbo::decode_default_split(ng); }
+
 int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq) {
   if (B < 1 || Hq < 1 || Hkv < 1 || max_groups_per_seq < 1) return 1;
   // One wave per (sequence, KV head, chunk).  The decode kernel holds three
@@ -306,9 +308,8 @@ int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq) {
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
                                     int kv_split_groups, int with_tail) {
   if (B < 1 || Hq < 1 || Hkv < 1 || max_groups_per_seq < 1 || kv_split_groups < 0) return 0;
-  const int split = kv_split_groups ? kv_split_groups
-                                    : turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq);
-  const long nws = (max_groups_per_seq + split - 1) / split + (with_tail ? 1 : 0);
+  const long nws = turbo::decode_max_chunks(max_groups_per_seq, kv_split_groups) +
+                   (with_tail ? 1 : 0);
   if (nws <= 1) return 0;
   return (size_t)B * Hq * nws * turbo::kWsStride * sizeof(float);
 }
@@ -340,12 +341,10 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache,
   if (st != TURBO_OK) return st;
   st = check_tail(tail, B, Hkv);
   if (st != TURBO_OK) return st;
-  const int split = kv_split_groups ? kv_split_groups
-                                    : turbo_decode_auto_split(B, Hq, Hkv, max_groups_per_seq);
-  const long nsplit = (max_groups_per_seq + split - 1) / split;
+  const long nsplit = turbo::decode_max_chunks(max_groups_per_seq, kv_split_groups);
   if ((long)B * Hkv * (nsplit + (tail ? 1 : 0)) > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
-  const size_t need =
-      turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups_per_seq, split, tail != nullptr);
+  const size_t need = turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups_per_seq,
+                                                   kv_split_groups, tail != nullptr);
   if (need > 0 && (!workspace || workspace_bytes < need)) return TURBO_ERR_WORKSPACE_TOO_SMALL;
   st = check_device();
   if (st != TURBO_OK) return st;
@@ -366,10 +365,9 @@ static int attn_decode_impl(const void* q, const turbo_kv_cache* cache,
   a.Hkv = Hkv;
   a.G = Hq / Hkv;
   a.sm_scale = sm_scale;
-  a.split = split;
+  a.split = kv_split_groups;
   a.nsplit = (int)nsplit;
   a.nws = (int)nsplit + (tail ? 1 : 0);
-  a.direct = a.nws == 1;
   a.ws = static_cast<float*>(workspace);
   if (tail) {
     a.tk = tail->k;

@@ -19,6 +19,7 @@ import pytest
 import torch
 
 from tests import cache_layout
+from tests.decode_split import oracle_decode, split_of
 
 pytestmark = pytest.mark.gpu
 
@@ -257,6 +258,10 @@ DECODE_CASES = [
     (1, 16, 1, 64 * 8, [4], [512], 3),
     (2, 16, 2, 64 * 6, [2, 4], [384, 250], 2),   # 8 query heads per KV head
     (2, 2, 1, 64 * 5, [2], [320, 128], 100),
+    # default chunking: 4 chunks of 35 groups and 2 chunks of 32 (merged in
+    # the decode launch); many chunks of one group
+    (2, 8, 2, 64 * 140, [4, 2], [64 * 140, 64 * 50 + 10], 0),
+    (1, 4, 1, 64 * 12, [4], [64 * 12], 1),
 ]
 
 
@@ -273,10 +278,45 @@ def test_decode_parity(orc, ta, dev, B, Hq, Hkv, Nc, bits, sl, split):
                                   return_lse=True)
     torch.cuda.synchronize()
     ref = orc.quantize_kv(k, v, bits)
-    used = ta.decode_split(B, Hq, Hkv, Nc // 64, split)
-    ro, rl = orc.attn_decode(q, ref, sl, 1 / np.sqrt(128), split=used)
+    ro, rl = oracle_decode(orc, q, ref, sl, 1 / np.sqrt(128), split, Nc // 64)
     _cmp_o(o, ro, "decode O")
     _cmp_lse(lse, rl, "decode lse")
+
+
+def test_decode_result_does_not_depend_on_the_batch(orc, ta, dev):
+    """With kv_split_groups = 0 the chunking follows each sequence's own group
+    count, so a sequence decoded on its own (with tables cut to its groups,
+    hence another grid) gives the same O and L bit for bit as inside a batch
+    of 64 sequences of other lengths; and both equal the oracle with that
+    sequence's chunk length."""
+    B, Hq, Hkv, mg = 64, 8, 2, 40
+    rng = np.random.default_rng(77)
+    sl = [int(x) for x in rng.integers(64 * 3, 64 * mg + 1, size=B)]
+    sl[5], sl[6], sl[7] = 64 * mg, 64 * 33, 64 * 32 + 63   # 2, 2 and 1 chunks
+    _log(f"decode batch independence B={B} Hq={Hq} Hkv={Hkv} seq={sl[:8]}...")
+    k = _rand((B, Hkv, 64 * mg, 128), 1901)
+    v = _rand((B, Hkv, 64 * mg, 128), 1902)
+    k[..., 5] *= 10
+    q = _rand((B, Hq, 128), 1903)
+    bits = [4, 2]
+    _, cache, bt, gt, btd, gtd = _quantize(ta, dev, k, v, bits, seed=19)
+    sld = torch.tensor(sl, dtype=torch.int32, device=dev)
+    o, lse = ta.turbo_attn_decode(q.to(dev), cache, sld, btd, gtd, 1 / np.sqrt(128), 0,
+                                  return_lse=True)
+    torch.cuda.synchronize()
+    for b in (5, 6, 7, 11, 40):
+        ng = sl[b] // 64
+        o1, l1 = ta.turbo_attn_decode(q[b:b + 1].to(dev), cache, sld[b:b + 1],
+                                      btd[b:b + 1, :4 * ng].contiguous(),
+                                      gtd[b:b + 1, :ng].contiguous(), 1 / np.sqrt(128), 0,
+                                      return_lse=True)
+        torch.cuda.synchronize()
+        assert torch.equal(o1.view(torch.int16), o[b:b + 1].view(torch.int16)), b
+        assert torch.equal(l1.view(torch.int32), lse[b:b + 1].view(torch.int32)), b
+    ref = orc.quantize_kv(k[[5, 6, 7]], v[[5, 6, 7]], bits)
+    ro, rl = oracle_decode(orc, q[[5, 6, 7]], ref, [sl[5], sl[6], sl[7]], 1 / np.sqrt(128), 0)
+    _cmp_o(o[[5, 6, 7]], ro, "decode O (default chunking)")
+    _cmp_lse(lse[[5, 6, 7]], rl, "decode lse (default chunking)")
 
 
 def test_decode_rows_with_empty_groups(orc, ta, dev):
@@ -476,7 +516,7 @@ def test_full_size_decode(orc, ta, dev, name):
     sl = torch.full((w.B,), w.N, dtype=torch.int32, device=dev)
     o, lse = ta.turbo_attn_decode(q, cache, sl, btd, gtd, w.sm_scale, 0, return_lse=True)
     torch.cuda.synchronize()
-    split = ta.decode_split(w.B, w.Hq, w.Hkv, w.max_groups, 0)
+    split = split_of(w.N, 0, w.max_groups)
     pages = cache.pages.cpu().numpy()
     gmeta = cache.group_meta.cpu().numpy()
     gscale = cache.group_scale.cpu().numpy()

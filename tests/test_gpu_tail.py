@@ -15,6 +15,7 @@ import pytest
 import torch
 
 from tests import cache_layout
+from tests.decode_split import oracle_decode, split_of
 
 pytestmark = pytest.mark.gpu
 
@@ -204,8 +205,7 @@ def test_decode_with_buffer_parity(orc, ta, dev, B, Hq, Hkv, N, mg, bits, extra,
     o, lse = ta.turbo_attn_decode(q.to(dev), s.cache, sld, s.btd, s.gtd, SM, split,
                                   return_lse=True, tail=s.tail)
     torch.cuda.synchronize()
-    used = ta.decode_split(B, Hq, Hkv, mg, split)
-    ro, rl = orc.attn_decode(q, s.rcache, seq, SM, split=used, tail=s.rtail)
+    ro, rl = oracle_decode(orc, q, s.rcache, seq, SM, split, mg, tail=s.rtail)
     _cmp_o(o, ro, "decode+buffer O")
     _cmp_lse(lse, rl, "decode+buffer lse")
     # the buffer's chunk, bit for bit, for one query row of each sequence
@@ -215,7 +215,8 @@ def test_decode_with_buffer_parity(orc, ta, dev, B, Hq, Hkv, N, mg, bits, extra,
         o2, g = ta.turbo_attn_decode_trace(q.to(dev), s.cache, sld, s.btd, s.gtd, (b, h, ng), SM,
                                            split, tail=s.tail)
         assert torch.equal(o2.view(torch.int16), o.view(torch.int16))
-        _, _, r = orc.attn_decode(q, s.rcache, seq, SM, split=used, tail=s.rtail,
+        _, _, r = orc.attn_decode(q, s.rcache, seq, SM, split=split_of(seq[b], split, mg),
+                                  tail=s.rtail,
                                   trace=(b, h, ng))
         if not r["hit"]:  # empty buffer: nothing traced on either side
             assert not any(np.asarray(x).any() for x in g.values())

@@ -12,6 +12,8 @@ import numpy as np
 import pytest
 import torch
 
+from tests.decode_split import split_of
+
 pytestmark = pytest.mark.gpu
 
 
@@ -99,6 +101,11 @@ DECODE_TRACE_CASES = [
     (3, 8, 2, 64 * 6, [4, 2], [384, 200, 0], 2, [(0, 1, 0), (0, 5, 4), (1, 6, 2), (1, 2, 3)]),
     (2, 4, 4, 64 * 4, [2, 4, 4, 2], [256, 256], 1, [(1, 0, 3), (0, 2, 1)]),
     (1, 16, 1, 64 * 8, [4], [512], 3, [(0, 13, 5), (0, 0, 7)]),
+    # two and eight query heads per KV head (the GP = 2 and GP = 8 instances)
+    (2, 4, 2, 64 * 5, [2, 4], [320, 192], 2, [(0, 1, 4), (1, 2, 2), (0, 3, 0)]),
+    (2, 16, 2, 64 * 5, [4, 2], [320, 256], 0, [(0, 7, 3), (1, 12, 1), (1, 9, 3)]),
+    # the default chunking with one sequence long enough for several chunks
+    (1, 8, 2, 64 * 40, [4, 2], [64 * 40], 0, [(0, 2, 35), (0, 6, 3)]),
 ]
 
 
@@ -124,7 +131,8 @@ def test_decode_group_integers_bit_exact(orc, ta, dev, B, Hq, Hkv, Nc, bits, sl,
         _log(f"decode trace B={B} Hq={Hq} Hkv={Hkv} bits={bits} split={split} group={(b, h, gi)}")
         o, g = ta.turbo_attn_decode_trace(q.to(dev), cache, sld, btd, gtd, (b, h, gi), sm, split)
         assert torch.equal(o.view(torch.int16), o_plain.view(torch.int16))
-        _, _, r = orc.attn_decode(q, ref, sl, sm, split=split, trace=(b, h, gi))
+        _, _, r = orc.attn_decode(q, ref, sl, sm, split=split_of(sl[b], split, mg),
+                                  trace=(b, h, gi))
         if not r["hit"]:  # group beyond the sequence: nothing traced on either side
             assert not any(np.asarray(x).any() for x in g.values())
             continue

@@ -43,7 +43,7 @@ def test_exports_every_declared_function(ta):
 
 def test_version_and_strerror(ta):
     L = ta.lib()
-    assert L.turbo_abi_version() == 3
+    assert L.turbo_abi_version() == 4
     for st in (0, -1, -2, -3, -4, 7):
         assert L.turbo_strerror(st)
 
@@ -224,10 +224,27 @@ def test_decode_split_and_workspace(ta):
     for B, Hq, Hkv, G in [(1, 8, 8, 256), (8, 32, 8, 128), (32, 16, 4, 300), (128, 16, 16, 64),
                           (3, 10, 5, 7), (2, 64, 4, 1000)]:
         assert L.turbo_decode_auto_split(B, Hq, Hkv, G) == brute(B, Hq, Hkv, G)
+    cnt = 0
     assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10, 0) == 0
-    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3, 0) == 4 * 8 * 4 * 132 * 4
-    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10, 1) == 4 * 8 * 2 * 132 * 4  # + buffer
-    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3, 1) == 4 * 8 * 5 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3, 0) == cnt + 4 * 8 * 4 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 10, 1) == cnt + 4 * 8 * 2 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 10, 3, 1) == cnt + 4 * 8 * 5 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(100, 8, 2, 10, 3, 0) == 100 * 8 * 4 * 132 * 4
+    # the default chunking (kv_split_groups = 0) follows each sequence's own
+    # group count: at most one chunk up to 32 groups, 4 chunks beyond 128
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 32, 0, 0) == 0
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 32, 0, 1) == cnt + 4 * 8 * 2 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 100, 0, 0) == cnt + 4 * 8 * 4 * 132 * 4
+    assert L.turbo_decode_workspace_bytes(4, 8, 2, 5000, 0, 1) == cnt + 4 * 8 * 5 * 132 * 4
+
+
+def test_default_decode_split_depends_on_the_sequence_only(ta):
+    from tests.decode_split import default_split
+    L = ta.lib()
+    for ng in list(range(0, 300)) + [511, 512, 513, 4096, 100000]:
+        assert L.turbo_decode_default_split(ng) == default_split(ng), ng
+        n = -(-max(ng, 1) // default_split(ng))
+        assert n <= 4 and (ng > 32 or n == 1)
 
 
 def test_step2_reciprocal_division_is_exact():
