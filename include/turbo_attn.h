@@ -363,6 +363,30 @@ int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const turbo_kv
                       size_t workspace_bytes, void* o, float* lse, hipStream_t stream);
 
 /*
+ * turbo_attn_decode_noalloc — turbo_attn_decode for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  Same arguments, kernels and results as
+ * turbo_attn_decode, without the workspace: the split-KV chunk states go to
+ * a fixed device array of TURBO_DECODE_SCRATCH_BYTES inside the library
+ * (one per GPU, held until the process ends; its address is looked up once
+ * per device on the first call there).  The call itself allocates nothing.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (other streams, other host threads) race and must be ordered by the
+ * caller.  Nothing in the array needs clearing: each call writes every chunk
+ * state before reading it.
+ * Errors as turbo_attn_decode, plus TURBO_ERR_WORKSPACE_TOO_SMALL (before
+ * any launch) when turbo_decode_workspace_bytes(B, Hq, Hkv,
+ * max_groups_per_seq, kv_split_groups, tail != NULL) exceeds
+ * TURBO_DECODE_SCRATCH_BYTES, e.g. B * Hq * chunks > 63550.
+ */
+#define TURBO_DECODE_SCRATCH_BYTES (32u << 20)
+int turbo_attn_decode_noalloc(const void* q, const turbo_kv_cache* cache,
+                              const turbo_kv_tail* tail, const int32_t* seq_lens,
+                              const int32_t* block_table, const int32_t* group_table,
+                              int max_groups_per_seq, int B, int Hq, float sm_scale,
+                              int kv_split_groups, void* o, float* lse, hipStream_t stream);
+
+/*
  * Test hook (not part of the method): turbo_attn_decode with the integers of
  * group tg of (sequence tb, query head th) written to `trace` (device,
  * TURBO_TRACE_BYTES, layout above; row 0 of each array is used):

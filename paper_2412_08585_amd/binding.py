@@ -53,6 +53,7 @@ def lib() -> ctypes.CDLL:
             "turbo_quantize_kv": ([P, P, I, I, I, I, P, P, P, P, P, P, P, I, P], I),
             "turbo_attn_prefill": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
             "turbo_attn_decode": ([P, P, P, P, P, P, I, I, I, F, I, P, Z, P, P, P], I),
+            "turbo_attn_decode_noalloc": ([P, P, P, P, P, P, I, I, I, F, I, P, P, P], I),
             "turbo_attn_prefill_trace": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, I, I, I, I, P,
                                           P], I),
             "turbo_attn_decode_trace": ([P, P, P, P, P, P, I, I, I, F, I, P, Z, P, P, I, I, I, P,
@@ -326,6 +327,32 @@ def turbo_attn_decode(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tens
                                  _ptr(lse), _stream(q.device))
     _check(st, "turbo_attn_decode")
     return (o, lse) if return_lse else o
+
+
+def turbo_attn_decode_noalloc(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tensor,
+                              block_table: torch.Tensor, group_table: torch.Tensor,
+                              sm_scale: Optional[float] = None, kv_split_groups: int = 0,
+                              return_lse: bool = False, out=None,
+                              tail: Optional[KVTail] = None, lse_out=None):
+    """turbo_attn_decode without a workspace: the library's fixed per-GPU
+    scratch holds the chunk states (no device allocation by the library;
+    pass `out` and `lse_out` to allocate nothing here either)."""
+    B, Hq, d = q.shape
+    mg = group_table.shape[1]
+    sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
+    o = torch.empty_like(q) if out is None else out
+    lse = lse_out
+    if return_lse and lse is None:
+        lse = torch.empty(B, Hq, dtype=torch.float32, device=q.device)
+    cs = cache.struct()
+    ts = tail.struct() if tail is not None else None
+    st = lib().turbo_attn_decode_noalloc(_ptr(q), ctypes.byref(cs),
+                                         ctypes.byref(ts) if ts is not None else None,
+                                         _ptr(seq_lens), _ptr(block_table), _ptr(group_table),
+                                         mg, B, Hq, sm, int(kv_split_groups), _ptr(o), _ptr(lse),
+                                         _stream(q.device))
+    _check(st, "turbo_attn_decode_noalloc")
+    return (o, lse) if (return_lse or lse_out is not None) else o
 
 
 def turbo_attn_decode_trace(q: torch.Tensor, cache: PagedKVCache, seq_lens: torch.Tensor,

@@ -38,6 +38,29 @@ int check_device() {
   return st == 1 ? TURBO_OK : TURBO_ERR_UNSUPPORTED;
 }
 
+// Scratch of turbo_attn_decode_noalloc: the split-KV chunk states live in a
+// file-scope device array instead of a caller workspace.  Each GPU the
+// library runs on holds its own copy until the process ends.  In host code
+// `scratch` is only a stand-in for the symbol; its device address comes from
+// hipGetSymbolAddress, once per device, and only that address is passed on.
+constexpr size_t kDecodeScratchBytes = size_t(32) << 20;  // TURBO_DECODE_SCRATCH_BYTES
+static_assert(kDecodeScratchBytes == TURBO_DECODE_SCRATCH_BYTES, "header and library agree");
+static __device__ __align__(256) unsigned char scratch[kDecodeScratchBytes];
+std::atomic<void*> g_scratch[kMaxDevices];
+
+// Device address of this device's scratch (nullptr on failure).  Written once
+// per device; concurrent first calls store the same address.
+void* decode_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    g_scratch[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
 int check_cache(const turbo_kv_cache* c, int Hkv, unsigned long long* int2_mask,
                 int* page_bytes) {
   if (!c || !c->pages || !c->group_meta || !c->group_scale) return TURBO_ERR_INVALID_ARG;
@@ -391,6 +414,30 @@ int turbo_attn_decode(const void* q, const turbo_kv_cache* cache, const turbo_kv
   return attn_decode_impl(q, cache, tail, seq_lens, block_table, group_table, max_groups_per_seq,
                           B, Hq, sm_scale, kv_split_groups, workspace, workspace_bytes, o, lse,
                           nullptr, -1, -1, -1, stream);
+}
+
+int turbo_attn_decode_noalloc(const void* q, const turbo_kv_cache* cache,
+                              const turbo_kv_tail* tail, const int32_t* seq_lens,
+                              const int32_t* block_table, const int32_t* group_table,
+                              int max_groups_per_seq, int B, int Hq, float sm_scale,
+                              int kv_split_groups, void* o, float* lse, hipStream_t stream) {
+  if (!cache || B < 0 || Hq < 1 || max_groups_per_seq < 1 || kv_split_groups < 0)
+    return TURBO_ERR_INVALID_ARG;
+  const int Hkv = cache->num_kv_heads;
+  if (Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || Hq % Hkv != 0) return TURBO_ERR_INVALID_ARG;
+  const size_t need = turbo_decode_workspace_bytes(B, Hq, Hkv, max_groups_per_seq,
+                                                   kv_split_groups, tail != nullptr);
+  if (need > kDecodeScratchBytes) return TURBO_ERR_WORKSPACE_TOO_SMALL;
+  void* ws = nullptr;
+  if (need > 0 && B > 0) {
+    const int st = check_device();  // before the symbol lookup on a foreign device
+    if (st != TURBO_OK) return st;
+    ws = decode_scratch();
+    if (!ws) return TURBO_ERR_HIP;
+  }
+  return attn_decode_impl(q, cache, tail, seq_lens, block_table, group_table, max_groups_per_seq,
+                          B, Hq, sm_scale, kv_split_groups, ws, ws ? kDecodeScratchBytes : 0, o,
+                          lse, nullptr, -1, -1, -1, stream);
 }
 
 int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache,
