@@ -52,14 +52,16 @@ extern "C" {
 #define TURBO_MAX_KV_HEADS 64
 #define TURBO_MAX_GQA 16         /* max query heads per KV head */
 
-/* Layout of the tile trace written by the *_trace test hooks (bytes): */
-#define TURBO_TRACE_Q8 0         /* int8  [64][128]  Q^{q1} rows of the block  */
-#define TURBO_TRACE_S 8192       /* int32 [64][64]   QK^T accumulators         */
-#define TURBO_TRACE_P 24576      /* int8  [64][64]   Q(P~) codes               */
-#define TURBO_TRACE_PV 28672     /* int32 [64][128]  PV accumulators           */
-#define TURBO_TRACE_SQ 61440     /* fp32             s_Q                       */
-#define TURBO_TRACE_PMAX 61444   /* fp32             max P~ behind the P scale */
-#define TURBO_TRACE_BYTES 61448
+/* Layout of the tile trace written by the *_trace test hooks (bytes), for a
+ * tile of B_r query rows and B_c keys (B_r, B_c <= 128; 64 x 64 for the
+ * default prefill, one row of 64 keys for decode): */
+#define TURBO_TRACE_Q8 0         /* int8  [B_r][128]  Q^{q1} rows of the block  */
+#define TURBO_TRACE_S 16384      /* int32 [B_r][B_c]  QK^T accumulators         */
+#define TURBO_TRACE_P 81920      /* int8  [B_r][B_c]  Q(P~) codes               */
+#define TURBO_TRACE_PV 98304     /* int32 [B_r][128]  PV accumulators           */
+#define TURBO_TRACE_SQ 163840    /* fp32              s_Q                       */
+#define TURBO_TRACE_PMAX 163844  /* fp32              max P~ behind the P scale */
+#define TURBO_TRACE_BYTES 163848
 
 typedef enum turbo_status {
   TURBO_OK = 0,
@@ -283,6 +285,20 @@ int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq,
                       const int32_t* group_table, int max_groups_per_seq, hipStream_t stream);
 
 /*
+ * Test hook (not part of the method): turbo_qkv_project that also writes the
+ * fp16 projection it quantizes, y fp16 [B][N][F] (F = (Hq + 2 Hkv) * 128,
+ * feature order of w's rows), so that its codes, scales and cache bytes can
+ * be checked bit for bit as FlashQ of that projection.  The same kernel
+ * source runs (an instance with the extra stores).  INVALID_ARG also when
+ * y is NULL.
+ */
+int turbo_qkv_project_trace(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv,
+                            int d, int8_t* q8, float* s_q, int8_t* k8, int8_t* v8, float* s_k,
+                            float* s_v, const turbo_kv_cache* cache, const int32_t* block_table,
+                            const int32_t* group_table, int max_groups_per_seq, void* y,
+                            hipStream_t stream);
+
+/*
  * Test hook (not part of the method): turbo_attn_prefill with the integers of
  * one (sequence tb, query head th, query block ti, key block tj) tile written
  * to `trace` (device, TURBO_TRACE_BYTES, layout above).  The same kernel runs;
@@ -301,6 +317,20 @@ int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
                              const float* s_k, const float* s_v, int B, int Hq, int Hkv, int N,
                              int d, float sm_scale, int causal, void* o, float* lse, int tb,
                              int th, int ti, int tj, void* trace, hipStream_t stream);
+
+/*
+ * Test hook (not part of the method): turbo_attn_prefill_blocks with the
+ * integers of one tile -- query block ti of block_rows rows, key block tj of
+ * block_cols keys -- written to `trace` as for turbo_attn_prefill_trace, with
+ * B_r = block_rows rows and row strides B_c = block_cols for S and P.  Rows of
+ * the tile that see no key of it (causal, B_r > B_c) store their products and
+ * Q(P~) = 0, PV = 0.  Errors as turbo_attn_prefill_trace.
+ */
+int turbo_attn_prefill_blocks_trace(const void* q, const int8_t* k8, const int8_t* v8,
+                                    const float* s_k, const float* s_v, int B, int Hq, int Hkv,
+                                    int N, int d, float sm_scale, int causal, int block_rows,
+                                    int block_cols, void* o, float* lse, int tb, int th, int ti,
+                                    int tj, void* trace, hipStream_t stream);
 
 /*
  * turbo_attn_decode — Algorithm 2 (TurboAttention decode): the new query of

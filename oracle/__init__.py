@@ -197,23 +197,27 @@ def quantize_kv_blocks(k, v, block_cols: int) -> dict:
     return out
 
 
-def qkv_project(x, w, Hq: int, Hkv: int, bits, d: int = 128) -> dict:
-    """The QKV projection followed by FlashQ (Sec. 5.2 folds the quantization
-    into this projection; Sec. 3.1 step 1 and step 2).
-
-    x: [B][N][D] hidden states, w: [(Hq + 2 Hkv) d][D] weights (fp16 values;
-    query heads, then key heads, then value heads).  Reading: each projection
-    output is the exact sum X W^T rounded to fp16 (the precision of the
-    unfused path's Q, K, V) before FlashQ.  The sum is a float64 matmul, exact
-    for the small-integer test inputs whose partial sums fit in 53 bits.
-
-    Returns the fp16 values q [B][Hq][N][d], k, v [B][Hkv][N][d]; the Q block
-    codes q8 [B][Hq][N][d] and scales sq [B][Hq][ceil(N/64)] (the prefill's
-    Q rule: one block per 64 rows of a head); and quantize_kv(k, v, bits)."""
+def project_exact(x, w):
+    """The QKV projection X W^T of fp16 values before any rounding, and
+    sum_i |x_i| |w_i| of every output (the scale of its summation error).
+    x [..., D], w [F][D]; float64 matmuls (a library primitive), whose own
+    error (below D 2^-53 of sum |x||w|) is negligible next to any fp32 sum.
+    Returns (y, yabs), float64 [..., F]."""
     x = np.asarray(x, dtype=np.float64)
     w = np.asarray(w, dtype=np.float64)
-    B, N, D = x.shape
-    y = (x.reshape(B * N, D) @ w.T).astype(np.float16).astype(np.float32)
+    return x @ w.T, np.abs(x) @ np.abs(w).T
+
+
+def flashq_of_projection(y, Hq: int, Hkv: int, bits, d: int = 128) -> dict:
+    """FlashQ applied to a projection y [B][N][(Hq + 2 Hkv) d] of fp16 values
+    (Sec. 5.2 folds the quantization into the projection; Sec. 3.1 steps 1
+    and 2): y splits into the query heads, key heads and value heads; Q gets
+    the prefill's rule (one int8 block per 64 rows of a head), K and V
+    quantize_kv(k, v, bits).  Returns q [B][Hq][N][d], k, v [B][Hkv][N][d]
+    (the fp16 values), q8 [B][Hq][N][d], sq [B][Hq][ceil(N/64)] and the
+    entries of quantize_kv."""
+    y = np.asarray(y, dtype=np.float32)
+    B, N, F = y.shape
     y = y.reshape(B, N, Hq + 2 * Hkv, d).transpose(0, 2, 1, 3)
     q = np.ascontiguousarray(y[:, :Hq])
     k = np.ascontiguousarray(y[:, Hq:Hq + Hkv])
@@ -227,11 +231,28 @@ def qkv_project(x, w, Hq: int, Hkv: int, bits, d: int = 128) -> dict:
     return out
 
 
-def _trace(d: int, sel):
+def qkv_project(x, w, Hq: int, Hkv: int, bits, d: int = 128) -> dict:
+    """The QKV projection followed by FlashQ (Sec. 5.2 folds the quantization
+    into this projection; Sec. 3.1 step 1 and step 2).
+
+    x: [B][N][D] hidden states, w: [(Hq + 2 Hkv) d][D] weights (fp16 values;
+    query heads, then key heads, then value heads).  Reading: each projection
+    output is the exact sum X W^T rounded to fp16 (the precision of the
+    unfused path's Q, K, V) before FlashQ.  The sum is a float64 matmul, exact
+    for the small-integer test inputs whose partial sums fit in 53 bits.
+    Returns flashq_of_projection of that fp16 projection."""
+    x = np.asarray(x, dtype=np.float64)
+    B, N, D = x.shape
+    y, _ = project_exact(x.reshape(B * N, D), w)
+    y = y.astype(np.float16).astype(np.float32).reshape(B, N, -1)
+    return flashq_of_projection(y, Hq, Hkv, bits, d)
+
+
+def _trace(d: int, sel, br: int = 64, bc: int = 64):
     if sel is None:
         return None, None
-    bufs = dict(q8=np.zeros((64, d), np.int8), sacc=np.zeros((64, 64), np.int32),
-                qp=np.zeros((64, 64), np.int8), pvacc=np.zeros((64, d), np.int32))
+    bufs = dict(q8=np.zeros((br, d), np.int8), sacc=np.zeros((br, bc), np.int32),
+                qp=np.zeros((br, bc), np.int8), pvacc=np.zeros((br, d), np.int32))
     b, h, i, j = sel
     tr = Trace(b, h, i, j, 0, _p(bufs["q8"]).value, _p(bufs["sacc"]).value, _p(bufs["qp"]).value,
                _p(bufs["pvacc"]).value, 0.0, 0.0)
@@ -243,7 +264,8 @@ def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = Tr
                  block_cols: int = 64):
     """Algorithm 1.  q [B][Hq][N][d], k, v [B][Hkv][N][d] (fp16 values).
     Returns (o float64 [B][Hq][N][d] = O/l before fp16 rounding, lse float64
-    [B][Hq][N]) and, with trace=(b, h, i, j), a dict of that tile's integers.
+    [B][Hq][N]) and, with trace=(b, h, i, j) (query block i of B_r rows, key
+    block j of B_c keys), a dict of that tile's integers.
     qblocks=(i0, i1) restricts the work to query blocks i0..i1-1 (other rows NaN).
     block_rows = B_r, block_cols = B_c (Table 3): the query block of the Q
     scale, the key block of the K/V scales and of each online step, and the
@@ -253,10 +275,9 @@ def attn_prefill(q, k, v, sm_scale: float, causal: bool = True, quant: bool = Tr
     Hkv = k.shape[1]
     o = np.full((B, Hq, N, d), np.nan, np.float64)
     lse = np.full((B, Hq, N), np.nan, np.float64)
-    tr, bufs = _trace(d, trace)
-    i0, i1 = (-1, -1) if qblocks is None else qblocks
     assert block_rows in (32, 64, 128) and block_cols in (32, 64, 128)
-    assert tr is None or block_rows == block_cols == 64
+    tr, bufs = _trace(d, trace, block_rows, block_cols)
+    i0, i1 = (-1, -1) if qblocks is None else qblocks
     lib().or_attn_prefill_blocks(_p(q), _p(k), _p(v), B, Hq, Hkv, N, d,
                                  float(np.float32(sm_scale)), int(causal),
                                  _Opts(int(quant), int(sas)), int(block_rows), int(block_cols),

@@ -251,12 +251,13 @@ typedef struct or_row {
 
 /* Optional trace of one tile, for checking another implementation's
  * integers bit for bit: prefill selects (b, h, i, j) = (batch, query head,
- * query block, key block); decode selects (b, h, j) = (batch, query head,
- * group) and ignores i.  Buffers are filled only for the selected tile:
- *   q8    int8  [64][d]  quantized query block (decode: row 0 only)
- *   sacc  int32 [64][64] QK^T accumulators (row r, key t) of visible pairs
- *   qp    int8  [64][64] Q(P~) (0 where not visible)
- *   pvacc int32 [64][d]  Q(P~) V^{q1} accumulators
+ * query block of B_r rows, key block of B_c keys); decode selects (b, h, j) =
+ * (batch, query head, group) and ignores i (B_r = 1, B_c = 64).  Buffers are
+ * filled only for the selected tile:
+ *   q8    int8  [B_r][d]   quantized query block (decode: row 0 only)
+ *   sacc  int32 [B_r][B_c] QK^T accumulators (row r, key t) of visible pairs
+ *   qp    int8  [B_r][B_c] Q(P~) (0 where not visible)
+ *   pvacc int32 [B_r][d]   Q(P~) V^{q1} accumulators
  *   sq    query block scale; pmax tile maximum of P~ (decode: of the row). */
 typedef struct or_trace {
   int b, h, i, j;
@@ -325,7 +326,7 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
       if (!act[r]) continue;
       for (int t = 0; t < nk; ++t) {
         qp[r * ldsc + t] = (int8_t)rint((double)p[r * ldsc + t] * (double)inv);
-        if (tr) tr->qp[r * OR_BS + t] = vis[r * ldsc + t] ? qp[r * ldsc + t] : 0;
+        if (tr) tr->qp[r * ldsc + t] = vis[r * ldsc + t] ? qp[r * ldsc + t] : 0;
       }
       for (int e = 0; e < d; ++e) {
         int32_t acc = 0;
@@ -364,14 +365,13 @@ static void or_tile(const or_opts* o, or_row* rows, int nr, int nk, const double
  * Block sizes (Table 3 varies them): Q is quantized per br rows of a head
  * (br = B_r in {32, 64, 128}); K and V are quantized per bc tokens (bc = B_c
  * in {32, 64, 128}), each online step covers bc keys and the P scale covers
- * the br x bc tile.  Query blocks i0..i1 count br-row blocks.  The trace is
- * produced for br = bc = 64 only. */
+ * the br x bc tile.  Query blocks i0..i1 count br-row blocks; the trace
+ * selects a (br-row block, bc-key block) tile. */
 void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int B, int Hq,
                             int Hkv, int N, int d, float sm_scale, int causal, or_opts opts,
                             int br, int bc, double* o, double* lse, or_trace* tr, int i0,
                             int i1) {
   const int G = Hq / Hkv, nb = (N + bc - 1) / bc, nbq = (N + br - 1) / br;
-  if (br != OR_BS || bc != OR_BS) tr = NULL; /* the trace layout is that of 64x64 tiles */
 #pragma omp parallel
   {
     int8_t* k8 = malloc((size_t)N * d + 1);
@@ -429,7 +429,7 @@ void or_attn_prefill_blocks(const float* q, const float* k, const float* v, int 
                   for (int e = 0; e < d; ++e)
                     acc += (int32_t)q8[(size_t)r * d + e] * (int32_t)k8[(size_t)(k0 + t) * d + e];
                   sc[r * bc + t] = (double)((float)acc * c);
-                  if (trq && tr->j == j) tr->sacc[r * OR_BS + t] = acc;
+                  if (trq && tr->j == j) tr->sacc[r * bc + t] = acc;
                 } else {
                   double acc = 0.0;
                   for (int e = 0; e < d; ++e)

@@ -20,7 +20,7 @@ PAGE_TOKENS = 16
 MAX_KV_HEADS = 64
 # tile trace layout of the *_trace test hooks (include/turbo_attn.h)
 TRACE_Q8, TRACE_S, TRACE_P, TRACE_PV, TRACE_SQ, TRACE_PMAX, TRACE_BYTES = (
-    0, 8192, 24576, 28672, 61440, 61444, 61448)
+    0, 16384, 81920, 98304, 163840, 163844, 163848)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libturboattn.so")
@@ -56,6 +56,8 @@ def lib() -> ctypes.CDLL:
             "turbo_attn_decode_noalloc": ([P, P, P, P, P, P, I, I, I, F, I, P, P, P], I),
             "turbo_attn_prefill_trace": ([P, P, P, P, P, I, I, I, I, I, F, I, P, P, I, I, I, I, P,
                                           P], I),
+            "turbo_attn_prefill_blocks_trace": ([P, P, P, P, P, I, I, I, I, I, F, I, I, I, P, P, I,
+                                                 I, I, I, P, P], I),
             "turbo_attn_decode_trace": ([P, P, P, P, P, P, I, I, I, F, I, P, Z, P, P, I, I, I, P,
                                          P], I),
             "turbo_tail_init": ([P, P, I, I, I, I, P, P, P, P], I),
@@ -68,6 +70,8 @@ def lib() -> ctypes.CDLL:
                                           I),
             "turbo_quantize_kv_blocks": ([P, P, I, I, I, I, I, P, P, P, P, P], I),
             "turbo_qkv_project": ([P, P, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P], I),
+            "turbo_qkv_project_trace": ([P, P, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P,
+                                         P], I),
             "turbo_decode_auto_split": ([I, I, I, I], I),
             "turbo_decode_default_split": ([I], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
@@ -255,32 +259,37 @@ def _trace_buffer(device) -> torch.Tensor:
     return torch.zeros(TRACE_BYTES, dtype=torch.uint8, device=device)
 
 
-def _trace_dict(buf: torch.Tensor) -> dict:
+def _trace_dict(buf: torch.Tensor, br: int = 64, bc: int = 64) -> dict:
+    """The trace of a B_r x B_c tile (layout TURBO_TRACE_* of the header)."""
     h = buf.cpu().numpy()
-    return dict(q8=h[TRACE_Q8:TRACE_S].view(np.int8).reshape(64, HEAD_DIM).copy(),
-                sacc=h[TRACE_S:TRACE_P].view(np.int32).reshape(64, 64).copy(),
-                qp=h[TRACE_P:TRACE_PV].view(np.int8).reshape(64, 64).copy(),
-                pvacc=h[TRACE_PV:TRACE_SQ].view(np.int32).reshape(64, HEAD_DIM).copy(),
+    return dict(q8=h[TRACE_Q8:TRACE_Q8 + br * HEAD_DIM].view(np.int8).reshape(br, HEAD_DIM).copy(),
+                sacc=h[TRACE_S:TRACE_S + 4 * br * bc].view(np.int32).reshape(br, bc).copy(),
+                qp=h[TRACE_P:TRACE_P + br * bc].view(np.int8).reshape(br, bc).copy(),
+                pvacc=h[TRACE_PV:TRACE_PV + 4 * br * HEAD_DIM].view(np.int32)
+                .reshape(br, HEAD_DIM).copy(),
                 sq=h[TRACE_SQ:TRACE_PMAX].view(np.float32)[0],
                 pmax=h[TRACE_PMAX:TRACE_BYTES].view(np.float32)[0])
 
 
 def turbo_attn_prefill_trace(q: torch.Tensor, k8, v8, s_k, s_v, tile, sm_scale=None,
-                             causal: bool = True):
-    """Test hook: turbo_attn_prefill that also returns the integers of tile
-    (b, h, i, j) as a dict of numpy arrays (q8, sacc, qp, pvacc, sq, pmax)."""
+                             causal: bool = True, block_rows: int = 64, block_cols: int = 64):
+    """Test hook: turbo_attn_prefill (turbo_attn_prefill_blocks for other
+    block sizes) that also returns the integers of tile (b, h, i, j) -- query
+    block i of block_rows rows, key block j of block_cols keys -- as a dict of
+    numpy arrays (q8, sacc, qp, pvacc, sq, pmax)."""
     B, Hq, N, d = q.shape
     Hkv = s_k.shape[1]
     sm = float(1.0 / np.sqrt(d)) if sm_scale is None else float(sm_scale)
     o = torch.empty_like(q)
     buf = _trace_buffer(q.device)
     b, h, i, j = tile
-    st = lib().turbo_attn_prefill_trace(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v), B, Hq,
-                                        Hkv, N, d, sm, int(bool(causal)), _ptr(o), None, b, h, i,
-                                        j, _ptr(buf), _stream(q.device))
-    _check(st, "turbo_attn_prefill_trace")
+    st = lib().turbo_attn_prefill_blocks_trace(_ptr(q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v),
+                                               B, Hq, Hkv, N, d, sm, int(bool(causal)),
+                                               int(block_rows), int(block_cols), _ptr(o), None,
+                                               b, h, i, j, _ptr(buf), _stream(q.device))
+    _check(st, "turbo_attn_prefill_blocks_trace")
     torch.cuda.synchronize(q.device)
-    return o, _trace_dict(buf)
+    return o, _trace_dict(buf, block_rows, block_cols)
 
 
 def decode_split(seq_len: int, kv_split_groups: int = 0) -> int:
@@ -418,10 +427,12 @@ def turbo_sas_softmax(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> to
 def turbo_qkv_project(x: torch.Tensor, w: torch.Tensor, Hq: int, Hkv: int,
                       cache: Optional[PagedKVCache] = None,
                       block_table: Optional[torch.Tensor] = None,
-                      group_table: Optional[torch.Tensor] = None, out=None):
+                      group_table: Optional[torch.Tensor] = None, out=None, y=None):
     """QKV projection with FlashQ fused (Sec. 5.2): x fp16 [B][N][D], w fp16
     [(Hq + 2 Hkv) 128][D].  Returns (q8, s_q, k8, v8, s_k, s_v) in the layouts
-    of include/turbo_attn.h; writes the full K/V groups into `cache`."""
+    of include/turbo_attn.h; writes the full K/V groups into `cache`.  With y
+    (fp16 [B][N][(Hq + 2 Hkv) 128]) the test hook turbo_qkv_project_trace runs
+    and also stores the fp16 projection there."""
     B, N, D = x.shape
     nb = (N + BLOCK - 1) // BLOCK
     dev = x.device
@@ -436,11 +447,14 @@ def turbo_qkv_project(x: torch.Tensor, w: torch.Tensor, Hq: int, Hkv: int,
         q8, s_q, k8, v8, s_k, s_v = out
     cs = cache.struct() if cache is not None else None
     mg = group_table.shape[1] if group_table is not None else 0
-    _check(lib().turbo_qkv_project(_ptr(x), _ptr(w), B, N, D, Hq, Hkv, HEAD_DIM, _ptr(q8),
-                                   _ptr(s_q), _ptr(k8), _ptr(v8), _ptr(s_k), _ptr(s_v),
-                                   ctypes.byref(cs) if cs is not None else None,
-                                   _ptr(block_table), _ptr(group_table), mg, _stream(dev)),
-           "turbo_qkv_project")
+    args = [_ptr(x), _ptr(w), B, N, D, Hq, Hkv, HEAD_DIM, _ptr(q8), _ptr(s_q), _ptr(k8), _ptr(v8),
+            _ptr(s_k), _ptr(s_v), ctypes.byref(cs) if cs is not None else None,
+            _ptr(block_table), _ptr(group_table), mg]
+    if y is None:
+        _check(lib().turbo_qkv_project(*args, _stream(dev)), "turbo_qkv_project")
+    else:
+        _check(lib().turbo_qkv_project_trace(*args, _ptr(y), _stream(dev)),
+               "turbo_qkv_project_trace")
     return q8, s_q, k8, v8, s_k, s_v
 
 

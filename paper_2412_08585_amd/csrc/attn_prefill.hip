@@ -155,7 +155,8 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
     }
   }
   // wave-uniform; a key block the loop never reaches traces nothing
-  const bool traced = kTrace && L == a.tr_L && a.tr_j <= (a.causal ? i : a.nb - 1);
+  const bool traced = kTrace && L == a.tr_L &&
+                      a.tr_j <= (a.causal ? min(a.nbc - 1, (kBr * i + kBr - 1) / kBc) : a.nbc - 1);
   if constexpr (kTrace) {
     if (traced) {
 #pragma unroll
@@ -243,7 +244,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
     const bool trace_tile = traced && j == a.tr_j;
     if constexpr (kTrace) {
       if (trace_tile) {
-        int* ts = reinterpret_cast<int*>(a.trace + TURBO_TRACE_S) + (32 * qh + n) * 64 + 16 * hf;
+        int* ts = reinterpret_cast<int*>(a.trace + TURBO_TRACE_S) + (32 * qh + n) * kBc + 16 * hf;
 #pragma unroll
         for (int kb = 0; kb < kKb; ++kb)
 #pragma unroll
@@ -291,7 +292,8 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
     // whose maximum did not move.  A row that sees no key of the tile (with
     // B_r > B_c its keys can all follow the row) has only -inf scores, keeps
     // its maximum and adds nothing: it is left as it is.
-    const float alpha = mnew > mold ? sas_y(mnew - mold, lut) : 1.0f;
+    float alpha = sas_y(mnew - mold, lut);
+    alpha = mnew > mold ? alpha : 1.0f;
     lhalf = alpha * lhalf + rs;
     mrow = mnew;
     // ---- tile maximum of P~ over the waves -----------------------------
@@ -331,7 +333,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_attn_prefill(PrefillArgs a) 
       if (trace_tile) {
 #pragma unroll
         for (int kb = 0; kb < kKb; ++kb)
-          *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_P + (32 * qh + n) * 64 + 32 * kb +
+          *reinterpret_cast<v4i*>(a.trace + TURBO_TRACE_P + (32 * qh + n) * kBc + 32 * kb +
                                   16 * hf) = pop[kb];
         if (tid == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
       }
@@ -785,34 +787,43 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
   }
 }
 
-template <int kWaves>
+template <bool kTrace, int kWaves>
 static void launch_bc(const PrefillArgs& a, int total, hipStream_t stream) {
   const dim3 grid(total), block(64 * kWaves);
   if (a.bc == 32)
-    hipLaunchKernelGGL((k_attn_prefill<false, false, kWaves, 32>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill<kTrace, false, kWaves, 32>), grid, block, 0, stream, a);
   else if (a.bc == 128)
-    hipLaunchKernelGGL((k_attn_prefill<false, false, kWaves, 128>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill<kTrace, false, kWaves, 128>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((k_attn_prefill<false, false, kWaves, 64>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((k_attn_prefill<kTrace, false, kWaves, 64>), grid, block, 0, stream, a);
+}
+
+// (B_r, B_c) = (64, 64) and (128, 64) run on the 16-row-wave kernel, the
+// other pairs on the 32-row-wave kernel; the test hook runs the same kernel
+// as the plain call (its trace instance).
+template <bool kTrace>
+static void launch_prefill(const PrefillArgs& a, hipStream_t stream) {
+  const int total = a.B * a.Hq * a.nbq;
+  if (a.waves == 2 && a.bc == 64)
+    hipLaunchKernelGGL((k_attn_prefill16<kTrace, false, 4>), dim3(total), dim3(256), 0, stream, a);
+  else if (a.waves == 4 && a.bc == 64)
+    hipLaunchKernelGGL((k_attn_prefill16<kTrace, false, 8>), dim3(total), dim3(512), 0, stream, a);
+  else if (a.waves == 1)
+    launch_bc<kTrace, 1>(a, total, stream);
+  else if (a.waves == 4)
+    launch_bc<kTrace, 4>(a, total, stream);
+  else
+    launch_bc<kTrace, 2>(a, total, stream);
 }
 
 hipError_t launch_attn_prefill(const PrefillArgs& a, hipStream_t stream) {
-  const int total = a.B * a.Hq * a.nbq;
-  const dim3 b16(256);
-  if (a.trace)  // test hook: B_r = B_c = 64 only
-    hipLaunchKernelGGL((k_attn_prefill16<true, false, 4>), dim3(total), b16, 0, stream, a);
-  else if (a.q8)  // B_r = B_c = 64 only
-    hipLaunchKernelGGL((k_attn_prefill16<false, true, 4>), dim3(total), b16, 0, stream, a);
-  else if (a.waves == 2 && a.bc == 64)
-    hipLaunchKernelGGL((k_attn_prefill16<false, false, 4>), dim3(total), b16, 0, stream, a);
-  else if (a.waves == 4 && a.bc == 64)  // (B_r, B_c) = (128, 64)
-    hipLaunchKernelGGL((k_attn_prefill16<false, false, 8>), dim3(total), dim3(512), 0, stream, a);
-  else if (a.waves == 1)
-    launch_bc<1>(a, total, stream);
-  else if (a.waves == 4)
-    launch_bc<4>(a, total, stream);
+  if (a.q8)  // B_r = B_c = 64 only
+    hipLaunchKernelGGL((k_attn_prefill16<false, true, 4>), dim3(a.B * a.Hq * a.nbq), dim3(256), 0,
+                       stream, a);
+  else if (a.trace)
+    launch_prefill<true>(a, stream);
   else
-    launch_bc<2>(a, total, stream);
+    launch_prefill<false>(a, stream);
   return hipGetLastError();
 }
 

@@ -49,6 +49,7 @@ struct QkvArgs {
   const int* block_table;  // [B][4*max_groups]
   const int* group_table;  // [B][max_groups]
   int max_groups;
+  _Float16* y;     // test hook: the fp16 projection [B][N][F] (null: not written)
 };
 
 constexpr int kProjThreads = 256;
@@ -90,6 +91,9 @@ __device__ __forceinline__ void qkv_tile(int x, int ntiles, int nheads, int& til
   tile = tl * 8 + k;
 }
 
+// kY = true only for the test hook that also stores the fp16 projection
+// (the production instance carries no such store).
+template <bool kY>
 __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
   __shared__ __align__(16) uint8_t lds[kQkvLds];
   __shared__ float sblk[4];
@@ -200,7 +204,12 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
         const int row = 32 * mb + 8 * (r >> 2) + 4 * h + (r & 3);
         const float y = (float)(_Float16)acc[mb][nb][r];
         acc[mb][nb][r] = y;
-        if (n0 + row < a.N) amax = fmaxf(amax, fabsf(y));
+        if (n0 + row < a.N) {
+          amax = fmaxf(amax, fabsf(y));
+          if constexpr (kY)
+            a.y[((long)b * a.N + n0 + row) * (long)(128 * nheads) + 128 * head + 32 * nb + m] =
+                (_Float16)y;
+        }
       }
   amax = wave_max_fast(amax);
   float s = 0.0f, inv = 0.0f;
@@ -299,7 +308,10 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
 
 hipError_t launch_qkv_project(const QkvArgs& a, hipStream_t stream) {
   const int total = a.B * a.ntile * (a.Hq + 2 * a.Hkv);
-  hipLaunchKernelGGL(k_qkv_project, dim3(total), dim3(kProjThreads), 0, stream, a);
+  if (a.y)
+    hipLaunchKernelGGL(k_qkv_project<true>, dim3(total), dim3(kProjThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(k_qkv_project<false>, dim3(total), dim3(kProjThreads), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -241,10 +241,11 @@ int turbo_attn_prefill_q8(const int8_t* q8, const float* s_q, const int8_t* k8, 
                            causal, 64, 64, o, lse, nullptr, -1, -1, stream);
 }
 
-int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv, int d,
-                      int8_t* q8, float* s_q, int8_t* k8, int8_t* v8, float* s_k, float* s_v,
-                      const turbo_kv_cache* cache, const int32_t* block_table,
-                      const int32_t* group_table, int max_groups_per_seq, hipStream_t stream) {
+static int qkv_project_impl(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv,
+                            int d, int8_t* q8, float* s_q, int8_t* k8, int8_t* v8, float* s_k,
+                            float* s_v, const turbo_kv_cache* cache, const int32_t* block_table,
+                            const int32_t* group_table, int max_groups_per_seq, void* y,
+                            hipStream_t stream) {
   if (B < 0 || N < 0 || D < 64 || D % 64 != 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || Hq < 1 ||
       Hq % Hkv != 0 || d != TURBO_HEAD_DIM)
     return TURBO_ERR_INVALID_ARG;
@@ -285,22 +286,53 @@ int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq,
   a.v8 = v8;
   a.sk = s_k;
   a.sv = s_v;
+  a.y = static_cast<_Float16*>(y);
   return turbo::launch_qkv_project(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_qkv_project(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv, int d,
+                      int8_t* q8, float* s_q, int8_t* k8, int8_t* v8, float* s_k, float* s_v,
+                      const turbo_kv_cache* cache, const int32_t* block_table,
+                      const int32_t* group_table, int max_groups_per_seq, hipStream_t stream) {
+  return qkv_project_impl(x, w, B, N, D, Hq, Hkv, d, q8, s_q, k8, v8, s_k, s_v, cache,
+                          block_table, group_table, max_groups_per_seq, nullptr, stream);
+}
+
+int turbo_qkv_project_trace(const void* x, const void* w, int B, int N, int D, int Hq, int Hkv,
+                            int d, int8_t* q8, float* s_q, int8_t* k8, int8_t* v8, float* s_k,
+                            float* s_v, const turbo_kv_cache* cache, const int32_t* block_table,
+                            const int32_t* group_table, int max_groups_per_seq, void* y,
+                            hipStream_t stream) {
+  if (B > 0 && N > 0 && !y) return TURBO_ERR_INVALID_ARG;
+  return qkv_project_impl(x, w, B, N, D, Hq, Hkv, d, q8, s_q, k8, v8, s_k, s_v, cache,
+                          block_table, group_table, max_groups_per_seq, y, stream);
+}
+
+int turbo_attn_prefill_blocks_trace(const void* q, const int8_t* k8, const int8_t* v8,
+                                    const float* s_k, const float* s_v, int B, int Hq, int Hkv,
+                                    int N, int d, float sm_scale, int causal, int block_rows,
+                                    int block_cols, void* o, float* lse, int tb, int th, int ti,
+                                    int tj, void* trace, hipStream_t stream) {
+  if (block_rows != 32 && block_rows != 64 && block_rows != 128) return TURBO_ERR_INVALID_ARG;
+  if (block_cols != 32 && block_cols != 64 && block_cols != 128) return TURBO_ERR_INVALID_ARG;
+  const int nbq = N > 0 ? (N + block_rows - 1) / block_rows : 0;
+  const int nbc = N > 0 ? (N + block_cols - 1) / block_cols : 0;
+  if (!trace || tb < 0 || tb >= B || th < 0 || th >= Hq || ti < 0 || ti >= nbq || tj < 0 ||
+      tj >= nbc)
+    return TURBO_ERR_INVALID_ARG;
+  // logical work index of (tb, th, ti): longest query blocks first
+  const int tr_L = (nbq - 1 - ti) * B * Hq + tb * Hq + th;
+  return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
+                           causal, block_rows, block_cols, o, lse,
+                           static_cast<unsigned char*>(trace), tr_L, tj, stream);
 }
 
 int turbo_attn_prefill_trace(const void* q, const int8_t* k8, const int8_t* v8,
                              const float* s_k, const float* s_v, int B, int Hq, int Hkv, int N,
                              int d, float sm_scale, int causal, void* o, float* lse, int tb,
                              int th, int ti, int tj, void* trace, hipStream_t stream) {
-  const int nb = N > 0 ? (N + TURBO_BLOCK - 1) / TURBO_BLOCK : 0;
-  if (!trace || tb < 0 || tb >= B || th < 0 || th >= Hq || ti < 0 || ti >= nb || tj < 0 ||
-      tj >= nb)
-    return TURBO_ERR_INVALID_ARG;
-  // logical work index of (tb, th, ti): longest query blocks first
-  const int tr_L = (nb - 1 - ti) * B * Hq + tb * Hq + th;
-  return attn_prefill_impl(q, nullptr, nullptr, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale,
-                           causal, 64, 64, o, lse, static_cast<unsigned char*>(trace), tr_L,
-                           tj, stream);
+  return turbo_attn_prefill_blocks_trace(q, k8, v8, s_k, s_v, B, Hq, Hkv, N, d, sm_scale, causal,
+                                         64, 64, o, lse, tb, th, ti, tj, trace, stream);
 }
 
 int turbo_decode_default_split(int ng) { return turbo::decode_default_split(ng); }

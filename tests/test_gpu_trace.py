@@ -88,6 +88,68 @@ def test_prefill_tile_integers_bit_exact(orc, ta, dev, B, Hq, Hkv, N, causal, ti
         assert np.array_equal(g["sacc"], qi @ kj.T)
 
 
+# Table 3's block sizes (and the two other pairs the kernels take): tiles
+# (b, h, i, j) count B_r-row query blocks and B_c-key key blocks.  Chosen to
+# cover diagonal tiles (for B_r > B_c also the tile whose first rows see no
+# key), off-diagonal tiles, ragged last blocks and GQA.
+BLOCK_TRACE_CASES = [
+    # B_r, B_c, B, Hq, Hkv, N, causal, tiles
+    (32, 32, 1, 4, 2, 64 * 4 + 20, True, [(0, 1, 8, 8), (0, 3, 5, 2), (0, 0, 8, 0)]),
+    (32, 64, 2, 4, 1, 200, True, [(1, 2, 6, 3), (0, 1, 3, 1), (1, 0, 0, 0)]),
+    (64, 32, 1, 2, 2, 64 * 3 + 33, True, [(0, 1, 2, 5), (0, 0, 3, 6), (0, 1, 1, 1), (0, 0, 3, 0)]),
+    (64, 128, 1, 4, 2, 64 * 5 + 7, True, [(0, 3, 5, 2), (0, 1, 2, 1), (0, 2, 4, 0)]),
+    (128, 64, 2, 4, 2, 64 * 5 + 9, True, [(1, 3, 2, 5), (0, 0, 1, 3), (1, 1, 2, 4), (0, 2, 1, 0)]),
+    (128, 128, 1, 2, 1, 64 * 6 + 50, True, [(0, 1, 3, 3), (0, 0, 2, 1), (0, 1, 1, 1)]),
+    (32, 128, 1, 2, 2, 64 * 4 + 12, True, [(0, 0, 8, 2), (0, 1, 5, 1)]),
+    (128, 32, 1, 2, 1, 64 * 4 + 12, True, [(0, 1, 2, 8), (0, 1, 1, 7), (0, 0, 1, 4), (0, 1, 2, 0)]),
+    (64, 64, 1, 2, 2, 64 * 3 + 10, False, [(0, 1, 1, 3)]),
+    (128, 64, 1, 2, 1, 64 * 3 + 10, False, [(0, 0, 0, 3), (0, 1, 1, 0)]),
+    (32, 128, 1, 2, 1, 64 * 3 + 10, False, [(0, 1, 2, 1)]),
+]
+
+
+@pytest.mark.parametrize("br,bc,B,Hq,Hkv,N,causal,tiles", BLOCK_TRACE_CASES)
+def test_prefill_block_size_tile_integers_bit_exact(orc, ta, dev, br, bc, B, Hq, Hkv, N, causal,
+                                                    tiles):
+    q = _rand((B, Hq, N, 128), 2300 + N + br)
+    k = _rand((B, Hkv, N, 128), 2400 + N + bc)
+    v = _rand((B, Hkv, N, 128), 2500 + N)
+    k[..., 6] *= 10
+    sm = 1 / np.sqrt(128)
+    k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev), block_cols=bc)
+    o_plain = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv, sm, causal, block_rows=br,
+                                    block_cols=bc)
+    torch.cuda.synchronize()
+    k8h = k8.cpu().numpy()
+    nkeys = k8h.shape[2]  # key rows held (64 ceil(N / 64))
+    for (b, h, i, j) in tiles:
+        _log(f"prefill trace B_r={br} B_c={bc} B={B} Hq={Hq} Hkv={Hkv} N={N} causal={causal} "
+             f"tile={(b, h, i, j)}")
+        o, g = ta.turbo_attn_prefill_trace(q.to(dev), k8, v8, sk, sv, (b, h, i, j), sm, causal,
+                                           block_rows=br, block_cols=bc)
+        assert torch.equal(o.view(torch.int16), o_plain.view(torch.int16))
+        _, _, r = orc.attn_prefill(q, k, v, sm, causal, trace=(b, h, i, j), qblocks=(i, i + 1),
+                                   block_rows=br, block_cols=bc)
+        assert r["hit"] == 1
+        nq, nk = min(br, N - br * i), min(bc, N - bc * j)
+        rows = np.arange(br)[:, None]
+        keys = np.arange(bc)[None, :]
+        vis = (rows < nq) & (keys < nk)
+        if causal:
+            vis &= bc * j + keys <= br * i + rows
+        assert np.array_equal(g["q8"], r["q8"]), "Q8"
+        assert np.array_equal(g["sacc"][vis], r["sacc"][vis]), "QK^T accumulators"
+        assert np.array_equal(g["qp"], r["qp"]), "Q(P~)"
+        assert not g["qp"][~vis].any()
+        assert np.array_equal(g["pvacc"], r["pvacc"]), "PV accumulators"
+        assert _same_f32(g["sq"], r["sq"]) and _same_f32(g["pmax"], r["pmax"])
+        # the GPU's S of every key it holds is the plain product (masked ones too)
+        held = min(bc, nkeys - bc * j)
+        qi = g["q8"].astype(np.int64)
+        kj = k8h[b, h // (Hq // Hkv), bc * j:bc * j + held].astype(np.int64)
+        assert np.array_equal(g["sacc"][:, :held], qi @ kj.T)
+
+
 def test_prefill_trace_of_an_unprocessed_tile_writes_nothing(ta, dev):
     N = 64 * 3
     q, k, v = _rand((1, 2, N, 128), 1), _rand((1, 2, N, 128), 2), _rand((1, 2, N, 128), 3)

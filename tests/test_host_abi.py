@@ -145,9 +145,10 @@ def test_trace_layout_matches_header(ta):
             vals["TURBO_TRACE_PV"], vals["TURBO_TRACE_SQ"], vals["TURBO_TRACE_PMAX"],
             vals["TURBO_TRACE_BYTES"]) == (b.TRACE_Q8, b.TRACE_S, b.TRACE_P, b.TRACE_PV,
                                            b.TRACE_SQ, b.TRACE_PMAX, b.TRACE_BYTES)
-    # contiguous: int8 64x128, int32 64x64, int8 64x64, int32 64x128, two floats
-    assert b.TRACE_S == 64 * 128 and b.TRACE_P == b.TRACE_S + 4 * 64 * 64
-    assert b.TRACE_PV == b.TRACE_P + 64 * 64 and b.TRACE_SQ == b.TRACE_PV + 4 * 64 * 128
+    # contiguous, sized for the largest tile (B_r = B_c = 128): int8 128x128,
+    # int32 128x128, int8 128x128, int32 128x128, two floats
+    assert b.TRACE_S == 128 * 128 and b.TRACE_P == b.TRACE_S + 4 * 128 * 128
+    assert b.TRACE_PV == b.TRACE_P + 128 * 128 and b.TRACE_SQ == b.TRACE_PV + 4 * 128 * 128
     assert b.TRACE_BYTES == b.TRACE_SQ + 8
 
 

@@ -163,3 +163,34 @@ def test_kv_scales_follow_the_key_blocks(orc, fine, coarse):
         eq = np.array_equal(a[:, :, rows], b[:, :, rows]) and np.array_equal(la[:, :, rows],
                                                                              lb[:, :, rows])
         assert eq == same, (bc, same)
+
+
+@pytest.mark.parametrize("br,bc", [(32, 32), (128, 64), (64, 128), (128, 128), (32, 128)])
+def test_traced_tile_integers_for_other_block_sizes(orc, br, bc):
+    """The trace of a (B_r-row, B_c-key) tile: the Q block codes are step 1 of
+    its B_r rows, the accumulators are integer matrix products over the
+    visible pairs, Q(P~) is 0 where masked and 119 somewhere, and PV is Q(P~)
+    times the B_c-key V block."""
+    N = 300
+    q, k, v = _qkv(9, 1, 2, 1, N)
+    kb = orc.quantize_kv_blocks(k, v, bc)
+    nbq, nbc = -(-N // br), -(-N // bc)
+    for i, j in [(nbq - 1, (nbq - 1) * br // bc), (nbq - 1, 0), (1, (br + br - 1) // bc)]:
+        if j >= nbc or j * bc > i * br + br - 1:
+            continue
+        _, _, tr = orc.attn_prefill(q, k, v, SM, True, trace=(0, 1, i, j), block_rows=br,
+                                    block_cols=bc)
+        assert tr["hit"]
+        r0, k0 = i * br, j * bc
+        nq, nk = min(br, N - r0), min(bc, N - k0)
+        q8, s = orc.block_quant(q[0, 1, r0:r0 + nq].reshape(1, -1))
+        assert np.array_equal(tr["q8"][:nq], q8.reshape(nq, 128)) and tr["sq"] == s[0]
+        assert not tr["q8"][nq:].any()
+        vis = (np.arange(nk)[None, :] + k0) <= (np.arange(nq)[:, None] + r0)
+        k8 = kb["k8"][0, 0, k0:k0 + nk].astype(np.int64)
+        v8 = kb["v8"][0, 0, k0:k0 + nk].astype(np.int64)
+        sacc = tr["q8"][:nq].astype(np.int64) @ k8.T
+        assert np.array_equal(tr["sacc"][:nq, :nk][vis], sacc[vis])
+        qp = tr["qp"][:nq, :nk].astype(np.int64)
+        assert qp.min() >= 0 and qp.max() == 119 and not qp[~vis].any()
+        assert np.array_equal(tr["pvacc"][:nq], qp @ v8)

@@ -67,3 +67,16 @@ def test_scaled_weights_scale_the_block_scales(orc):
         assert np.array_equal(a[key], b[key])
     for key in ("sq", "sk", "sv"):
         assert np.array_equal(2 * a[key], b[key])
+
+
+def test_project_exact_against_integer_products(orc):
+    """The exact projection and its absolute-value sum against integer
+    arithmetic (inputs i/8 and j/64 make every product a multiple of 2^-9)."""
+    rng = np.random.default_rng(3)
+    x = rng.integers(-8, 9, (5, 7, 96))
+    w = rng.integers(-8, 9, (40, 96))
+    y, yabs = orc.project_exact(x / 8.0, w / 64.0)
+    ii = np.einsum("bnd,fd->bnf", x, w)
+    ia = np.einsum("bnd,fd->bnf", np.abs(x), np.abs(w))
+    assert np.array_equal(y * 512, ii.astype(np.float64))
+    assert np.array_equal(yabs * 512, ia.astype(np.float64))
