@@ -86,14 +86,38 @@ def ramp_clocks(fn, seconds: float = 0.2):
     """Untimed launches of the step until `seconds` of wall time have passed:
     the GPU idles during input generation and its clocks fall; the warmup
     steps proper (--warmup) and the timed steps (--steps) follow."""
-    import time
-
     import torch
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < seconds:
         for _ in range(4):
             fn()
         torch.cuda.synchronize()
+
+
+def launch_times(fn, iters: int, prev=None):
+    """GPU time (ms) of each of `iters` launches of fn, from a HIP event pair
+    around each launch on the stream the library launches on (torch's current
+    stream).  prev (optional) is launched untimed before each timed launch:
+    it hides the host's launch overhead of fn when fn is shorter than it."""
+    import torch
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(iters)]
+    fn()
+    torch.cuda.synchronize()
+    for a, b in ev:
+        if prev is not None:
+            prev()
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def stats(ts):
+    """Median and mean of per-launch times (ms)."""
+    return float(np.median(ts)), float(np.mean(ts))
 
 
 CPU_SAMPLE_SECONDS = 10.0
@@ -112,6 +136,71 @@ def cpu_sample(run_chunk, n_total: int, chunk: int, seconds: float = CPU_SAMPLE_
     return done, dt
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+# The paper's own efficiency result, quoted as context (other hardware, other
+# baseline): TurboAttention's attention speedup over FP16 FlashAttention.
+PAPER_CONTEXT = {
+    "attention_speedup_vs_fp16_flashattention": "1.2-1.8x (prefill up to 1.8x, decode up to 1.7x)",
+    "hardware": "NVIDIA A100-80GB-SXM, Triton kernels",
+    "workload": "Phi3-medium attention, batch 1-64 at 1k context and 4k-32k context at batch 4",
+    "source": "Abstract; Sec. 5.3, Fig. 5",
+    "comparable_here": False,
+}
+
+
+def measured_ceilings(dev):
+    """The int8 MFMA rate and the HBM streaming-read rate of this GPU, from the
+    library's probe kernels (median of 5 launches each)."""
+    import torch
+
+    import paper_2412_08585_amd as ta
+    ops = [0]
+
+    def mfma():
+        ops[0] = ta.binding.probe_mfma_i8(4096, dev)
+
+    buf = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+    ramp_clocks(mfma, 0.1)
+    t_m, _ = stats(launch_times(mfma, 5))
+    t_r, _ = stats(launch_times(lambda: ta.binding.probe_read(buf), 5))
+    nbytes = buf.numel() * 4
+    del buf
+    return {"int8_mfma_TOPS": round(ops[0] / (t_m * 1e-3) / 1e12, 1),
+            "hbm_read_GBs": round(nbytes / (t_r * 1e-3) / 1e9, 1),
+            "probes": "turbo_probe_mfma_i8 (8 chains of v_mfma_i32_16x16x64_i8 per wave, 2048 "
+                      "waves) and turbo_probe_read (1 GiB streaming read), median of 5"}
+
+
+def rel_l2(a, ref) -> float:
+    a = np.asarray(a, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return float(np.linalg.norm(a - ref) / np.linalg.norm(ref))
+
+
+def error_decomposition(run_oracle, exact, got):
+    """rel-L2 against exact fp64 softmax attention of the GPU output and of the
+    oracle with FlashQ and SAS on (the method), FlashQ alone (exact exp, no
+    threshold) and SAS alone (unquantized operands): the operator-level
+    analogue of the paper's Table 4 ablation."""
+    both = run_oracle(True, True)
+    return {"gpu": rel_l2(got, exact), "oracle_flashq_and_sas": rel_l2(both, exact),
+            "oracle_flashq_only": rel_l2(run_oracle(True, False), exact),
+            "oracle_sas_only": rel_l2(run_oracle(False, True), exact),
+            "gpu_vs_oracle_max_rel_rowmax": float(
+                np.max(np.abs(np.asarray(got, np.float64) - both)
+                       / np.maximum(np.abs(both).max(axis=-1, keepdims=True), 1e-30)))}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,10 +213,15 @@ def parse():
                          "library's default, each sequence by its own length; -1: the "
                          "occupancy-fitted turbo_decode_auto_split)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["quantize", "prefill", "decode", "copy"], default=None,
+    ap.add_argument("--no-decode-half", action="store_true",
+                    help="prefill workloads: skip the Phi-3-medium decode half of the line")
+    ap.add_argument("--no-error", action="store_true",
+                    help="skip the error decomposition against exact fp64 attention")
+    ap.add_argument("--only", choices=["quantize", "prefill", "decode", "copy", "mfma-ceiling",
+                                       "read-ceiling"], default=None,
                     help="launch only this kernel --steps times (for profiler passes); "
                          "'copy' runs a plain 1 GiB device copy (calibration of the HBM "
-                         "byte counters)")
+                         "byte counters); the ceilings run the library's probe kernels")
     return ap.parse_args()
 
 
@@ -144,15 +238,25 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    if args.only == "copy":
-        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
-        dst = torch.empty_like(src)
-        for _ in range(args.warmup + args.steps):
-            dst.copy_(src)
+    if args.only in ("copy", "mfma-ceiling", "read-ceiling"):
+        n = args.warmup + args.steps
+        if args.only == "copy":
+            src = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+            dst = torch.empty_like(src)
+            for _ in range(n):
+                dst.copy_(src)
+            info = {"bytes_read": src.numel() * 4, "bytes_written": dst.numel() * 4}
+        elif args.only == "mfma-ceiling":
+            for _ in range(n):
+                ops = ta.binding.probe_mfma_i8(4096, dev)
+            info = {"int8_ops_per_launch": ops}
+        else:
+            buf = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+            for _ in range(n):
+                nb_ = ta.binding.probe_read(buf)
+            info = {"bytes_read_per_launch": nb_}
         torch.cuda.synchronize()
-        print(json.dumps({"only": "copy", "bytes_read": src.numel() * 4,
-                          "bytes_written": dst.numel() * 4,
-                          "launches": args.warmup + args.steps}))
+        print(json.dumps({"only": args.only, "launches": n, **info}))
         return
     w = W.WORKLOADS[args.workload]
     if w.kind == "decode":
@@ -178,10 +282,9 @@ def main():
     sv = torch.empty_like(sk)
     o = torch.empty_like(q)
     od = torch.empty_like(qd)
-    lse = torch.empty(B, Hq, N, dtype=torch.float32, device=dev)
     sl = torch.full((B,), N, dtype=torch.int32, device=dev)
     # the decode of this batch (B * Hkv = 40 units of 64 groups) takes the
-    # occupancy-fitted chunk length; the decode workloads use the default
+    # occupancy-fitted chunk length; the decode half below uses the default
     split = ta.decode_auto_split(B, Hq, Hkv, w.max_groups)
     ws = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev)
 
@@ -222,42 +325,15 @@ def main():
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
 
-    # ---- per-kernel timing (same stream, events around repeated launches) ----
-    def time_kernel(fn, iters):
-        fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(iters):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / iters
-
-    def time_after(prev, fn, iters):
-        """GPU time of fn launched behind prev: the events bracket fn alone,
-        and prev (about 1 ms) hides the host's launch overhead of fn, which
-        for the 15-us decode of this workload exceeds its GPU time."""
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(iters)]
-        prev()
-        fn()
-        torch.cuda.synchronize()
-        for a, b in ev:
-            prev()
-            a.record(stream)
-            fn()
-            b.record(stream)
-        torch.cuda.synchronize()
-        return sum(a.elapsed_time(b) for a, b in ev) / iters
-
-    ms_q = time_kernel(run_quant, args.kernel_iters)
-    ms_p = time_kernel(run_prefill, args.kernel_iters)
-    ms_d = time_after(run_prefill, run_decode, args.kernel_iters)
+    # ---- per-kernel timing: HIP events around each launch, median -------------
+    ms_q, mean_q = stats(launch_times(run_quant, args.kernel_iters))
+    ms_p, mean_p = stats(launch_times(run_prefill, args.kernel_iters))
+    # the 15-us decode behind a prefill, which hides its host launch overhead
+    ms_d, mean_d = stats(launch_times(run_decode, args.kernel_iters, prev=run_prefill))
     prio = torch.empty(Hkv, dtype=torch.float32, device=dev)
-    ms_h = time_kernel(lambda: ta.binding.lib().turbo_head_priority(
+    ms_h, _ = stats(launch_times(lambda: ta.binding.lib().turbo_head_priority(
         ta.binding._ptr(k), B, Hkv, N, d, ta.binding._ptr(prio), ta.binding._stream(dev)),
-        args.kernel_iters)
+        args.kernel_iters))
 
     # ---- algorithmic work -------------------------------------------------------
     prefill_ops = 2.0 * d * N * (N + 1) * B * Hq          # QK^T + PV over causal pairs
@@ -269,6 +345,7 @@ def main():
     decode_bytes = sum(decode_bytes_per_token(int(bits[h])) for h in range(Hkv)) * B * (N // 64 * 64)
     decode_bytes += B * Hq * d * 2 * 2                    # q in, o out (fp16)
     prefill_tops = prefill_ops / (ms_p * 1e-3) / 1e12
+    ceil = measured_ceilings(dev)
 
     result = {
         "metric": "attention TOPS (prefill) & HBM GB/s (decode), % of MI355X roofline",
@@ -285,25 +362,68 @@ def main():
         "data": "synthetic (seeded N(0,1) fp16 with 4 K outlier channels x10; no weights)",
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "seq_len": N,
                    "head_dim": d, "causal": True, "kv_cache": w.bits, "block_rows": 64,
-                   "block_cols": 64, "decode_tokens": 1, "decode_kv_split_groups": split},
+                   "block_cols": 64, "decode_tokens": 1, "decode_kv_split_groups": split,
+                   "decode_half": "phi3m-decode-8k"},
         "kernels": {
-            "quantize_kv": {"ms": round(ms_q, 4), "GB/s": round(quant_bytes / ms_q / 1e6, 1),
+            "timing": "median of per-launch HIP events (mean in brackets)",
+            "quantize_kv": {"ms": round(ms_q, 4), "mean_ms": round(mean_q, 4),
+                            "GB/s": round(quant_bytes / ms_q / 1e6, 1),
                             "frac_hbm": round(quant_bytes / ms_q / 1e6 / PEAK_HBM_GBS, 4)},
             "head_priority": {"ms": round(ms_h, 4), "GB/s": round(B * Hkv * N * d * 2 / ms_h / 1e6, 1),
+                              "frac_hbm": round(B * Hkv * N * d * 2 / ms_h / 1e6 / PEAK_HBM_GBS, 4),
                               "note": "Sec. 3.2 bit choice from the prefill K; not in the step"},
-            "attn_prefill": {"ms": round(ms_p, 4), "TOPS": round(prefill_tops, 2),
+            "attn_prefill": {"ms": round(ms_p, 4), "mean_ms": round(mean_p, 4),
+                             "TOPS": round(prefill_tops, 2),
                              "frac_int8_mfma": round(prefill_tops / PEAK_INT8_TOPS, 4)},
-            "attn_decode": {"ms": round(ms_d, 4),
+            "attn_decode": {"ms": round(ms_d, 4), "mean_ms": round(mean_d, 4),
                             "GB/s": round(decode_bytes / ms_d / 1e6, 1),
                             "frac_hbm": round(decode_bytes / ms_d / 1e6 / PEAK_HBM_GBS, 4),
-                            "note": "cache of this workload (22 MB) may sit in the 256 MB MALL"},
+                            "note": "this workload's 22 MB cache may sit in the 256 MB MALL; "
+                                    "the decode roofline is roofline_decode"},
         },
         "roofline": {"kernel": "k_attn_prefill16", "bound": "mfma",
                      "achieved": round(prefill_tops, 2), "peak": PEAK_INT8_TOPS,
                      "unit": "TOP/s", "frac": round(prefill_tops / PEAK_INT8_TOPS, 4),
                      "traffic": measured_traffic("k_attn_prefill16", w.name),
-                     "per_launch_ops": prefill_ops},
+                     "per_launch_ops": prefill_ops,
+                     "frac_of_measured_ceiling": round(prefill_tops / ceil["int8_mfma_TOPS"], 4),
+                     "valu_note": "issue-bound on the VALU (SAS + P quantization + accumulator "
+                                  "update); see profiles/k_attn_prefill16_phi3m-prefill-4k.md"},
+        "ceilings_measured": ceil,
+        "paper_context": PAPER_CONTEXT,
     }
+
+    # ---- the decode half of the headline: Phi-3-medium decode ---------------
+    if not args.no_decode_half:
+        wd = W.WORKLOADS["phi3m-decode-8k"]
+        dec = decode_measure(args, wd, dev, 0)
+        result["roofline_decode"] = dict(dec["roofline"],
+                                         frac_of_measured_ceiling=round(
+                                             dec["roofline"]["achieved"] / ceil["hbm_read_GBs"], 4),
+                                         workload=wd.name, ms=dec["ms"], mean_ms=dec["mean_ms"],
+                                         kv_split_groups=dec["split"])
+        if not args.no_error:
+            result["error_vs_fp64"] = {"decode": decode_error(wd, dec, dev)}
+        del dec
+        torch.cuda.empty_cache()
+
+    # ---- error of GPU and oracle against exact fp64 attention (one unit) -----
+    if not args.no_error:
+        import oracle
+        b0, h0 = 0, 0
+        qs = q[b0, h0 * G:(h0 + 1) * G][None].cpu()
+        ks, vs = k[b0, h0][None, None].cpu(), v[b0, h0][None, None].cpu()
+        got = o[b0, h0 * G:(h0 + 1) * G][None].float().cpu().numpy()
+        ex, _ = oracle.attn_exact(qs, ks, vs, float(np.float32(w.sm_scale)), True)
+        dec_err = result.get("error_vs_fp64", {}).get("decode")
+        result["error_vs_fp64"] = {
+            "metric": "rel-L2 over the unit's query heads, rows and channels",
+            "prefill": dict(error_decomposition(
+                lambda qu, sa: oracle.attn_prefill(qs, ks, vs, w.sm_scale, True, quant=qu,
+                                                   sas=sa)[0], ex, got),
+                sample=f"sequence {b0}, KV head {h0} with its {G} query heads, {N} causal rows")}
+        if dec_err is not None:
+            result["error_vs_fp64"]["decode"] = dec_err
 
     # ---- CPU oracle on a bounded sample -----------------------------------------
     if not args.no_cpu_baseline:
@@ -330,45 +450,33 @@ def main():
 
         n_units, dt = cpu_sample(run_units, B * Hkv, max(1, math.ceil(threads / G)))
         units, ro = order[:n_units], np.concatenate(ros)
-        qs = torch.stack([q[b, h * G:(h + 1) * G] for b, h in units[:1]]).cpu()
-        ks = k[units[0][0], units[0][1]][None, None].cpu()
-        vs = v[units[0][0], units[0][1]][None, None].cpu()
         sample_ops = (prefill_ops + decode_ops) * n_units / (B * Hkv)
         result["cpu_baseline"] = {
             "value": round(sample_ops / dt / 1e12, 6), "unit": "TOPS",
             "cores": min(threads, n_units * G), "kind": "oracle",
+            "cpu_model": cpu_model(), "host_threads": os.cpu_count(),
             "sample": f"{n_units} of {B * Hkv} (sequence, KV head) units, full length "
                       f"(quantize + prefill + decode), {dt:.1f} s"}
-        # parity and error of the sampled units (reported, not gated here)
         got = torch.stack([o[b, h * G:(h + 1) * G] for b, h in units]).float().cpu().numpy()
         rowmax = np.abs(ro).max(axis=-1, keepdims=True)
-        ex, _ = oracle.attn_exact(qs[:1], ks[:1].reshape(1, 1, N, d), vs[:1].reshape(1, 1, N, d),
-                                  float(np.float32(w.sm_scale)), True)
-        rel = lambda a, r: float(np.linalg.norm(a - r) / np.linalg.norm(r))
         result["parity"] = {
             "max_err_vs_oracle_rel_rowmax": float(np.max(np.abs(got - ro) / rowmax)),
-            "rel_l2_vs_exact_fp64_gpu": rel(got[:1], ex), "rel_l2_vs_exact_fp64_oracle": rel(ro[:1], ex),
             "sample_units": n_units}
     print(json.dumps(result), flush=True)
 
 
-def bench_decode(args, w):
-    """Decode-only workload: the compressed cache (built once, untimed) is read
-    by turbo_attn_decode for one new query per sequence.  Two cache copies
-    with their own page/group tables are used alternately so that timed calls
-    stream from HBM rather than from the 256 MB MALL."""
+def build_decode_caches(w, dev, ncopy: int):
+    """The compressed cache of a decode workload (and its Sec. 3.3 buffer),
+    built untimed, `ncopy` times with the same contents so that timed calls
+    can alternate between copies and stream from HBM rather than the MALL."""
     import torch
 
     import paper_2412_08585_amd as ta
     from paper_2412_08585_amd import workloads as W
-
-    dev = torch.device("cuda:0")
-    B, Hq, Hkv, N, G = w.B, w.Hq, w.Hkv, w.N, w.G
+    B, Hkv, N = w.B, w.Hkv, w.N
     bits = W.head_bits(w)
     bt, gt = W.tables(w)
-    ncopy = 2
-    caches = []
-    tails = []
+    caches, tails = [], []
     for c in range(ncopy):
         cache = ta.PagedKVCache(bt.size, gt.size, bits, dev)
         tail = ta.KVTail(B, Hkv, dev)
@@ -387,9 +495,21 @@ def bench_decode(args, w):
         caches.append((cache, btd, gtd))
         tails.append(tail)
     torch.cuda.synchronize()
+    return caches, tails, bits
+
+
+def decode_measure(args, w, dev, split: int, buffer_step: bool = False):
+    """Times turbo_attn_decode on a decode workload (two cache copies used
+    alternately); returns the timing, the roofline and the output."""
+    import torch
+
+    import paper_2412_08585_amd as ta
+    from paper_2412_08585_amd import workloads as W
+    B, Hq, Hkv, N = w.B, w.Hq, w.Hkv, w.N
+    ncopy = 2
+    caches, tails, bits = build_decode_caches(w, dev, ncopy)
     q = W.decode_query(w, device=dev)
     sl = torch.full((B,), N, dtype=torch.int32, device=dev)
-    split = args.kv_split_groups
     if split < 0:
         split = ta.decode_auto_split(B, Hq, Hkv, w.max_groups)
     ws = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev)
@@ -401,93 +521,130 @@ def bench_decode(args, w):
         it[0] += 1
         ta.turbo_attn_decode(q, cache, sl, btd, gtd, w.sm_scale, split, workspace=ws, out=o)
 
+    out = {"run": run, "q": q, "o": o, "split": ta.decode_split(N, split), "bits": bits}
     if args.only:
-        for _ in range(args.warmup + args.steps):
-            run()
-        torch.cuda.synchronize()
-        print(json.dumps({"only": "decode", "launches": args.warmup + args.steps}))
-        return
+        return out
     ramp_clocks(run)
     for _ in range(args.warmup):
         run()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        run()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-
-    # ---- the Sec. 3.3 decoding step: append the new token's K/V to the int8
-    # buffer, then attend the cache plus the buffer (not the headline) -------
-    g = torch.Generator(device="cpu").manual_seed(7)
-    knew = torch.randn(B, Hkv, 128, generator=g).half().to(dev)
-    vnew = torch.randn(B, Hkv, 128, generator=g).half().to(dev)
-    sl1 = torch.full((B,), N + 1, dtype=torch.int32, device=dev)
-    ws1 = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev, with_tail=True)
-    it1 = [0]
-
-    def run_append():
-        cache, btd, gtd = caches[it1[0] % ncopy]
-        ta.turbo_append_kv(knew, vnew, sl, cache, tails[it1[0] % ncopy], btd, gtd)
-
-    def run_decode_buf():
-        cache, btd, gtd = caches[it1[0] % ncopy]
-        ta.turbo_attn_decode(q, cache, sl1, btd, gtd, w.sm_scale, split, workspace=ws1, out=o,
-                             tail=tails[it1[0] % ncopy])
-        it1[0] += 1
-
-    def time_loop(fn):
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps
-
-    ms_app = time_loop(run_append)
-    ms_buf = time_loop(lambda: (run_append(), run_decode_buf()))
+    ts = launch_times(run, max(args.steps, 20))
+    ms, mean = stats(ts)
     kv_bytes = sum(decode_bytes_per_token(int(bits[h])) for h in range(Hkv)) * B * N
     qo_bytes = B * Hq * 128 * 2 * 2
     gbs = (kv_bytes + qo_bytes) / (ms * 1e-3) / 1e9
+    out.update(ms=ms, mean_ms=mean, kv_bytes=kv_bytes, qo_bytes=qo_bytes, gbs=gbs,
+               roofline={"kernel": "k_attn_decode", "bound": "hbm", "achieved": round(gbs, 1),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": measured_traffic("k_attn_decode", w.name),
+                         "per_launch_bytes": kv_bytes + qo_bytes})
+    run()  # o of the first copy (both copies hold the same cache)
+    torch.cuda.synchronize()
+    if buffer_step:
+        # the Sec. 3.3 decoding step: append the new token's K/V to the int8
+        # buffer, then attend the cache plus the buffer (not the headline)
+        g = torch.Generator(device="cpu").manual_seed(7)
+        knew = torch.randn(B, Hkv, 128, generator=g).half().to(dev)
+        vnew = torch.randn(B, Hkv, 128, generator=g).half().to(dev)
+        sl1 = torch.full((B,), N + 1, dtype=torch.int32, device=dev)
+        ws1 = ta.decode_workspace(B, Hq, Hkv, w.max_groups, split, dev, with_tail=True)
+        o1 = torch.empty_like(q)
+        it1 = [0]
+
+        def run_append():
+            cache, btd, gtd = caches[it1[0] % ncopy]
+            ta.turbo_append_kv(knew, vnew, sl, cache, tails[it1[0] % ncopy], btd, gtd)
+
+        def run_decode_buf():
+            cache, btd, gtd = caches[it1[0] % ncopy]
+            ta.turbo_attn_decode(q, cache, sl1, btd, gtd, w.sm_scale, split, workspace=ws1,
+                                 out=o1, tail=tails[it1[0] % ncopy])
+            it1[0] += 1
+
+        ms_app, _ = stats(launch_times(run_append, args.steps))
+        ms_buf, _ = stats(launch_times(lambda: (run_append(), run_decode_buf()), args.steps))
+        out["buffer_step"] = {
+            "note": "Sec. 3.3 decoding step: turbo_append_kv of the new token, then "
+                    "turbo_attn_decode over the cache plus the int8 buffer (seq_len N+1)",
+            "append_ms": round(ms_app, 4), "step_ms": round(ms_buf, 4),
+            "GB/s": round((kv_bytes + qo_bytes) / (ms_buf * 1e-3) / 1e9, 1)}
+    del caches, tails, ws
+    return out
+
+
+def decode_error(w, dec, dev):
+    """rel-L2 against exact fp64 attention of the decode output of one
+    sequence over all its cached tokens, for one int4 and (mixed caches) one
+    int2 KV head, with the oracle's decomposition."""
+    import oracle
+    import torch
+
+    from paper_2412_08585_amd import workloads as W
+    bits = dec["bits"]
+    heads = [int(np.argmax(bits == 4))] + ([int(np.argmax(bits == 2))] if (bits == 2).any() else [])
+    res = {"metric": "rel-L2 over the query heads of the KV head and channels"}
+    for h in heads:
+        ku, vu = W.unit_kv(w, 0, h, device=dev)
+        ks, vs = ku[None, None].cpu(), vu[None, None].cpu()
+        qs = dec["q"][0:1, h * w.G:(h + 1) * w.G].cpu()
+        got = dec["o"][0:1, h * w.G:(h + 1) * w.G].float().cpu().numpy()
+        ref = oracle.quantize_kv(ks, vs, [int(bits[h])])
+        ex, _ = oracle.attn_exact(qs[:, :, None], ks, vs, float(np.float32(w.sm_scale)), False)
+        res[f"kv_head_{h}_int{int(bits[h])}"] = error_decomposition(
+            lambda qu, sa: oracle.attn_decode(qs, ref, [w.N], w.sm_scale, split=dec["split"],
+                                              quant=qu, sas=sa)[0], ex[:, :, 0], got)
+    res["sample"] = f"sequence 0, {w.N} cached tokens, chunks of {dec['split']} groups"
+    return res
+
+
+def bench_decode(args, w):
+    """Decode-only workload: the compressed cache (built once, untimed) is read
+    by turbo_attn_decode for one new query per sequence.  Two cache copies
+    with their own page/group tables are used alternately so that timed calls
+    stream from HBM rather than from the 256 MB MALL."""
+    import torch
+    dev = torch.device("cuda:0")
+    B, Hq, Hkv, N = w.B, w.Hq, w.Hkv, w.N
+    dec = decode_measure(args, w, dev, args.kv_split_groups, buffer_step=True)
+    if args.only:
+        for _ in range(args.warmup + args.steps):
+            dec["run"]()
+        torch.cuda.synchronize()
+        print(json.dumps({"only": "decode", "launches": args.warmup + args.steps}))
+        return
+    ceil = measured_ceilings(dev)
     ops = 4.0 * 128 * N * B * Hq
     result = {
         "metric": "attention TOPS (prefill) & HBM GB/s (decode), % of MI355X roofline",
-        "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "value": round(dec["gbs"], 1), "unit": "GB/s", "n_gpus": 1, "steps": max(args.steps, 20),
+        "warmup": args.warmup, "ms_per_step": round(dec["ms"], 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int8",
         "data": "synthetic (seeded N(0,1) fp16 K/V with 4 K outlier channels x10, "
                 "compressed before timing; no weights)",
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "kv_len": N,
                    "head_dim": 128, "kv_cache": w.bits,
-                   "head_bits": [int(x) for x in bits], "page_tokens": 16,
-                   "kv_split_groups": ta.decode_split(N, split), "cache_copies": ncopy},
-        "attention_TOPS": round(ops / (ms * 1e-3) / 1e12, 3),
-        "roofline": {"kernel": "k_attn_decode", "bound": "hbm",
-                     "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(gbs / PEAK_HBM_GBS, 4),
-                     "traffic": measured_traffic("k_attn_decode", w.name),
-                     "per_launch_bytes": kv_bytes + qo_bytes},
-        "buffer_step": {
-            "note": "Sec. 3.3 decoding step: turbo_append_kv of the new token, then "
-                    "turbo_attn_decode over the cache plus the int8 buffer (seq_len N+1)",
-            "append_ms": round(ms_app, 4), "step_ms": round(ms_buf, 4),
-            "GB/s": round((kv_bytes + qo_bytes) / (ms_buf * 1e-3) / 1e9, 1)},
+                   "head_bits": [int(x) for x in dec["bits"]], "page_tokens": 16,
+                   "kv_split_groups": dec["split"], "cache_copies": 2,
+                   "timing": "median of per-launch HIP events"},
+        "attention_TOPS": round(ops / (dec["ms"] * 1e-3) / 1e12, 3),
+        "roofline": dict(dec["roofline"], frac_of_measured_ceiling=round(
+            dec["gbs"] / ceil["hbm_read_GBs"], 4), mean_ms=round(dec["mean_ms"], 4)),
+        "ceilings_measured": ceil,
+        "buffer_step": dec["buffer_step"],
+        "paper_context": PAPER_CONTEXT,
     }
+    if not args.no_error:
+        result["error_vs_fp64"] = {"decode": decode_error(w, dec, dev)}
 
     # ---- CPU oracle: the oracle's caches of the first sequences (built
     # untimed, like the GPU cache), attended until the sample time is spent ----
     if not args.no_cpu_baseline:
         import oracle
-        qc = q.cpu()
-        run()                       # o of the plain decode (the buffer step overwrote it)
-        got = o.float().cpu().numpy()
+
+        from paper_2412_08585_amd import workloads as W
+        qc = dec["q"].cpu()
+        got = dec["o"].float().cpu().numpy()
+        bits = dec["bits"]
         refs, t0 = [], time.perf_counter()
         while len(refs) < B and time.perf_counter() - t0 < 15.0:
             b = len(refs)
@@ -500,16 +657,16 @@ def bench_decode(args, w):
         while passes == 0 or dt < CPU_SAMPLE_SECONDS:
             for b, ref in enumerate(refs):
                 t1 = time.perf_counter()
-                ro, _ = oracle.attn_decode(qc[b:b + 1], ref, [N], w.sm_scale,
-                                           split=ta.decode_split(N, split))
+                ro, _ = oracle.attn_decode(qc[b:b + 1], ref, [N], w.sm_scale, split=dec["split"])
                 dt += time.perf_counter() - t1
                 rowmax = np.abs(ro[0]).max(axis=-1, keepdims=True)
                 err = max(err, float(np.max(np.abs(got[b] - ro[0]) / rowmax)))
             passes += 1
         nseq = len(refs) * passes
         result["cpu_baseline"] = {
-            "value": round((kv_bytes + qo_bytes) * nseq / B / dt / 1e9, 3), "unit": "GB/s",
-            "cores": min(oracle.num_threads(), Hq), "kind": "oracle",
+            "value": round((dec["kv_bytes"] + dec["qo_bytes"]) * nseq / B / dt / 1e9, 3),
+            "unit": "GB/s", "cores": min(oracle.num_threads(), Hq), "kind": "oracle",
+            "cpu_model": cpu_model(), "host_threads": os.cpu_count(),
             "sample": f"{len(refs)} of {B} sequences (oracle cache built untimed), each attended "
                       f"{passes} times, {dt:.1f} s"}
         result["parity"] = {"max_err_vs_oracle_rel_rowmax": err, "sample_sequences": len(refs)}
@@ -532,15 +689,7 @@ def bench_softmax(args, w):
     ramp_clocks(run)
     for _ in range(args.warmup):
         run()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        run()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    ms, _ = stats(launch_times(run, args.steps))
     nbytes = rows * cols * 4 * 2               # fp32 read once, written once
     gbs = nbytes / (ms * 1e-3) / 1e9
     result = {
@@ -595,14 +744,7 @@ def bench_projection(args, w):
         ramp_clocks(fn)
         for _ in range(args.warmup):
             fn()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(iters):
-            fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / iters
+        return stats(launch_times(fn, iters))[0]
 
     ms = time_loop(run, args.steps)
     # context: the library fp16 GEMM alone (no quantization, fp16 output)

@@ -536,6 +536,27 @@ int turbo_decode_auto_split(int B, int Hq, int Hkv, int max_groups_per_seq);
 size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_seq,
                                     int kv_split_groups, int with_tail);
 
+/*
+ * Measurement probes (not part of the method): the ceilings the attention
+ * kernels are measured against, on the GPU at hand.
+ *
+ * turbo_probe_mfma_i8 — chains of v_mfma_i32_16x16x64_i8 on register
+ * operands, `iters` rounds of 8 per wave, 2048 waves (two per SIMD of 256
+ * CUs); no memory traffic.  *ops (host) receives the int8 ops the launch
+ * performs (2 * 16 * 16 * 64 per MFMA); sink (device, int32 [512]) receives
+ * one folded word per work-group.  The int8 MFMA rate is *ops / elapsed.
+ *
+ * turbo_probe_read — a streaming read of `bytes` (a multiple of 16, 16-byte
+ * aligned device buffer) by 2048 work-groups of 256 threads with eight
+ * 16-byte loads in flight per thread; sink (device, uint32 [8192]) receives
+ * one folded word per wave.  The read rate is bytes / elapsed.
+ *
+ * Both queue one launch on `stream`.  INVALID_ARG for iters < 1, null
+ * pointers, or a misaligned / zero-sized buffer.
+ */
+int turbo_probe_mfma_i8(int iters, int* sink, int64_t* ops, hipStream_t stream);
+int turbo_probe_read(const void* src, size_t bytes, unsigned* sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
                                          P], I),
             "turbo_decode_auto_split": ([I, I, I, I], I),
             "turbo_decode_default_split": ([I], I),
+            "turbo_probe_mfma_i8": ([I, P, P, P], I),
+            "turbo_probe_read": ([P, Z, P, P], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
         }
         for name, (args, res) in sig.items():
@@ -472,3 +474,21 @@ def turbo_attn_prefill_q8(q8: torch.Tensor, s_q: torch.Tensor, k8, v8, s_k, s_v,
                                        _ptr(o), _ptr(lse), _stream(q8.device)),
            "turbo_attn_prefill_q8")
     return (o, lse) if return_lse else o
+
+
+def probe_mfma_i8(iters: int, device="cuda") -> int:
+    """Queues the int8 MFMA ceiling probe; returns the int8 ops it performs."""
+    sink = torch.empty(512, dtype=torch.int32, device=device)
+    ops = ctypes.c_int64(0)
+    _check(lib().turbo_probe_mfma_i8(int(iters), _ptr(sink), ctypes.byref(ops),
+                                     _stream(torch.device(device))), "turbo_probe_mfma_i8")
+    return int(ops.value)
+
+
+def probe_read(buf: torch.Tensor) -> int:
+    """Queues the streaming-read probe over buf; returns the bytes it reads."""
+    sink = torch.empty(8192, dtype=torch.int32, device=buf.device)
+    n = buf.numel() * buf.element_size()
+    _check(lib().turbo_probe_read(_ptr(buf), n, _ptr(sink), _stream(buf.device)),
+           "turbo_probe_read")
+    return n

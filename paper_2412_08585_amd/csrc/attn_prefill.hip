@@ -439,6 +439,17 @@ __device__ __forceinline__ int vswz(int ch) {
   return (((ch >> 1) ^ (ch >> 3)) & 1) | (((ch >> 2) & 1) << 1);
 }
 
+// Raw buffer resource over `bytes` bytes at p (gfx9 descriptor word 3).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t unit_rsrc(const int8_t* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(p), 0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 tile_load(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, soff, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 template <int kW>
 struct Prefill16Lds {
   __attribute__((aligned(16))) int8_t k[2][64 * 128];   // [key][128 channels], swizzled
@@ -469,8 +480,11 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
   const int row0 = kBr * i + 16 * w;  // first query row of this wave
   const int qrow = row0 + n;
   const long kvu = (long)b * a.Hkv + kh;
-  const float* skp = a.sk + kvu * a.nbc;
-  const float* svp = a.sv + kvu * a.nbc;
+  // the block scales are read-only here: read them through the constant
+  // address space, which keeps these wave-uniform reads on the scalar unit
+  typedef const __attribute__((address_space(4))) float cfloat;
+  const cfloat* skp = (const cfloat*)(a.sk + kvu * a.nbc);
+  const cfloat* svp = (const cfloat*)(a.sv + kvu * a.nbc);
   // last key tile: the one holding the block's last row when causal
   const int jend = a.causal ? min(a.nbc - 1, (kBr * i + kBr - 1) / 64) : a.nbc - 1;
 
@@ -481,6 +495,11 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
   const uint4* kg = reinterpret_cast<const uint4*>(a.k8 + kvu * a.nb * 8192);
   const uint4* vg = reinterpret_cast<const uint4*>(a.v8 + kvu * a.nb * 8192);
   const int c0 = tid, c1 = tid + 256;
+  // buffer resources over this unit's K8 and V8 blocks (loads past them,
+  // which never occur, would read 0)
+  const __amdgpu_buffer_rsrc_t krs = unit_rsrc(a.k8 + kvu * a.nb * 8192, a.nb * 8192);
+  const __amdgpu_buffer_rsrc_t vrs = unit_rsrc(a.v8 + kvu * a.nb * 8192, a.nb * 8192);
+  const unsigned lane16 = 16u * (unsigned)tid;
   const int kdst0 = (c0 >> 3) * 128 + 16 * ((c0 & 7) ^ kswz(c0 >> 3));
   const int kdst1 = (c1 >> 3) * 128 + 16 * ((c1 & 7) ^ kswz(c1 >> 3));
   const int vdst0 = (c0 >> 2) * 64 + 16 * ((c0 & 3) ^ vswz(c0 >> 2));
@@ -609,9 +628,12 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     }
     *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst0]) = kp0;
     if constexpr (kTwo) *reinterpret_cast<uint4*>(&L.k[buf ^ 1][kdst1]) = kp1;
-    const long o2 = (long)min(j + 2, jend) * 512;
-    kp0 = kg[o2 + tid];
-    if constexpr (kTwo) kp1 = kg[o2 + tid + 256];
+    // tile j + 2: buffer loads with the tile offset in a scalar register and
+    // the lane's fixed offset in a vector register (no per-lane address
+    // arithmetic per tile)
+    const int o2 = min(j + 2, jend) * 8192;
+    kp0 = tile_load(krs, lane16, o2);
+    if constexpr (kTwo) kp1 = tile_load(krs, lane16 + 4096u, o2);
     const bool trace_tile = traced && j == a.tr_j;
     if constexpr (kTrace) {
       if (trace_tile) {
@@ -649,7 +671,12 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     smax = max_xor32(max_xor16_nn(smax));
     const float mold = mrow;
     const float mnew = fmaxf(mold, smax);
-    float rs, pmax;
+    // A row whose maximum over this tile reaches its running maximum holds a
+    // score with y = 0, whose P~ is SAS(0) = c0, and no P~ exceeds c0 (LUT[k]
+    // <= 1 and POLY is decreasing from c0 on [0, 1)): the wave's P~ maximum
+    // is then c0 without a reduction.
+    const bool top = __builtin_amdgcn_ballot_w64(smax >= mold && smax != -INFINITY) != 0;
+    float rs;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -657,7 +684,6 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
         const float p = sas_y(mnew - P[mb][r], L.lut);
         P[mb][r] = p;
         rs = (mb | r) ? rs + p : p;
-        pmax = (mb | r) ? fmaxf(pmax, p) : p;
       }
     // Rescale by SAS(m_old - m_new): 0 when m_old = -inf, exactly 1 (e^0)
     // for a row whose maximum did not move.  When no row of the wave moved
@@ -671,7 +697,15 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     lpart = moved ? alpha * lpart + rs : lpart + rs;
     mrow = mnew;
     // ---- tile maximum of P~ over the four waves ------------------------
-    pmax = wave_max_pos(pmax);  // P~ >= 0
+    float pmax = kC0;
+    if (!top) {  // wave-uniform
+      pmax = P[0][0];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = (mb == 0); r < 4; ++r) pmax = fmaxf(pmax, P[mb][r]);
+      pmax = wave_max_pos(pmax);  // P~ >= 0
+    }
     if (lane == 0) L.xmax[buf][w] = pmax;
     __syncthreads();
     {
@@ -749,8 +783,8 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     }
     *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst0]) = vp0;
     if constexpr (kTwo) *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst1]) = vp1;
-    vp0 = vg[o2 + tid];
-    if constexpr (kTwo) vp1 = vg[o2 + tid + 256];
+    vp0 = tile_load(vrs, lane16, o2);
+    if constexpr (kTwo) vp1 = tile_load(vrs, lane16 + 4096u, o2);
     skj = skn;
     svj = svn;
   };

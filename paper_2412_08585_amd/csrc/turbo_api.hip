@@ -16,6 +16,7 @@
 #include "kv_tail.hip"
 #include "sas_softmax.hip"
 #include "qkv_project.hip"
+#include "probes.hip"
 
 namespace {
 
@@ -591,6 +592,26 @@ int turbo_append_kv(const void* k_new, const void* v_new, int B, int Hkv, int d,
   a.group_table = group_table;
   a.max_groups = max_groups_per_seq;
   return turbo::launch_append_kv(a, B, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
+int turbo_probe_mfma_i8(int iters, int* sink, int64_t* ops, hipStream_t stream) {
+  if (iters < 1 || !sink || !ops) return TURBO_ERR_INVALID_ARG;
+  const int st = check_device();
+  if (st != TURBO_OK) return st;
+  // 4 waves per work-group, kProbeChains MFMAs of 2 * 16 * 16 * 64 ops each
+  *ops = (int64_t)turbo::kProbeMfmaBlocks * 4 * turbo::kProbeChains * iters * (2 * 16 * 16 * 64);
+  return turbo::launch_probe_mfma_i8(iters, sink, stream) == hipSuccess ? TURBO_OK
+                                                                         : TURBO_ERR_HIP;
+}
+
+int turbo_probe_read(const void* src, size_t bytes, unsigned* sink, hipStream_t stream) {
+  if (!src || !sink || bytes < 16 || bytes % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(src) % 16 != 0)
+    return TURBO_ERR_INVALID_ARG;
+  const int st = check_device();
+  if (st != TURBO_OK) return st;
+  return turbo::launch_probe_read(src, bytes, sink, stream) == hipSuccess ? TURBO_OK
+                                                                          : TURBO_ERR_HIP;
 }
 
 }  // extern "C"
