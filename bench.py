@@ -178,7 +178,8 @@ def measured_ceilings(dev):
     return {"int8_mfma_TOPS": round(ops[0] / (t_m * 1e-3) / 1e12, 1),
             "hbm_read_GBs": round(nbytes / (t_r * 1e-3) / 1e9, 1),
             "probes": "turbo_probe_mfma_i8 (8 chains of v_mfma_i32_16x16x64_i8 per wave, 2048 "
-                      "waves) and turbo_probe_read (1 GiB streaming read), median of 5"}
+                      "waves) and turbo_probe_read (1 GiB nontemporal streaming read, one "
+                      "32 KiB chunk per work-group), median of 5"}
 
 
 def rel_l2(a, ref) -> float:
@@ -331,9 +332,11 @@ def main():
     # the 15-us decode behind a prefill, which hides its host launch overhead
     ms_d, mean_d = stats(launch_times(run_decode, args.kernel_iters, prev=run_prefill))
     prio = torch.empty(Hkv, dtype=torch.float32, device=dev)
+    nws_h = int(ta.binding.lib().turbo_head_priority_workspace_bytes(B, Hkv, N))
+    ws_h = torch.empty(nws_h // 4, dtype=torch.float32, device=dev)
     ms_h, _ = stats(launch_times(lambda: ta.binding.lib().turbo_head_priority(
-        ta.binding._ptr(k), B, Hkv, N, d, ta.binding._ptr(prio), ta.binding._stream(dev)),
-        args.kernel_iters))
+        ta.binding._ptr(k), B, Hkv, N, d, ta.binding._ptr(ws_h), nws_h, ta.binding._ptr(prio),
+        ta.binding._stream(dev)), args.kernel_iters))
 
     # ---- algorithmic work -------------------------------------------------------
     prefill_ops = 2.0 * d * N * (N + 1) * B * Hq          # QK^T + PV over causal pairs

@@ -444,10 +444,17 @@ int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache,
  *   gap_c = max - min of channel c,  gap = max - min over all channels,
  *   std   = population standard deviation of the 128 gap_c,
  *   priority[h] = gap * std   (device fp32 [Hkv], written on `stream`).
- * INVALID_ARG for B == 0 or N == 0 (no statistics), null pointers, d != 128.
+ * workspace   device scratch of at least turbo_head_priority_workspace_bytes
+ *             (per-slab channel maxima and minima; no initialization needed).
+ * INVALID_ARG for B == 0 or N == 0 (no statistics), null pointers, d != 128;
+ * WORKSPACE_TOO_SMALL for a missing or short workspace.
  */
-int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, float* priority,
-                        hipStream_t stream);
+int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, void* workspace,
+                        size_t workspace_bytes, float* priority, hipStream_t stream);
+
+/* Workspace bytes of turbo_head_priority: fp32 [Hkv][B * ceil(N / 256)][256]
+ * (0 for arguments < 1). */
+size_t turbo_head_priority_workspace_bytes(int B, int Hkv, int N);
 
 /*
  * turbo_int2_heads — the quantization strategy of Sec. 3.2 on the host:
@@ -546,10 +553,11 @@ size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_s
  * performs (2 * 16 * 16 * 64 per MFMA); sink (device, int32 [512]) receives
  * one folded word per work-group.  The int8 MFMA rate is *ops / elapsed.
  *
- * turbo_probe_read — a streaming read of `bytes` (a multiple of 16, 16-byte
- * aligned device buffer) by 2048 work-groups of 256 threads with eight
- * 16-byte loads in flight per thread; sink (device, uint32 [8192]) receives
- * one folded word per wave.  The read rate is bytes / elapsed.
+ * turbo_probe_read — a streaming read of `bytes` (a multiple of 16 up to
+ * 2^40, 16-byte aligned device buffer): one work-group of 256 threads per
+ * 32 KiB chunk, eight nontemporal 16-byte loads in flight per thread; sink
+ * (device, uint32 [1]) is written only if the folded data hit a fixed
+ * pattern.  The read rate is bytes / elapsed.
  *
  * Both queue one launch on `stream`.  INVALID_ARG for iters < 1, null
  * pointers, or a misaligned / zero-sized buffer.

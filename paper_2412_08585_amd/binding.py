@@ -62,7 +62,8 @@ def lib() -> ctypes.CDLL:
                                          P], I),
             "turbo_tail_init": ([P, P, I, I, I, I, P, P, P, P], I),
             "turbo_append_kv": ([P, P, I, I, I, P, P, P, P, P, I, P], I),
-            "turbo_head_priority": ([P, I, I, I, I, P, P], I),
+            "turbo_head_priority": ([P, I, I, I, I, P, Z, P, P], I),
+            "turbo_head_priority_workspace_bytes": ([I, I, I], Z),
             "turbo_int2_heads": ([P, I, I, P], I),
             "turbo_sas_softmax": ([P, P, ctypes.c_int64, I, P], I),
             "turbo_attn_prefill_q8": ([P, P, P, P, P, P, I, I, I, I, I, F, I, P, P, P], I),
@@ -398,8 +399,10 @@ def turbo_head_priority(k: torch.Tensor) -> torch.Tensor:
     k fp16 [B][Hkv][N][128]; returns fp32 [Hkv] on k's device."""
     B, Hkv, N, d = k.shape
     out = torch.empty(Hkv, dtype=torch.float32, device=k.device)
-    _check(lib().turbo_head_priority(_ptr(k), B, Hkv, N, d, _ptr(out), _stream(k.device)),
-           "turbo_head_priority")
+    n = int(lib().turbo_head_priority_workspace_bytes(B, Hkv, N))
+    ws = torch.empty(max(n, 4) // 4, dtype=torch.float32, device=k.device)
+    _check(lib().turbo_head_priority(_ptr(k), B, Hkv, N, d, _ptr(ws), n, _ptr(out),
+                                     _stream(k.device)), "turbo_head_priority")
     return out
 
 
@@ -487,7 +490,7 @@ def probe_mfma_i8(iters: int, device="cuda") -> int:
 
 def probe_read(buf: torch.Tensor) -> int:
     """Queues the streaming-read probe over buf; returns the bytes it reads."""
-    sink = torch.empty(8192, dtype=torch.int32, device=buf.device)
+    sink = torch.empty(1, dtype=torch.int32, device=buf.device)
     n = buf.numel() * buf.element_size()
     _check(lib().turbo_probe_read(_ptr(buf), n, _ptr(sink), _stream(buf.device)),
            "turbo_probe_read")

@@ -1,11 +1,16 @@
 // Head-wise mixed precision (Sec. 3.2): the priority gap x std of each KV
 // head, from the prefill keys of the whole batch.
 //
-// One workgroup of 1024 threads per KV head.  Thread (tl, cg) covers channels
-// 8cg .. 8cg+7 (16 bytes of a 256-byte fp16 row, so 16 threads read a whole
-// row) of the tokens tl, tl + 64, ... of every sequence, four rows in flight,
-// keeping per-channel maxima and minima; the 64 token lanes are then merged
-// through LDS, and one wave forms the channel gaps, their mean and spread.
+// Two launches, so that the reads of the keys spread over the whole chip:
+//   * k_head_minmax: one work-group of 256 threads per (KV head, sequence,
+//     256-token slab).  Thread (row lane tl, channel group cg) covers channels
+//     8cg .. 8cg+7 (16 bytes of a 256-byte fp16 row: 16 threads read a whole
+//     row, a wave four consecutive rows) of rows tl, tl + 16, ..., sixteen
+//     loads in flight at once; the 16 row lanes are merged through LDS and the
+//     slab's per-channel maxima and minima go to the workspace.
+//   * k_head_priority_final: one work-group of 1024 threads per KV head merges
+//     its slabs (four threads per statistic, eight loads in flight each), then
+//     one wave forms the channel gaps, their mean and spread.
 #include "turbo_common.h"
 
 namespace turbo {
@@ -13,16 +18,20 @@ namespace turbo {
 struct PriorityArgs {
   const uint4* k;   // fp16 [B][Hkv][N][128] as 8-half units
   int B, Hkv, N;
+  int nslab;        // 128-token slabs per sequence
+  float* ws;        // [Hkv][B * nslab][256]: channel maxima, then minima
   float* priority;  // [Hkv]
 };
 
-constexpr int kPrioThreads = 1024;
-constexpr int kPrioTokenLanes = kPrioThreads / 16;
+constexpr int kPrioSlab = 256;  // tokens per slab
+constexpr int kPrioRowLanes = 16;
+constexpr int kPrioLoads = 16;  // rows per thread in flight at once
 
-__global__ __launch_bounds__(kPrioThreads) void k_head_priority(PriorityArgs a) {
-  __shared__ float smax[kPrioTokenLanes / 4][128 + 4];
-  __shared__ float smin[kPrioTokenLanes / 4][128 + 4];
-  const int h = blockIdx.x;
+__global__ __launch_bounds__(256) void k_head_minmax(PriorityArgs a) {
+  __shared__ float sx[kPrioRowLanes / 4][2][128 + 4];
+  const int s = blockIdx.x % a.nslab;
+  const int b = (blockIdx.x / a.nslab) % a.B;
+  const int h = blockIdx.x / (a.nslab * a.B);
   const int tid = threadIdx.x;
   const int cg = tid & 15, tl = tid >> 4;
   float mx[8], mn[8];
@@ -31,30 +40,29 @@ __global__ __launch_bounds__(kPrioThreads) void k_head_priority(PriorityArgs a) 
     mx[e] = -INFINITY;
     mn[e] = INFINITY;
   }
-  auto fold = [&](uint4 raw) {
-    const f16x8_t v = __builtin_bit_cast(f16x8_t, raw);
+  for (int r0 = 0; r0 < kPrioSlab; r0 += kPrioRowLanes * kPrioLoads) {
+    const int t0 = s * kPrioSlab + r0 + tl;
+    if (t0 >= a.N) break;
+    const uint4* rows = a.k + (((long)b * a.Hkv + h) * a.N + t0) * 16 + cg;
+    uint4 raw[kPrioLoads];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      mx[e] = fmaxf(mx[e], (float)v[e]);
-      mn[e] = fminf(mn[e], (float)v[e]);
+    for (int u = 0; u < kPrioLoads; ++u)  // rows past N read as -inf (max) and are skipped (min)
+      raw[u] = t0 + kPrioRowLanes * u < a.N
+                   ? rows[(long)u * kPrioRowLanes * 16]
+                   : make_uint4(0xfc00fc00u, 0xfc00fc00u, 0xfc00fc00u, 0xfc00fc00u);
+#pragma unroll
+    for (int u = 0; u < kPrioLoads; ++u) {
+      const bool ok = t0 + kPrioRowLanes * u < a.N;
+      const f16x8_t v = __builtin_bit_cast(f16x8_t, raw[u]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        mx[e] = fmaxf(mx[e], (float)v[e]);
+        mn[e] = ok ? fminf(mn[e], (float)v[e]) : mn[e];
+      }
     }
-  };
-  for (int b = 0; b < a.B; ++b) {
-    const uint4* rows = a.k + ((long)b * a.Hkv + h) * a.N * 16 + cg;
-    int t = tl;
-    for (; t + 3 * kPrioTokenLanes < a.N; t += 4 * kPrioTokenLanes) {
-      const uint4 r0 = rows[(long)t * 16];
-      const uint4 r1 = rows[(long)(t + kPrioTokenLanes) * 16];
-      const uint4 r2 = rows[(long)(t + 2 * kPrioTokenLanes) * 16];
-      const uint4 r3 = rows[(long)(t + 3 * kPrioTokenLanes) * 16];
-      fold(r0);
-      fold(r1);
-      fold(r2);
-      fold(r3);
-    }
-    for (; t < a.N; t += kPrioTokenLanes) fold(rows[(long)t * 16]);
   }
-  // merge the 64 token lanes: four at a time through LDS
+  // merge the 16 row lanes: the four of a wave by lane exchanges, the four
+  // waves through LDS
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 16));
@@ -62,14 +70,54 @@ __global__ __launch_bounds__(kPrioThreads) void k_head_priority(PriorityArgs a) 
     mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 32));
     mn[e] = fminf(mn[e], __shfl_xor(mn[e], 32));
   }
-  // lanes 0..15 of each wave now hold the wave's 4 token lanes merged
   const int wv = tid >> 6;
   if ((tid & 63) < 16) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      smax[wv][8 * cg + e] = mx[e];
-      smin[wv][8 * cg + e] = mn[e];
+      sx[wv][0][8 * cg + e] = mx[e];
+      sx[wv][1][8 * cg + e] = mn[e];
     }
+  }
+  __syncthreads();
+  // thread j: channel j & 127, maximum (j < 128) or minimum
+  const int c = tid & 127, w = tid >> 7;
+  float r = sx[0][w][c];
+#pragma unroll
+  for (int l = 1; l < 4; ++l) r = w ? fminf(r, sx[l][w][c]) : fmaxf(r, sx[l][w][c]);
+  a.ws[((long)h * a.B * a.nslab + (long)b * a.nslab + s) * 256 + tid] = r;
+}
+
+__global__ __launch_bounds__(1024) void k_head_priority_final(PriorityArgs a) {
+  __shared__ float part[4][256];
+  __shared__ float cm[256];
+  const int h = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int j = tid & 255, q = tid >> 8;  // statistic j of slabs q, q + 4, ...
+  const int w = j >> 7;                   // 0: maxima, 1: minima
+  const long n = (long)a.B * a.nslab;
+  const float* src = a.ws + (long)h * n * 256 + j;
+  constexpr int kU = 8;  // loads in flight per thread
+  float r[kU];
+#pragma unroll
+  for (int u = 0; u < kU; ++u) r[u] = w ? INFINITY : -INFINITY;
+  long i = q;
+  for (; i + 4 * (kU - 1) < n; i += 4 * kU) {
+    float x[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) x[u] = src[(i + 4 * u) * 256];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) r[u] = w ? fminf(r[u], x[u]) : fmaxf(r[u], x[u]);
+  }
+  for (; i < n; i += 4) r[0] = w ? fminf(r[0], src[i * 256]) : fmaxf(r[0], src[i * 256]);
+#pragma unroll
+  for (int u = 1; u < kU; ++u) r[0] = w ? fminf(r[0], r[u]) : fmaxf(r[0], r[u]);
+  part[q][j] = r[0];
+  __syncthreads();
+  if (tid < 256) {
+    float v = part[0][tid];
+#pragma unroll
+    for (int u = 1; u < 4; ++u) v = w ? fminf(v, part[u][tid]) : fmaxf(v, part[u][tid]);
+    cm[tid] = v;
   }
   __syncthreads();
   if (tid < 64) {
@@ -77,13 +125,8 @@ __global__ __launch_bounds__(kPrioThreads) void k_head_priority(PriorityArgs a) 
     float gap[2], cmax[2], cmin[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int c = tid + 64 * u;
-      cmax[u] = -INFINITY;
-      cmin[u] = INFINITY;
-      for (int l = 0; l < kPrioTokenLanes / 4; ++l) {
-        cmax[u] = fmaxf(cmax[u], smax[l][c]);
-        cmin[u] = fminf(cmin[u], smin[l][c]);
-      }
+      cmax[u] = cm[tid + 64 * u];
+      cmin[u] = cm[128 + tid + 64 * u];
       gap[u] = cmax[u] - cmin[u];
     }
     const float gmax = wave_max(fmaxf(cmax[0], cmax[1]));
@@ -98,8 +141,16 @@ __global__ __launch_bounds__(kPrioThreads) void k_head_priority(PriorityArgs a) 
   }
 }
 
+size_t head_priority_ws_bytes(int B, int Hkv, int N) {
+  const long nslab = (N + kPrioSlab - 1) / kPrioSlab;
+  return (size_t)Hkv * B * nslab * 256 * sizeof(float);
+}
+
 hipError_t launch_head_priority(const PriorityArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(k_head_priority, dim3(a.Hkv), dim3(kPrioThreads), 0, stream, a);
+  hipLaunchKernelGGL(k_head_minmax, dim3(a.Hkv * a.B * a.nslab), dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_head_priority_final, dim3(a.Hkv), dim3(1024), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -3,11 +3,11 @@
 //   * k_probe_mfma_i8: every wave runs chains of v_mfma_i32_16x16x64_i8 on
 //     register operands -- the int8 matrix-core rate with no memory traffic
 //     and no VALU work between the MFMAs;
-//   * k_probe_read: a grid-stride streaming read of a device buffer (16-byte
+//   * k_probe_read: a streaming read of a device buffer (nontemporal 16-byte
 //     loads, eight in flight per thread) -- the HBM read rate a kernel that
 //     only reads can reach.
-// Each folds its results into one word per work-group so nothing is
-// eliminated, and that word is written.
+// Each folds what it computes or reads into a word that a store depends on,
+// so nothing is eliminated.
 #include "turbo_common.h"
 
 namespace turbo {
@@ -34,29 +34,28 @@ __global__ __launch_bounds__(256, 2) void k_probe_mfma_i8(int iters, int* sink) 
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
+// Each work-group reads one contiguous chunk of 256 x 8 x 16 bytes, eight
+// nontemporal 16-byte loads per thread in flight (of the shapes tried --
+// grid-stride loops of 4 to 16 loads per thread over 1k to 32k work-groups,
+// chunks of 1 to 16 loads, cached and nontemporal -- the fastest).
+constexpr int kProbeReadU = 8;
+
 __global__ __launch_bounds__(256) void k_probe_read(const u32x4* src, long n16, unsigned* sink) {
-  const long stride = (long)gridDim.x * blockDim.x;
-  long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long base = (long)blockIdx.x * 256 * kProbeReadU + threadIdx.x;
+  u32x4 v[kProbeReadU];
+#pragma unroll
+  for (int u = 0; u < kProbeReadU; ++u)
+    v[u] = base + 256L * u < n16 ? __builtin_nontemporal_load(src + base + 256L * u)
+                                 : u32x4{0, 0, 0, 0};
   unsigned x = 0;
-  for (; i + 7 * stride < n16; i += 8 * stride) {
-    u32x4 v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(src + i + u * stride);
-#pragma unroll
-    for (int u = 0; u < 8; ++u) x ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
-  }
-  for (; i < n16; i += stride) {
-    const u32x4 v = src[i];
-    x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
-  }
-  x = (unsigned)wave_max_i((int)x);
-  if ((threadIdx.x & 63) == 0) sink[blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6)] = x;
+  for (int u = 0; u < kProbeReadU; ++u) x ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+  // keeps the loads: a store that depends on every word read
+  if (x == 0x9E3779B9u) sink[0] = x;
 }
 
-// Work-groups of the probes: two per CU for the MFMA loop (8 waves per CU,
-// two per SIMD), eight per CU for the read.
+// Work-groups of the MFMA probe: two per CU (8 waves per CU, two per SIMD).
 constexpr int kProbeMfmaBlocks = 512;
-constexpr int kProbeReadBlocks = 2048;
 
 hipError_t launch_probe_mfma_i8(int iters, int* sink, hipStream_t stream) {
   hipLaunchKernelGGL(k_probe_mfma_i8, dim3(kProbeMfmaBlocks), dim3(256), 0, stream, iters, sink);
@@ -64,8 +63,10 @@ hipError_t launch_probe_mfma_i8(int iters, int* sink, hipStream_t stream) {
 }
 
 hipError_t launch_probe_read(const void* src, size_t bytes, unsigned* sink, hipStream_t stream) {
-  hipLaunchKernelGGL(k_probe_read, dim3(kProbeReadBlocks), dim3(256), 0, stream,
-                     static_cast<const u32x4*>(src), (long)(bytes / 16), sink);
+  const long n16 = (long)(bytes / 16);
+  const long blocks = (n16 + 256 * kProbeReadU - 1) / (256 * kProbeReadU);
+  hipLaunchKernelGGL(k_probe_read, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     static_cast<const u32x4*>(src), n16, sink);
   return hipGetLastError();
 }
 

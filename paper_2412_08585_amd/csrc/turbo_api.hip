@@ -486,12 +486,21 @@ int turbo_attn_decode_trace(const void* q, const turbo_kv_cache* cache,
                           static_cast<unsigned char*>(trace), tb, th, tg, stream);
 }
 
-int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, float* priority,
-                        hipStream_t stream) {
+size_t turbo_head_priority_workspace_bytes(int B, int Hkv, int N) {
+  if (B < 1 || Hkv < 1 || N < 1) return 0;
+  return turbo::head_priority_ws_bytes(B, Hkv, N);
+}
+
+int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, void* workspace,
+                        size_t workspace_bytes, float* priority, hipStream_t stream) {
   if (B < 0 || N < 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || d != TURBO_HEAD_DIM)
     return TURBO_ERR_INVALID_ARG;
   if (!k || !priority || B == 0 || N == 0) return TURBO_ERR_INVALID_ARG;
-  if ((long)B * Hkv * N > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
+  const long nslab = (N + turbo::kPrioSlab - 1) / turbo::kPrioSlab;
+  if ((long)B * Hkv * N > 0x7fffffffL || (long)Hkv * B * nslab > 0x7fffffffL)
+    return TURBO_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < turbo::head_priority_ws_bytes(B, Hkv, N))
+    return TURBO_ERR_WORKSPACE_TOO_SMALL;
   int st = check_device();
   if (st != TURBO_OK) return st;
   turbo::PriorityArgs a{};
@@ -499,6 +508,8 @@ int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, float* prio
   a.B = B;
   a.Hkv = Hkv;
   a.N = N;
+  a.nslab = (int)nslab;
+  a.ws = static_cast<float*>(workspace);
   a.priority = priority;
   return turbo::launch_head_priority(a, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
 }
@@ -605,7 +616,7 @@ int turbo_probe_mfma_i8(int iters, int* sink, int64_t* ops, hipStream_t stream) 
 }
 
 int turbo_probe_read(const void* src, size_t bytes, unsigned* sink, hipStream_t stream) {
-  if (!src || !sink || bytes < 16 || bytes % 16 != 0 ||
+  if (!src || !sink || bytes < 16 || bytes % 16 != 0 || bytes > (size_t(1) << 40) ||
       reinterpret_cast<uintptr_t>(src) % 16 != 0)
     return TURBO_ERR_INVALID_ARG;
   const int st = check_device();

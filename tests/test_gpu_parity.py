@@ -542,6 +542,9 @@ PRIORITY_CASES = [
     (2, 8, 200, [1, 4, 6, 7]),
     (1, 3, 1, [2]),
     (3, 10, 64 * 5 + 13, [0, 3, 5, 8, 9]),
+    (2, 2, 257, [1]),         # one row past a 256-token slab
+    (1, 4, 256 * 3, [0, 2]),  # whole slabs only
+    (1, 3, 700, [2]),         # a slab ending inside a batch of rows
 ]
 
 

@@ -195,9 +195,14 @@ def test_int2_heads_rule_matches_the_oracle(ta, orc):
     assert L.turbo_int2_heads(None, 4, 2, out.ctypes.data_as(P)) == -1
     # head priority: empty input and bad shapes are rejected before any launch
     dummy = P(16)
-    assert L.turbo_head_priority(dummy, 0, 4, 64, 128, dummy, None) == -1
-    assert L.turbo_head_priority(dummy, 1, 4, 64, 64, dummy, None) == -1
-    assert L.turbo_head_priority(None, 1, 4, 64, 128, dummy, None) == -1
+    assert L.turbo_head_priority(dummy, 0, 4, 64, 128, dummy, 1 << 20, dummy, None) == -1
+    assert L.turbo_head_priority(dummy, 1, 4, 64, 64, dummy, 1 << 20, dummy, None) == -1
+    assert L.turbo_head_priority(None, 1, 4, 64, 128, dummy, 1 << 20, dummy, None) == -1
+    # workspace: [Hkv][B * ceil(N / 256)][256] fp32
+    assert L.turbo_head_priority_workspace_bytes(4, 10, 4096) == 10 * 4 * 16 * 256 * 4
+    assert L.turbo_head_priority_workspace_bytes(2, 3, 257) == 3 * 2 * 2 * 256 * 4
+    assert L.turbo_head_priority(dummy, 2, 3, 257, 128, dummy, 3 * 2 * 2 * 256 * 4 - 1, dummy,
+                                 None) == -3
 
 
 def test_decode_split_and_workspace(ta):
