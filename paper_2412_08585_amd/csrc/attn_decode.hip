@@ -72,18 +72,18 @@ constexpr int kWsO = 4;
 // four equal chunks beyond.  It depends on the sequence alone, so a
 // sequence's result does not depend on the batch it is decoded in.
 __host__ __device__ constexpr int decode_default_split(int ng) {
-  return ng <= 32 ? (ng > 0 ? ng : 1) : (ng <= 128 ? 32 : (ng + 3) / 4);
+  return ng <= 32 ? (ng > 0 ? ng : 1) : (ng <= 128 ? 32 : ceil_div(ng, 4));
 }
 
 // Chunks of a sequence with ng groups (chunk length split > 0 or the
 // default rule), and the most any sequence of at most max_groups groups has.
 __host__ __device__ constexpr int decode_chunks(int ng, int split) {
-  return ng <= 0 ? 0 : (ng + (split > 0 ? split : decode_default_split(ng)) - 1) /
-                           (split > 0 ? split : decode_default_split(ng));
+  return ng <= 0 ? 0 : ceil_div(ng, split > 0 ? split : decode_default_split(ng));
 }
 __host__ __device__ constexpr int decode_max_chunks(int max_groups, int split) {
-  return split > 0 ? (max_groups + split - 1) / split
-                   : (max_groups <= 32 ? 1 : (max_groups <= 128 ? (max_groups + 31) / 32 : 4));
+  return max_groups <= 0 ? 0
+         : split > 0     ? ceil_div(max_groups, split)
+                         : (max_groups <= 32 ? 1 : (max_groups <= 128 ? ceil_div(max_groups, 32) : 4));
 }
 
 // The cached groups and buffered tokens decode attends for sequence b.

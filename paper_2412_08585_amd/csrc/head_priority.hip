@@ -142,7 +142,7 @@ __global__ __launch_bounds__(1024) void k_head_priority_final(PriorityArgs a) {
 }
 
 size_t head_priority_ws_bytes(int B, int Hkv, int N) {
-  const long nslab = (N + kPrioSlab - 1) / kPrioSlab;
+  const long nslab = ceil_div(N, kPrioSlab);
   return (size_t)Hkv * B * nslab * 256 * sizeof(float);
 }
 

@@ -135,7 +135,7 @@ int turbo_quantize_kv(const void* k, const void* v, int B, int Hkv, int N, int d
   a.v = static_cast<const uint4*>(v);
   a.Hkv = Hkv;
   a.N = N;
-  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.nb = turbo::ceil_div(N, TURBO_BLOCK);
   a.bc = TURBO_BLOCK;
   a.nbc = a.nb;
   a.k8 = k8;
@@ -163,9 +163,9 @@ int turbo_quantize_kv_blocks(const void* k, const void* v, int B, int Hkv, int N
   a.v = static_cast<const uint4*>(v);
   a.Hkv = Hkv;
   a.N = N;
-  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.nb = turbo::ceil_div(N, TURBO_BLOCK);
   a.bc = block_cols;
-  a.nbc = (N + block_cols - 1) / block_cols;
+  a.nbc = turbo::ceil_div(N, block_cols);
   a.k8 = k8;
   a.v8 = v8;
   a.sk = s_k;
@@ -187,7 +187,7 @@ static int attn_prefill_impl(const void* q, const int8_t* q8, const float* s_q,
   if (block_rows != 32 && block_rows != 64 && block_rows != 128) return TURBO_ERR_INVALID_ARG;
   if (block_cols != 32 && block_cols != 64 && block_cols != 128) return TURBO_ERR_INVALID_ARG;
   if (q8 && (block_rows != 64 || block_cols != 64)) return TURBO_ERR_INVALID_ARG;
-  const long tiles = (long)B * Hq * ((N + block_rows - 1) / block_rows);
+  const long tiles = (long)B * Hq * (turbo::ceil_div(N, block_rows));
   if (tiles > 0x7fffffffL) return TURBO_ERR_INVALID_ARG;
   int st = check_device();
   if (st != TURBO_OK) return st;
@@ -203,11 +203,11 @@ static int attn_prefill_impl(const void* q, const int8_t* q8, const float* s_q,
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.N = N;
-  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.nb = turbo::ceil_div(N, TURBO_BLOCK);
   a.waves = block_rows / 32;
-  a.nbq = (N + block_rows - 1) / block_rows;
+  a.nbq = turbo::ceil_div(N, block_rows);
   a.bc = block_cols;
-  a.nbc = (N + block_cols - 1) / block_cols;
+  a.nbc = turbo::ceil_div(N, block_cols);
   a.sm_scale = sm_scale;
   a.causal = causal ? 1 : 0;
   a.o = static_cast<uint2*>(o);
@@ -252,7 +252,7 @@ static int qkv_project_impl(const void* x, const void* w, int B, int N, int D, i
     return TURBO_ERR_INVALID_ARG;
   if (B == 0 || N == 0) return TURBO_OK;
   if (!x || !w || !q8 || !s_q || !k8 || !v8 || !s_k || !s_v) return TURBO_ERR_INVALID_ARG;
-  const long ntile = (N + 255) / 256;
+  const long ntile = turbo::ceil_div(N, 256);
   if ((long)B * ntile * (Hq + 2 * Hkv) > 0x7fffffffL || (long)B * N > 0x7fffffffL)
     return TURBO_ERR_INVALID_ARG;
   turbo::QkvArgs a{};
@@ -279,7 +279,7 @@ static int qkv_project_impl(const void* x, const void* w, int B, int N, int D, i
   a.D = D;
   a.Hq = Hq;
   a.Hkv = Hkv;
-  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.nb = turbo::ceil_div(N, TURBO_BLOCK);
   a.ntile = (int)ntile;
   a.q8 = q8;
   a.sq = s_q;
@@ -316,8 +316,8 @@ int turbo_attn_prefill_blocks_trace(const void* q, const int8_t* k8, const int8_
                                     int tj, void* trace, hipStream_t stream) {
   if (block_rows != 32 && block_rows != 64 && block_rows != 128) return TURBO_ERR_INVALID_ARG;
   if (block_cols != 32 && block_cols != 64 && block_cols != 128) return TURBO_ERR_INVALID_ARG;
-  const int nbq = N > 0 ? (N + block_rows - 1) / block_rows : 0;
-  const int nbc = N > 0 ? (N + block_cols - 1) / block_cols : 0;
+  const int nbq = N > 0 ? turbo::ceil_div(N, block_rows) : 0;
+  const int nbc = N > 0 ? turbo::ceil_div(N, block_cols) : 0;
   if (!trace || tb < 0 || tb >= B || th < 0 || th >= Hq || ti < 0 || ti >= nbq || tj < 0 ||
       tj >= nbc)
     return TURBO_ERR_INVALID_ARG;
@@ -496,7 +496,7 @@ int turbo_head_priority(const void* k, int B, int Hkv, int N, int d, void* works
   if (B < 0 || N < 0 || Hkv < 1 || Hkv > TURBO_MAX_KV_HEADS || d != TURBO_HEAD_DIM)
     return TURBO_ERR_INVALID_ARG;
   if (!k || !priority || B == 0 || N == 0) return TURBO_ERR_INVALID_ARG;
-  const long nslab = (N + turbo::kPrioSlab - 1) / turbo::kPrioSlab;
+  const long nslab = turbo::ceil_div(N, turbo::kPrioSlab);
   if ((long)B * Hkv * N > 0x7fffffffL || (long)Hkv * B * nslab > 0x7fffffffL)
     return TURBO_ERR_INVALID_ARG;
   if (!workspace || workspace_bytes < turbo::head_priority_ws_bytes(B, Hkv, N))
@@ -563,7 +563,7 @@ int turbo_tail_init(const void* k, const void* v, int B, int Hkv, int N, int d, 
   a.sv = s_v;
   a.Hkv = Hkv;
   a.N = N;
-  a.nb = (N + TURBO_BLOCK - 1) / TURBO_BLOCK;
+  a.nb = turbo::ceil_div(N, TURBO_BLOCK);
   a.tk = tail->k;
   a.tv = tail->v;
   a.tscale = tail->scale;

@@ -17,6 +17,9 @@ typedef unsigned short u16;
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 
+// ceil(a / b) for a >= 0, b > 0, without overflow near INT_MAX.
+__host__ __device__ constexpr int ceil_div(int a, int b) { return a / b + (a % b != 0); }
+
 // Symmetric int8 divisor of Algorithms 1 and 2.
 constexpr float kQmax = 119.0f;
 // 1.5 * 2^23: adding it to a value of magnitude < 2^22 leaves the value

@@ -420,15 +420,59 @@ def test_prefill_rescale_paths(orc, ta, dev, case, causal, br):
     _cmp_lse(lse, rl, f"prefill rescale {case} lse")
 
 
+def _bits_of(t):
+    return t.detach().contiguous().view(torch.uint8).cpu()
+
+
 def test_determinism(ta, dev):
-    N = 64 * 4 + 9
-    q, k, v = _rand((2, 4, N, 128), 1), _rand((2, 2, N, 128), 2), _rand((2, 2, N, 128), 3)
-    outs = []
+    """Two runs of the whole path on the same inputs give the same bytes:
+    quantization and cache, prefill (and its Table 3 variant), decode (split
+    and unsplit, with and without the int8 buffer, also the allocation-free
+    entry point), buffer appends with a flush, the fused projection, the
+    head priority and the SAS softmax."""
+    N, B, Hq, Hkv = 64 * 4 + 9, 2, 4, 2
+    q, k, v = _rand((B, Hq, N, 128), 1), _rand((B, Hkv, N, 128), 2), _rand((B, Hkv, N, 128), 3)
+    qd = _rand((B, Hq, 128), 4).to(dev)
+    kn, vn = _rand((B, Hkv, 128), 5).to(dev), _rand((B, Hkv, 128), 6).to(dev)
+    x = _rand((B, N, 128), 7).to(dev)
+    w = (_rand(((Hq + 2 * Hkv) * 128, 128), 8).float() / 11).half().to(dev)
+    sx = (torch.randn(33, 5000, generator=torch.Generator().manual_seed(9)) * 2).to(dev)
+    mg = N // 64 + 1
+    bt, gt = _tables(B, mg, 10)
+    btd, gtd = torch.from_numpy(bt).to(dev), torch.from_numpy(gt).to(dev)
+    runs = []
     for _ in range(2):
-        k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev))
-        o = ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv)
-        outs.append(o.cpu())
-    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+        out = []
+        cache = ta.PagedKVCache(bt.size, gt.size, [4, 2], dev)
+        k8, v8, sk, sv = ta.turbo_quantize_kv(k.to(dev), v.to(dev), cache, btd, gtd)
+        out += [k8, v8, sk, sv, cache.pages, cache.group_meta, cache.group_scale]
+        out.append(ta.turbo_attn_prefill(q.to(dev), k8, v8, sk, sv))
+        k8b, v8b, skb, svb = ta.turbo_quantize_kv(k.to(dev), v.to(dev), block_cols=32)
+        out.append(ta.turbo_attn_prefill(q.to(dev), k8b, v8b, skb, svb, block_rows=128,
+                                         block_cols=32))
+        tail = ta.KVTail(B, Hkv, dev)
+        ta.turbo_tail_init(k.to(dev), v.to(dev), sk, sv, tail)
+        sl = torch.tensor([N, 64 * 3 + 1], dtype=torch.int32, device=dev)
+        for split in (0, 1):
+            out += list(ta.turbo_attn_decode(qd, cache, sl, btd, gtd, None, split,
+                                             return_lse=True))
+            out += list(ta.turbo_attn_decode(qd, cache, sl, btd, gtd, None, split,
+                                             return_lse=True, tail=tail))
+            out += list(ta.turbo_attn_decode_noalloc(qd, cache, sl, btd, gtd, None, split,
+                                                     return_lse=True, tail=tail))
+        for _step in range(60):  # crosses a flush of both sequences
+            ta.turbo_append_kv(kn, vn, sl, cache, tail, btd, gtd)
+            sl += 1
+        out += [cache.pages, cache.group_meta, cache.group_scale, tail.k, tail.v, tail.scale]
+        out += list(ta.turbo_attn_decode(qd, cache, sl, btd, gtd, None, 0, return_lse=True,
+                                         tail=tail))
+        out += list(ta.turbo_qkv_project(x, w, Hq, Hkv))
+        out.append(ta.turbo_head_priority(k.to(dev)))
+        out.append(ta.turbo_sas_softmax(sx))
+        torch.cuda.synchronize()
+        runs.append([_bits_of(t) for t in out])
+    for i, (a, b) in enumerate(zip(*runs)):
+        assert torch.equal(a, b), f"output {i} differs between runs"
 
 
 # ---- full-size workloads (launch configuration of the benchmark) -----------
