@@ -602,7 +602,11 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
   for (int cb = 0; cb < 8; ++cb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) O[cb][r] = 0.0f;
-  float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f, rbeta = 1.0f;  // rbeta ~ 1 / beta
+  // The running maximum starts at -FLT_MAX rather than -inf: SAS of
+  // m_new - (-FLT_MAX) is 0 as SAS(+inf) is, masked scores (-inf) still give
+  // +inf and 0, and a row that has seen no key never reaches its maximum
+  // (so the test below needs no separate -inf check).
+  float mrow = -0x1.fffffep127f, lpart = 0.0f, beta = 1.0f, rbeta = 1.0f;  // rbeta ~ 1 / beta
   // 119 / pmax of the last tile that computed it, as wave-uniform bits
   unsigned pmax_prev = 0xffffffffu, inv_prev = 0u;
   float skj = skp[0], svj = svp[0];
@@ -645,13 +649,13 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
       }
     }
     // ---- scores, online max, SAS (Algorithm 1, statistics step) --------
-    // (S read as float - seed) * (c 2^26) = float(S) * c, rounded once
-    const float c26 = (sq * skj) * sm26;
+    // (seed - S read as float) * (-c 2^26) = float(S) * c, rounded once
+    const float nc26 = -((sq * skj) * sm26);
     float P[4][4];
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) P[mb][r] = acc_unseed(S[mb][r]) * c26;
+      for (int r = 0; r < 4; ++r) P[mb][r] = acc_unseed_neg(S[mb][r]) * nc26;
     // masking on the diagonal tile and where keys or rows reach past N
     if ((a.causal && 64 * j + 63 > row0) || (64 * j + 64 > N) || (row0 + 16 > N)) {
 #pragma unroll
@@ -668,14 +672,15 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) smax = fmaxf(smax, P[mb][r]);
-    smax = max_xor32(max_xor16_nn(smax));
+    // scores and maxima are never NaN: maxima without canonicalization
+    smax = max_xor32_nn(max_xor16_nn(smax));
     const float mold = mrow;
-    const float mnew = fmaxf(mold, smax);
+    const float mnew = max_nn(mold, smax);
     // A row whose maximum over this tile reaches its running maximum holds a
     // score with y = 0, whose P~ is SAS(0) = c0, and no P~ exceeds c0 (LUT[k]
     // <= 1 and POLY is decreasing from c0 on [0, 1)): the wave's P~ maximum
     // is then c0 without a reduction.
-    const bool top = __builtin_amdgcn_ballot_w64(smax >= mold && smax != -INFINITY) != 0;
+    const bool top = __builtin_amdgcn_ballot_w64(smax >= mold) != 0;
     float rs;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
@@ -694,17 +699,18 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     const bool moved = __builtin_amdgcn_ballot_w64(mnew > mold) != 0;
     float alpha = 1.0f;
     if (moved) alpha = mnew > mold ? sas_y(mnew - mold, L.lut) : 1.0f;
-    lpart = moved ? alpha * lpart + rs : lpart + rs;
+    lpart = __builtin_fmaf(alpha, lpart, rs);  // alpha = 1: lpart + rs exactly
     mrow = mnew;
     // ---- tile maximum of P~ over the four waves ------------------------
     float pmax = kC0;
     if (!top) {  // wave-uniform
-      pmax = P[0][0];
+      // P~ >= 0: the maximum on the bits (integer order = float order)
+      int pm = __float_as_int(P[0][0]);
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-        for (int r = (mb == 0); r < 4; ++r) pmax = fmaxf(pmax, P[mb][r]);
-      pmax = wave_max_pos(pmax);  // P~ >= 0
+        for (int r = (mb == 0); r < 4; ++r) pm = max(pm, __float_as_int(P[mb][r]));
+      pmax = wave_max_pos(__int_as_float(pm));
     }
     if (lane == 0) L.xmax[buf][w] = pmax;
     __syncthreads();
@@ -740,7 +746,7 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     // s_P = pmax / 119 only scales O (no code depends on it): the product
     // with the rounded reciprocal is within one ulp of the quotient; the
     // factor 2^26 undoes the accumulator seed
-    const float g26 = ((pmax * (0x1p26f / kQmax)) * svj) * rbeta;
+    const float ng26 = -(((pmax * (0x1p26f / kQmax)) * svj) * rbeta);
     v4i pop;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
@@ -778,7 +784,7 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
       for (int c = 0; c < 4; ++c)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          O[4 * hv + c][r] = __builtin_fmaf(g26, acc_unseed(acc[c][r]), O[4 * hv + c][r]);
+          O[4 * hv + c][r] = __builtin_fmaf(ng26, acc_unseed_neg(acc[c][r]), O[4 * hv + c][r]);
       __builtin_amdgcn_sched_barrier(0);
     }
     *reinterpret_cast<uint4*>(&L.v[buf ^ 1][vdst0]) = vp0;

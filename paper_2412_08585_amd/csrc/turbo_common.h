@@ -40,6 +40,11 @@ constexpr float kAccSeedF = 0x1.45f306p-3f;
 // s * 2^-26 of a seeded accumulator entry (exact).
 __device__ __forceinline__ float acc_unseed(int r) { return __int_as_float(r) - kAccSeedF; }
 
+// -s * 2^-26 (exact): the seed minus the entry, which takes the seed as the
+// inline constant 1/(2 pi) (the subtraction the other way round needs a
+// 32-bit literal).  Callers multiply by the negated factor.
+__device__ __forceinline__ float acc_unseed_neg(int r) { return kAccSeedF - __int_as_float(r); }
+
 // SAS (Sec. 4): e^{-y} ~ LUT[floor y] * POLY(y - floor y) for y = m - s in
 // [0, 6]; zero for y > 6 (n_r = -6, Sec. 5.2).  LUT[k] = e^{-k} rounded to
 // binary32; POLY coefficients as printed in Sec. 4, rounded to binary32.
@@ -138,6 +143,12 @@ __device__ __forceinline__ float max_nn(float a, float b) {
   float r;
   asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
   return r;
+}
+
+__device__ __forceinline__ float max_xor32_nn(float v) {
+  const unsigned u = __float_as_uint(v);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return max_nn(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 __device__ __forceinline__ float max_xor16_nn(float v) {
