@@ -14,79 +14,77 @@
 // same LDS-tile routines as k_quantize_kv.  Q, K and V never reach HBM in
 // fp16.
 //
-// Work split.  A work-group of four waves owns 256 tokens of one sequence and
-// one head (128 features); wave w owns the 64-token FlashQ block w, so the
-// block maximum is a wave reduction.  Per 64-wide step of D, the W slice of
-// the head (128 x 64 fp16) is staged in LDS (two stages) and shared by the
-// four waves; each wave reads its own X rows straight into MFMA registers
-// (one step ahead).  A lane's 32 contiguous halves of a row serve four
-// k16-steps: contraction slot (step s, lane half h, element j) is column
-// 32h + 8s + j of the slice, the same for both operands.
+// Tiling.  A work-group of four waves computes a 256-token x 256-feature tile
+// (two heads).  The contraction runs in stages of 64 columns: the tile's 256
+// X rows and 256 W rows of a stage (128 bytes each) sit in LDS at a 144-byte
+// row pitch, so that the 16 lanes of each operand read hit 16 distinct
+// 4-bank groups.  There are two LDS stages and two register sets: each
+// thread loads its 16 chunks of stage k + 2 into registers at the top of
+// stage k and stores them to LDS at the end of stage k + 1 (one barrier per
+// stage), which gives the loads -- a fifth of which miss the XCD's L2 --
+// about 4k MFMA cycles to land.  Wave (wm, wn) owns tokens
+// 128 wm .. +127 and head wn of the pair: 4 x 4 MFMA blocks of 32 x 32, 256
+// fp32 accumulators per lane, which live in the AGPR file (one wave per SIMD;
+// this file is built as a translation unit of its own, without the VGPR-only
+// MFMA form of the attention kernels).  Every operand byte leaves L2 once per
+// work-group: X is read once per head pair and W once per 256-token tile.
 #include "turbo_common.h"
+#include "quant_tiles.h"
+#include "qkv_project.h"
 
 namespace turbo {
 
 typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
-struct QkvArgs {
-  const uint4* x;  // fp16 [B][N][D]
-  const uint4* w;  // fp16 [F][D]
-  int B, N, D, Hq, Hkv, nb, ntile;
-  int8_t* q8;      // [B][Hq][nb*64][128]
-  float* sq;       // [B][Hq][nb]
-  int8_t* k8;      // [B][Hkv][nb*64][128]
-  int8_t* v8;      // [B][Hkv][nb][128][64]
-  float* sk;       // [B][Hkv][nb]
-  float* sv;
-  // paged cache (pages == nullptr: none)
-  uint8_t* pages;
-  int8_t* gmeta;
-  float* gscale;
-  long num_pages, num_slots;
-  int page_bytes;
-  unsigned long long int2_mask;
-  const int* block_table;  // [B][4*max_groups]
-  const int* group_table;  // [B][max_groups]
-  int max_groups;
-  _Float16* y;     // test hook: the fp16 projection [B][N][F] (null: not written)
-};
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kProjThreads = 256;
-constexpr int kWRow = 144;                   // LDS bytes per W row: 128 + 16 (bank spread)
-constexpr int kWStage = 128 * kWRow;         // one 128 x 64 fp16 slice
-constexpr int kEpiTile = 64 * kTileStride;   // one 64 x 128 int8 block (k_quantize_kv layout)
-constexpr int kQkvLds = (2 * kWStage > 5 * kEpiTile) ? 2 * kWStage : 5 * kEpiTile;
+constexpr int kPRow = 144;               // LDS bytes per staged row: 128 + 16 (bank spread)
+constexpr int kPOp = 256 * kPRow;        // one operand (256 rows) of one stage
+constexpr int kPStage = 2 * kPOp;        // X rows, then W rows
+constexpr int kEpiTile = 64 * kTileStride;  // one 64 x 128 int8 block (k_quantize_kv layout)
+constexpr int kQkvLds = 2 * kPStage;
+static_assert(9 * kEpiTile <= kQkvLds, "the epilogue tiles fit in the stages");
 
 __device__ __forceinline__ f32x16_t mfma_f16(uint4 a, uint4 b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8_t, a),
                                                 __builtin_bit_cast(h8_t, b), c, 0, 0, 0);
 }
 
+// Raw buffer resource over `bytes` bytes at p (gfx9 descriptor word 3: 32-bit
+// data format).  Loads at offsets >= bytes return zeros: the rows past N of
+// the last token tile and past F of an odd head count.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 // Work-group order.  The dispatcher hands work-group x to XCD x % 8.  When
 // the token tiles are a multiple of 8, XCD k owns tiles k, k+8, ... and walks
-// them in blocks of (all its tiles) x (8 heads): the ~64 work-groups resident
-// on an XCD then share 8 X tiles and 8 W heads in its L2, so X is fetched
-// about nheads/8 times and W about ntiles/8 times in all (tile-major order
-// would fetch all of W once per tile).
-__device__ __forceinline__ void qkv_tile(int x, int ntiles, int nheads, int& tile, int& head) {
+// them in blocks of (all its tiles) x (8 head pairs): the 32 work-groups
+// resident on an XCD then share 4 X tiles and 8 W pairs in its L2.
+__device__ __forceinline__ void qkv_tile(int x, int ntiles, int npairs, int& tile, int& pair) {
   if (ntiles % 8 != 0) {
-    head = x % nheads;
-    tile = x / nheads;
+    pair = x % npairs;
+    tile = x / npairs;
     return;
   }
   const int k = x % 8, i = x / 8;
-  const int ntk = ntiles / 8;        // tiles of this XCD
-  const int full = nheads / 8;       // complete groups of 8 heads
+  const int ntk = ntiles / 8;   // tiles of this XCD
+  const int full = npairs / 8;  // complete groups of 8 pairs
   int tl;
   if (i < full * ntk * 8) {
     const int hg = i / (ntk * 8), rem = i % (ntk * 8);
     tl = rem / 8;
-    head = 8 * hg + rem % 8;
+    pair = 8 * hg + rem % 8;
   } else {
-    const int r = nheads - 8 * full, rem = i - full * ntk * 8;
+    const int r = npairs - 8 * full, rem = i - full * ntk * 8;
     tl = rem / r;
-    head = 8 * full + rem % r;
+    pair = 8 * full + rem % r;
   }
   tile = tl * 8 + k;
 }
@@ -94,220 +92,275 @@ __device__ __forceinline__ void qkv_tile(int x, int ntiles, int nheads, int& til
 // kY = true only for the test hook that also stores the fp16 projection
 // (the production instance carries no such store).
 template <bool kY>
-__global__ __launch_bounds__(kProjThreads, 2) void k_qkv_project(QkvArgs a) {
+__global__ __launch_bounds__(kProjThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void
+k_qkv_project(QkvArgs a) {
   __shared__ __align__(16) uint8_t lds[kQkvLds];
-  __shared__ float sblk[4];
+  __shared__ float sblk[8];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int h = lane >> 5, m = lane & 31;
+  const int wm = wv & 1, wn = wv >> 1;
+  const int m = lane & 31, hh = lane >> 5;
   const int nheads = a.Hq + 2 * a.Hkv;
-  int tile, head;
-  qkv_tile(blockIdx.x, a.B * a.ntile, nheads, tile, head);
+  const int npairs = ceil_div(nheads, 2);
+  const int F = 128 * nheads;
+  int tile, pair;
+  qkv_tile(blockIdx.x, a.B * a.ntile, npairs, tile, pair);
   const int b = tile / a.ntile;
-  const int t0 = (tile % a.ntile) * 256;
-  const int n0 = t0 + 64 * wv;  // first token of this wave's block
-  const int dq = a.D / 8;       // uint4 per row
+  const int t0 = (tile % a.ntile) * kQkvTileTokens;
 
-  // this lane's two X rows (clamped into the sequence; rows >= N are masked
-  // out in the epilogue) and the W row it stages
-  const uint4* xr[2];
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int n = min(n0 + 32 * mb + m, a.N - 1);
-    xr[mb] = a.x + ((long)b * a.N + n) * dq + 4 * h;
-  }
-  // W staging: thread (row 32 j + tid/8, 16-byte chunk tid%8) for j = 0..3, so
-  // one load instruction reads 8 whole 128-byte rows of the slice
-  const int wrow = tid >> 3, wc = tid & 7;
-  const uint4* wr = a.w + ((long)head * 128 + wrow) * dq + wc;
-  const long wj = 32L * dq;  // 32 rows
-  uint8_t* wdst = lds + wrow * kWRow + 16 * wc;
+  // ---- staging: thread (row sr + 32 j, 16-byte chunk sc), j = 0..7 ---------
+  // one load instruction reads 8 whole 128-byte rows of a stage
+  const int sr = tid >> 3, sc = tid & 7;
+  const unsigned D2 = 2u * (unsigned)a.D;  // bytes per row
+  const __amdgpu_buffer_rsrc_t xrs =
+      rows_rsrc(static_cast<const _Float16*>(a.x) + (long)b * a.N * a.D, a.N * (int)D2);
+  const __amdgpu_buffer_rsrc_t wrs = rows_rsrc(a.w, F * (int)D2);
+  const unsigned lv = (unsigned)sr * D2 + 16u * (unsigned)sc;  // lane part of both offsets
+  const unsigned xs0 = (unsigned)t0 * D2, ws0 = (unsigned)(256 * pair) * D2;
+  const unsigned sj = 32u * D2;  // 32 rows
+  const int sdst = sr * kPRow + 16 * sc;
 
-  f32x16_t acc[2][4];
+  // two register sets of a stage's 16 chunks (8 X, then 8 W): the loads of
+  // stage k + 2 are issued at the top of stage k and land in LDS at the end
+  // of stage k + 1, two stages (~4k MFMA cycles) later
+  uint4 g[2][16];
+  auto gload = [&](auto setc, int kk) {
+    constexpr int S = decltype(setc)::value;
+    const unsigned kb = 128u * (unsigned)kk;  // 64 fp16 columns per stage
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+    for (int j = 0; j < 8; ++j) {
+      g[S][j] = bload(xrs, lv, xs0 + j * sj + kb);
+      g[S][8 + j] = bload(wrs, lv, ws0 + j * sj + kb);
+    }
+  };
+  auto sstore = [&](auto setc, int st) {
+    constexpr int S = decltype(setc)::value;
+    uint8_t* d = lds + st * kPStage + sdst;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      *reinterpret_cast<uint4*>(d + j * 32 * kPRow) = g[S][j];
+      *reinterpret_cast<uint4*>(d + kPOp + j * 32 * kPRow) = g[S][8 + j];
+    }
+  };
+
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x16_t{};
 
-  // X operands in two half-step register sets: P holds k16-slots 0-1 of a
-  // step, R slots 2-3.  R is loaded at the top of its step and P (for the
-  // next step) after slots 0-1 are done, so each load has half a step of
-  // MFMAs to land, and each set is waited for only when it is used.  The W
-  // slice of the next step is loaded at the top and stored to the other LDS
-  // stage at the end of the step.
-  uint4 P[2][2], R[2][2];
+  // operand reads: A (X rows) row 128 wm + 32 mb + m, B (W rows) row
+  // 128 wn + 32 nb + m; contraction slot (step s, lane half hh, element e) is
+  // column 16 s + 8 hh + e of the stage for both operands
+  const int aA = (128 * wm + m) * kPRow + 16 * hh;
+  const int aB = kPOp + (128 * wn + m) * kPRow + 16 * hh;
+  // one stage: the operands of step s + 1 are read while the 16 MFMAs of
+  // step s run
+  auto compute = [&](int st) {
+    const uint8_t* sa = lds + st * kPStage + aA;
+    const uint8_t* sb = lds + st * kPStage + aB;
+    uint4 A[2][4], Bo[2][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      A[0][i] = *reinterpret_cast<const uint4*>(sa + i * 32 * kPRow);
+      Bo[0][i] = *reinterpret_cast<const uint4*>(sb + i * 32 * kPRow);
+    }
+    // (scheduling fences: the reads of step s + 1 go out before the MFMAs
+    // of step s, which then cover their latency)
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int cu = s & 1, nx = cu ^ 1;
+      if (s < 3) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          A[nx][i] = *reinterpret_cast<const uint4*>(sa + i * 32 * kPRow + 32 * (s + 1));
+          Bo[nx][i] = *reinterpret_cast<const uint4*>(sb + i * 32 * kPRow + 32 * (s + 1));
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma_f16(A[cu][mb], Bo[cu][nb], acc[mb][nb]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
   const int nk = a.D / 64;
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb) P[mb][j] = xr[mb][j];
-  {
-    const uint4 w0 = wr[0], w1 = wr[wj], w2 = wr[2 * wj], w3 = wr[3 * wj];
-    *reinterpret_cast<uint4*>(wdst) = w0;
-    *reinterpret_cast<uint4*>(wdst + 32 * kWRow) = w1;
-    *reinterpret_cast<uint4*>(wdst + 64 * kWRow) = w2;
-    *reinterpret_cast<uint4*>(wdst + 96 * kWRow) = w3;
-  }
+  // every load is issued on every path (the stage index is clamped at the
+  // end), so the waits the compiler places before each use stay exact
+  gload(std::integral_constant<int, 0>{}, 0);
+  sstore(std::integral_constant<int, 0>{}, 0);
+  gload(std::integral_constant<int, 1>{}, min(1, nk - 1));
   __syncthreads();
-  // every load is issued on every path (the index is clamped at the end), so
-  // the waits the compiler places before each use stay exact
-  for (int kk = 0; kk < nk; ++kk) {
-    const int st = kk & 1, kn = min(kk + 1, nk - 1);
-    const uint4* wn = wr + kn * 8;
-    const uint4 w0 = wn[0], w1 = wn[wj], w2 = wn[2 * wj], w3 = wn[3 * wj];
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) R[mb][j] = xr[mb][kk * 8 + 2 + j];
-    // keep the prefetches where they are: issued early, their latency hides
-    // behind MFMAs (the scheduler would otherwise sink them to their use)
+  for (int kk = 0; kk + 1 < nk; kk += 2) {
+    // stage kk from LDS 0; set 0 (free) takes stage kk + 2; set 1 (stage
+    // kk + 1) goes to LDS 1, whose last readers finished before the barrier
+    gload(std::integral_constant<int, 0>{}, min(kk + 2, nk - 1));
+    // keep the prefetch at the top (the scheduler would sink it to its use)
     __builtin_amdgcn_sched_barrier(0);
-    const uint8_t* base = lds + st * kWStage + m * kWRow + 64 * h;
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const uint4 bv = *reinterpret_cast<const uint4*>(base + nb * 32 * kWRow + 16 * s);
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) acc[mb][nb] = mfma_f16(P[mb][s], bv, acc[mb][nb]);
-      }
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) P[mb][j] = xr[mb][kn * 8 + j];
+    compute(0);
+    sstore(std::integral_constant<int, 1>{}, 1);
+    __syncthreads();
+    gload(std::integral_constant<int, 1>{}, min(kk + 3, nk - 1));
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int s = 2; s < 4; ++s)
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const uint4 bv = *reinterpret_cast<const uint4*>(base + nb * 32 * kWRow + 16 * s);
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) acc[mb][nb] = mfma_f16(R[mb][s - 2], bv, acc[mb][nb]);
-      }
-    uint8_t* d = wdst + (st ^ 1) * kWStage;
-    *reinterpret_cast<uint4*>(d) = w0;
-    *reinterpret_cast<uint4*>(d + 32 * kWRow) = w1;
-    *reinterpret_cast<uint4*>(d + 64 * kWRow) = w2;
-    *reinterpret_cast<uint4*>(d + 96 * kWRow) = w3;
+    compute(1);
+    sstore(std::integral_constant<int, 0>{}, 0);
     __syncthreads();
   }
-
-  // ---- epilogue: fp16 outputs, FlashQ step 1 per 64-token block --------------
-  // lane (m, h), register r of (mb, nb) <-> token n0 + 32 mb + 8 (r/4) + 4 h + r%4,
-  // channel 32 nb + m
-  float amax = 0.0f;
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = 32 * mb + 8 * (r >> 2) + 4 * h + (r & 3);
-        const float y = (float)(_Float16)acc[mb][nb][r];
-        acc[mb][nb][r] = y;
-        if (n0 + row < a.N) {
-          amax = fmaxf(amax, fabsf(y));
-          if constexpr (kY)
-            a.y[((long)b * a.N + n0 + row) * (long)(128 * nheads) + 128 * head + 32 * nb + m] =
-                (_Float16)y;
-        }
-      }
-  amax = wave_max_fast(amax);
-  float s = 0.0f, inv = 0.0f;
-  if (amax > 0.0f) {
-    s = amax / kQmax;
-    inv = kQmax / amax;
-  }
-  __syncthreads();  // the W stages are reused as the epilogue tiles
-  int8_t* tile_w = reinterpret_cast<int8_t*>(lds) + wv * kEpiTile;
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = 32 * mb + 8 * (r >> 2) + 4 * h + (r & 3);
-        const int q = n0 + row < a.N ? min(119, max(-119, rne_mul(acc[mb][nb][r], inv))) : 0;
-        tile_w[row * kTileStride + 32 * nb + m] = (int8_t)q;
-      }
-  if (lane == 0) sblk[wv] = s;
+  if (nk & 1) compute(0);  // the last stage of an odd count sits in LDS 0
   __syncthreads();
 
-  const int jb = n0 / 64;  // FlashQ block index of this wave's block
-  const bool live = jb < a.nb;
-  if (head < a.Hq + a.Hkv) {
-    // token-major int8 rows (Q8 or K8) and the block scale
-    const bool isq = head < a.Hq;
-    const int hh = isq ? head : head - a.Hq;
-    const long unit = (long)b * (isq ? a.Hq : a.Hkv) + hh;
-    int8_t* dst = (isq ? a.q8 : a.k8) + (unit * a.nb + jb) * 8192;
-    if (live) {
+  // ---- epilogue: fp16 outputs, FlashQ step 1 per 64-token block --------------
+  // lane (m, hh), register r of (mb, nb) <-> token 128 wm + 32 mb + 8 (r/4) +
+  // 4 hh + r%4 of the tile, channel 32 nb + m of head 2 pair + wn; FlashQ
+  // block i = mb >> 1 of the wave is block 2 wm + i of the tile
+  const int head = 2 * pair + wn;
+  const bool hv = head < nheads;  // wave-uniform (an odd head count leaves one out)
+  // one block at a time (128 accumulators of a lane), which bounds the
+  // registers the AGPR -> VGPR copies take; the stages are free for the tiles
+  // since the loop's last barrier
+  float sc_[2];
+  // block i of the wave: kFull when all its 64 tokens are below N (the
+  // common case: no per-element masking), else rows nv.. are masked out
+  auto block = [&](auto ic, auto fullc) {
+    constexpr int i = decltype(ic)::value;
+    constexpr bool kFull = decltype(fullc)::value;
+    const int nv = a.N - (t0 + 128 * wm + 64 * i);  // valid rows of the block
+    // max |fp16(y)| = fp16(max |y|): rounding is monotone and symmetric, so
+    // the first pass needs no conversion
+    float amax = 0.0f;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int row = 4 * i + (lane >> 4), c8 = lane & 15;
-        *reinterpret_cast<uint2*>(dst + row * 128 + 8 * c8) =
-            *reinterpret_cast<const uint2*>(tile_w + row * kTileStride + 8 * c8);
-      }
-      if (lane == 0) (isq ? a.sq : a.sk)[unit * a.nb + jb] = s;
-    }
-  } else {
-    // channel-major V8 block: lane (channel pair) of each wave writes its
-    // own block
-    const int hh = head - a.Hq - a.Hkv;
-    const long unit = (long)b * a.Hkv + hh;
-    if (live) {
-      int8_t* dst = a.v8 + (unit * a.nb + jb) * 8192;
+    for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-      for (int cc = 0; cc < 2; ++cc) {
-        const int c = 2 * lane + cc;
-        unsigned wd[16];
+      for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int t = 4 * i;
-          wd[i] = pack4(tile_w[t * kTileStride + c], tile_w[(t + 1) * kTileStride + c],
-                        tile_w[(t + 2) * kTileStride + c], tile_w[(t + 3) * kTileStride + c]);
+        for (int r = 0; r < 16; ++r) {
+          const int row = 32 * mi + 8 * (r >> 2) + 4 * hh + (r & 3);
+          amax = fmaxf(amax, (kFull || row < nv) ? fabsf(acc[2 * i + mi][nb][r]) : 0.0f);
+          if constexpr (kY) {
+            if (hv && (kFull || row < nv))
+              a.y[((long)b * a.N + t0 + 128 * wm + 64 * i + row) * (long)F + 128 * head + 32 * nb +
+                  m] = (_Float16)acc[2 * i + mi][nb][r];
+          }
         }
-        uint4* o = reinterpret_cast<uint4*>(dst + c * 64);
+    amax = (float)(_Float16)amax;
+    amax = wave_max_fast(amax);
+    float inv = 0.0f;
+    sc_[i] = 0.0f;
+    if (amax > 0.0f) {
+      sc_[i] = amax / kQmax;
+      inv = kQmax / amax;
+    }
+    int8_t* tw = reinterpret_cast<int8_t*>(lds) + (4 * wn + 2 * wm + i) * kEpiTile;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = make_uint4(wd[4 * i], wd[4 * i + 1], wd[4 * i + 2], wd[4 * i + 3]);
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = 32 * mi + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float y = (float)(_Float16)acc[2 * i + mi][nb][r];
+          const int q = min(119, max(-119, rne_mul(y, inv)));
+          tw[row * kTileStride + 32 * nb + m] = (int8_t)((kFull || row < nv) ? q : 0);
+        }
+    if (lane == 0) sblk[4 * wn + 2 * wm + i] = sc_[i];
+  };
+  // (i a compile-time constant: acc is indexed with it)
+  auto run = [&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+    if (t0 + 128 * wm + 64 * i + 64 <= a.N)  // wave-uniform
+      block(ic, std::true_type{});
+    else
+      block(ic, std::false_type{});
+  };
+  run(std::integral_constant<int, 0>{});
+  // the next block's AGPR reads stay below this point
+  __builtin_amdgcn_sched_barrier(0);
+  run(std::integral_constant<int, 1>{});
+  __syncthreads();
+
+  // ---- Q8 / K8 / V8 and the block scales: each wave its own two tiles --------
+  if (hv) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int8_t* tw = reinterpret_cast<const int8_t*>(lds) + (4 * wn + 2 * wm + i) * kEpiTile;
+      const int jb = (t0 + 128 * wm + 64 * i) / 64;  // FlashQ block index in the sequence
+      if (jb >= a.nb) continue;                      // wave-uniform
+      if (head < a.Hq + a.Hkv) {
+        // token-major int8 rows (Q8 or K8) and the block scale
+        const bool isq = head < a.Hq;
+        const int hq = isq ? head : head - a.Hq;
+        const long unit = (long)b * (isq ? a.Hq : a.Hkv) + hq;
+        int8_t* dst = (isq ? a.q8 : a.k8) + (unit * a.nb + jb) * 8192;
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+          const int row = 4 * it + (lane >> 4), c8 = lane & 15;
+          *reinterpret_cast<uint2*>(dst + row * 128 + 8 * c8) =
+              *reinterpret_cast<const uint2*>(tw + row * kTileStride + 8 * c8);
+        }
+        if (lane == 0) (isq ? a.sq : a.sk)[unit * a.nb + jb] = sc_[i];
+      } else {
+        // channel-major V8 block: lane = channel pair
+        const long unit = (long)b * a.Hkv + (head - a.Hq - a.Hkv);
+        int8_t* dst = a.v8 + (unit * a.nb + jb) * 8192;
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+          const int c = 2 * lane + cc;
+          unsigned wd[16];
+#pragma unroll
+          for (int k = 0; k < 16; ++k) {
+            const int t = 4 * k;
+            wd[k] = pack4(tw[t * kTileStride + c], tw[(t + 1) * kTileStride + c],
+                          tw[(t + 2) * kTileStride + c], tw[(t + 3) * kTileStride + c]);
+          }
+          uint4* o = reinterpret_cast<uint4*>(dst + c * 64);
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            o[k] = make_uint4(wd[4 * k], wd[4 * k + 1], wd[4 * k + 2], wd[4 * k + 3]);
+        }
+        if (lane == 0) a.sv[unit * a.nb + jb] = sc_[i];
       }
-      if (lane == 0) a.sv[unit * a.nb + jb] = s;
     }
   }
 
   // ---- step 2 and the cache write (K and V heads, full blocks) ---------------
-  if (a.pages == nullptr || head < a.Hq) return;  // work-group uniform
-  const bool isk = head < a.Hq + a.Hkv;
-  const int hkv = isk ? head - a.Hq : head - a.Hq - a.Hkv;
-  const int bits = ((a.int2_mask >> hkv) & 1ull) ? 2 : 4;
-  const int head_off = 512 * (4 * hkv - 2 * __popcll(a.int2_mask & ((1ull << hkv) - 1ull)));
-  uint8_t* ctile = lds + 4 * kEpiTile;
-  for (int w = 0; w < 4; ++w) {
-    const int g = (t0 + 64 * w) / 64;
-    if (t0 + 64 * w + 64 > a.N || g >= a.max_groups) break;  // uniform
-    long page[4];
-    bool ok = true;
-    const int* bt = a.block_table + (long)b * 4 * a.max_groups + 4 * g;
+  if (a.pages == nullptr) return;  // work-group uniform
+  uint8_t* ctile = lds + 8 * kEpiTile;
+  for (int hl = 0; hl < 2; ++hl) {
+    const int hd = 2 * pair + hl;
+    if (hd < a.Hq || hd >= nheads) continue;  // work-group uniform
+    const bool isk = hd < a.Hq + a.Hkv;
+    const int hkv = isk ? hd - a.Hq : hd - a.Hq - a.Hkv;
+    const int bits = ((a.int2_mask >> hkv) & 1ull) ? 2 : 4;
+    const int head_off = 512 * (4 * hkv - 2 * __popcll(a.int2_mask & ((1ull << hkv) - 1ull)));
+    for (int w = 0; w < 4; ++w) {
+      const int g = (t0 + 64 * w) / 64;
+      if (t0 + 64 * w + 64 > a.N || g >= a.max_groups) break;  // uniform
+      long page[4];
+      bool ok = true;
+      const int* bt = a.block_table + (long)b * 4 * a.max_groups + 4 * g;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      page[p] = bt[p];
-      ok = ok && page[p] >= 0 && page[p] < a.num_pages;
+      for (int p = 0; p < 4; ++p) {
+        page[p] = bt[p];
+        ok = ok && page[p] >= 0 && page[p] < a.num_pages;
+      }
+      const long slot = a.group_table[(long)b * a.max_groups + g];
+      if (!ok || slot < 0 || slot >= a.num_slots) continue;  // uniform
+      int8_t* meta = a.gmeta + (slot * a.Hkv + hkv) * 512;
+      const int8_t* tb = reinterpret_cast<const int8_t*>(lds) + (4 * hl + w) * kEpiTile;
+      if (isk)
+        compress_k(tb, ctile, bits, meta, a.gscale + (slot * a.Hkv + hkv) * 2 + 0, sblk[4 * hl + w],
+                   page, a.pages, a.page_bytes, head_off);
+      else
+        compress_v(tb, bits, meta, a.gscale + (slot * a.Hkv + hkv) * 2 + 1, sblk[4 * hl + w], page,
+                   a.pages, a.page_bytes, head_off);
+      __syncthreads();
     }
-    const long slot = a.group_table[(long)b * a.max_groups + g];
-    if (!ok || slot < 0 || slot >= a.num_slots) continue;  // uniform
-    int8_t* meta = a.gmeta + (slot * a.Hkv + hkv) * 512;
-    const int8_t* tb = reinterpret_cast<const int8_t*>(lds) + w * kEpiTile;
-    if (isk)
-      compress_k(tb, ctile, bits, meta, a.gscale + (slot * a.Hkv + hkv) * 2 + 0, sblk[w], page,
-                 a.pages, a.page_bytes, head_off);
-    else
-      compress_v(tb, bits, meta, a.gscale + (slot * a.Hkv + hkv) * 2 + 1, sblk[w], page, a.pages,
-                 a.page_bytes, head_off);
-    __syncthreads();
   }
 }
 
 hipError_t launch_qkv_project(const QkvArgs& a, hipStream_t stream) {
-  const int total = a.B * a.ntile * (a.Hq + 2 * a.Hkv);
+  const int total = a.B * a.ntile * ceil_div(a.Hq + 2 * a.Hkv, 2);
   if (a.y)
     hipLaunchKernelGGL(k_qkv_project<true>, dim3(total), dim3(kProjThreads), 0, stream, a);
   else

@@ -15,7 +15,7 @@
 #include "head_priority.hip"
 #include "kv_tail.hip"
 #include "sas_softmax.hip"
-#include "qkv_project.hip"
+#include "qkv_project.h"
 #include "probes.hip"
 
 namespace {
@@ -252,8 +252,12 @@ static int qkv_project_impl(const void* x, const void* w, int B, int N, int D, i
     return TURBO_ERR_INVALID_ARG;
   if (B == 0 || N == 0) return TURBO_OK;
   if (!x || !w || !q8 || !s_q || !k8 || !v8 || !s_k || !s_v) return TURBO_ERR_INVALID_ARG;
-  const long ntile = turbo::ceil_div(N, 256);
-  if ((long)B * ntile * (Hq + 2 * Hkv) > 0x7fffffffL || (long)B * N > 0x7fffffffL)
+  const long ntile = turbo::ceil_div(N, turbo::kQkvTileTokens);
+  const long npairs = turbo::ceil_div(Hq + 2 * Hkv, 2);
+  // the kernel addresses one sequence of X and all of W (rounded up to whole
+  // tiles) with 32-bit byte offsets
+  if ((long)B * ntile * npairs > 0x7fffffffL || (long)B * N > 0x7fffffffL ||
+      ntile * turbo::kQkvTileTokens * 2L * D > 0x7fffffffL || npairs * 256L * 2L * D > 0x7fffffffL)
     return TURBO_ERR_INVALID_ARG;
   turbo::QkvArgs a{};
   if (cache) {
@@ -272,8 +276,8 @@ static int qkv_project_impl(const void* x, const void* w, int B, int N, int D, i
   }
   int st = check_device();
   if (st != TURBO_OK) return st;
-  a.x = static_cast<const uint4*>(x);
-  a.w = static_cast<const uint4*>(w);
+  a.x = x;
+  a.w = w;
   a.B = B;
   a.N = N;
   a.D = D;

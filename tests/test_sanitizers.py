@@ -43,15 +43,17 @@ def test_abi_host_side_under_asan_ubsan(tmp_path):
     host_san = [x for f in SAN + ["-fno-omit-frame-pointer"] for x in ("-Xarch_host", f)]
     inc = ["-I", os.path.join(ROOT, "include"),
            "-I", os.path.join(ROOT, "paper_2412_08585_amd", "csrc")]
-    api_o, drv_o, exe = (str(tmp_path / n) for n in ("api.o", "drv.o", "abi_driver"))
-    subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-O1", "-g", "-std=c++17", "-fPIC",
-                           *host_san, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                           *inc, "-c",
-                           os.path.join(ROOT, "paper_2412_08585_amd", "csrc", "turbo_api.hip"),
-                           "-o", api_o], stderr=subprocess.DEVNULL)
+    api_o, prj_o, drv_o, exe = (str(tmp_path / n)
+                                for n in ("api.o", "prj.o", "drv.o", "abi_driver"))
+    for unit, obj in (("turbo_api.hip", api_o), ("qkv_project.hip", prj_o)):
+        subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-O1", "-g", "-std=c++17",
+                               "-fPIC", *host_san, "-Xclang", "-target-feature", "-Xclang",
+                               "-packed-fp32-ops", *inc, "-c",
+                               os.path.join(ROOT, "paper_2412_08585_amd", "csrc", unit),
+                               "-o", obj], stderr=subprocess.DEVNULL)
     subprocess.check_call([HIPCC, "-O1", "-g", "-std=c++17", *host_san, *inc, "-c",
                            os.path.join(ROOT, "tests", "sanitize", "abi_driver.cpp"), "-o",
                            drv_o], stderr=subprocess.DEVNULL)
-    subprocess.check_call([HIPCC, "--offload-arch=gfx950", *host_san, api_o, drv_o, "-o", exe],
+    subprocess.check_call([HIPCC, "--offload-arch=gfx950", *host_san, api_o, prj_o, drv_o, "-o", exe],
                           stderr=subprocess.DEVNULL)
     assert "ok" in _run(exe)
