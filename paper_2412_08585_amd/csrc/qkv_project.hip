@@ -20,9 +20,9 @@
 // row pitch, so that the 16 lanes of each operand read hit 16 distinct
 // 4-bank groups.  There are two LDS stages and two register sets: each
 // thread loads its 16 chunks of stage k + 2 into registers at the top of
-// stage k and stores them to LDS at the end of stage k + 1 (one barrier per
-// stage), which gives the loads -- a fifth of which miss the XCD's L2 --
-// about 4k MFMA cycles to land.  Wave (wm, wn) owns tokens
+// stage k and stores them to LDS during stage k + 1, between its MFMA steps
+// (one barrier per stage), which gives the loads -- a fifth of which miss
+// the XCD's L2 -- more than a stage to land.  Wave (wm, wn) owns tokens
 // 128 wm .. +127 and head wn of the pair: 4 x 4 MFMA blocks of 32 x 32, 256
 // fp32 accumulators per lane, which live in the AGPR file (one wave per SIMD;
 // this file is built as a translation unit of its own, without the VGPR-only
@@ -120,8 +120,8 @@ k_qkv_project(QkvArgs a) {
   const int sdst = sr * kPRow + 16 * sc;
 
   // two register sets of a stage's 16 chunks (8 X, then 8 W): the loads of
-  // stage k + 2 are issued at the top of stage k and land in LDS at the end
-  // of stage k + 1, two stages (~4k MFMA cycles) later
+  // stage k + 2 are issued at the top of stage k and stored to LDS during
+  // stage k + 1
   uint4 g[2][16];
   auto gload = [&](auto setc, int kk) {
     constexpr int S = decltype(setc)::value;
@@ -132,16 +132,6 @@ k_qkv_project(QkvArgs a) {
       g[S][8 + j] = bload(wrs, lv, ws0 + j * sj + kb);
     }
   };
-  auto sstore = [&](auto setc, int st) {
-    constexpr int S = decltype(setc)::value;
-    uint8_t* d = lds + st * kPStage + sdst;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      *reinterpret_cast<uint4*>(d + j * 32 * kPRow) = g[S][j];
-      *reinterpret_cast<uint4*>(d + kPOp + j * 32 * kPRow) = g[S][8 + j];
-    }
-  };
-
   f32x16_t acc[4][4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
@@ -155,17 +145,21 @@ k_qkv_project(QkvArgs a) {
   const int aB = kPOp + (128 * wn + m) * kPRow + 16 * hh;
   // one stage: the operands of step s + 1 are read while the 16 MFMAs of
   // step s run
-  auto compute = [&](int st) {
+  // one stage; the operands of step s + 1 are read while the 16 MFMAs of
+  // step s run, and the next stage's chunks (register set S) are stored
+  // into the other LDS buffer between the steps, so that the stores overlap
+  // the MFMAs instead of stalling the barrier
+  auto compute = [&](int st, auto setc) {
+    constexpr int S = decltype(setc)::value;
     const uint8_t* sa = lds + st * kPStage + aA;
     const uint8_t* sb = lds + st * kPStage + aB;
+    uint8_t* d = lds + (st ^ 1) * kPStage + sdst;
     uint4 A[2][4], Bo[2][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       A[0][i] = *reinterpret_cast<const uint4*>(sa + i * 32 * kPRow);
       Bo[0][i] = *reinterpret_cast<const uint4*>(sb + i * 32 * kPRow);
     }
-    // (scheduling fences: the reads of step s + 1 go out before the MFMAs
-    // of step s, which then cover their latency)
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -176,6 +170,13 @@ k_qkv_project(QkvArgs a) {
           A[nx][i] = *reinterpret_cast<const uint4*>(sa + i * 32 * kPRow + 32 * (s + 1));
           Bo[nx][i] = *reinterpret_cast<const uint4*>(sb + i * 32 * kPRow + 32 * (s + 1));
         }
+      }
+      // four of the next stage's 16 chunks per step: X chunks 0-3, X 4-7,
+      // W 0-3, W 4-7
+#pragma unroll
+      for (int q = 4 * s; q < 4 * s + 4; ++q) {
+        const int j = q & 7;
+        *reinterpret_cast<uint4*>(d + (q < 8 ? 0 : kPOp) + j * 32 * kPRow) = g[S][q];
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -189,7 +190,14 @@ k_qkv_project(QkvArgs a) {
   // every load is issued on every path (the stage index is clamped at the
   // end), so the waits the compiler places before each use stay exact
   gload(std::integral_constant<int, 0>{}, 0);
-  sstore(std::integral_constant<int, 0>{}, 0);
+  {
+    uint8_t* d = lds + sdst;  // stage 0 into LDS 0
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      *reinterpret_cast<uint4*>(d + j * 32 * kPRow) = g[0][j];
+      *reinterpret_cast<uint4*>(d + kPOp + j * 32 * kPRow) = g[0][8 + j];
+    }
+  }
   gload(std::integral_constant<int, 1>{}, min(1, nk - 1));
   __syncthreads();
   for (int kk = 0; kk + 1 < nk; kk += 2) {
@@ -198,16 +206,14 @@ k_qkv_project(QkvArgs a) {
     gload(std::integral_constant<int, 0>{}, min(kk + 2, nk - 1));
     // keep the prefetch at the top (the scheduler would sink it to its use)
     __builtin_amdgcn_sched_barrier(0);
-    compute(0);
-    sstore(std::integral_constant<int, 1>{}, 1);
+    compute(0, std::integral_constant<int, 1>{});
     __syncthreads();
     gload(std::integral_constant<int, 1>{}, min(kk + 3, nk - 1));
     __builtin_amdgcn_sched_barrier(0);
-    compute(1);
-    sstore(std::integral_constant<int, 0>{}, 0);
+    compute(1, std::integral_constant<int, 0>{});
     __syncthreads();
   }
-  if (nk & 1) compute(0);  // the last stage of an odd count sits in LDS 0
+  if (nk & 1) compute(0, std::integral_constant<int, 1>{});  // the last stage of an odd count
   __syncthreads();
 
   // ---- epilogue: fp16 outputs, FlashQ step 1 per 64-token block --------------
