@@ -318,7 +318,8 @@ def main():
         step()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    e0, e1 = mk(), mk()
     e0.record(stream)
     for _ in range(args.steps):
         step()
@@ -326,11 +327,21 @@ def main():
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
 
-    # ---- per-kernel timing: HIP events around each launch, median -------------
-    ms_q, mean_q = stats(launch_times(run_quant, args.kernel_iters))
-    ms_p, mean_p = stats(launch_times(run_prefill, args.kernel_iters))
-    # the 15-us decode behind a prefill, which hides its host launch overhead
-    ms_d, mean_d = stats(launch_times(run_decode, args.kernel_iters, prev=run_prefill))
+    # ---- per-kernel timing: the same steps again, with an event pair around
+    # every kernel on the library's stream; medians over the steps ------------
+    evs = [[mk() for _ in range(4)] for _ in range(args.steps)]
+    for ev in evs:
+        ev[0].record(stream)
+        run_quant()
+        ev[1].record(stream)
+        run_prefill()
+        ev[2].record(stream)
+        run_decode()
+        ev[3].record(stream)
+    torch.cuda.synchronize()
+    ms_q, mean_q = stats([ev[0].elapsed_time(ev[1]) for ev in evs])
+    ms_p, mean_p = stats([ev[1].elapsed_time(ev[2]) for ev in evs])
+    ms_d, mean_d = stats([ev[2].elapsed_time(ev[3]) for ev in evs])
     prio = torch.empty(Hkv, dtype=torch.float32, device=dev)
     nws_h = int(ta.binding.lib().turbo_head_priority_workspace_bytes(B, Hkv, N))
     ws_h = torch.empty(nws_h // 4, dtype=torch.float32, device=dev)
@@ -368,7 +379,8 @@ def main():
                    "block_cols": 64, "decode_tokens": 1, "decode_kv_split_groups": split,
                    "decode_half": "phi3m-decode-8k"},
         "kernels": {
-            "timing": "median of per-launch HIP events (mean in brackets)",
+            "timing": "median over the timed steps of HIP events around each kernel (mean in "
+                      "brackets)",
             "quantize_kv": {"ms": round(ms_q, 4), "mean_ms": round(mean_q, 4),
                             "GB/s": round(quant_bytes / ms_q / 1e6, 1),
                             "frac_hbm": round(quant_bytes / ms_q / 1e6 / PEAK_HBM_GBS, 4)},

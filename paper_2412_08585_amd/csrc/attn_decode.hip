@@ -111,8 +111,8 @@ __device__ __forceinline__ DecodeSeq decode_seq(const DecodeArgs& a, int b) {
 __device__ void decode_write_empty(const DecodeArgs& a, int b, int kh) {
   for (int r = 0; r < a.G; ++r) {
     const long bh = (long)b * a.Hq + kh * a.G + r;
-    reinterpret_cast<unsigned*>(a.o)[bh * 64 + threadIdx.x] = 0u;
-    if (a.lse && threadIdx.x == 0) a.lse[bh] = -INFINITY;
+    reinterpret_cast<unsigned*>(a.o)[bh * 64 + (threadIdx.x & 63)] = 0u;
+    if (a.lse && (threadIdx.x & 63) == 0) a.lse[bh] = -INFINITY;
   }
 }
 
@@ -226,7 +226,7 @@ struct GroupV {
 template <int BITS>
 __device__ __forceinline__ void load_k(const DecodeArgs& a, int kh, int head_off, const int* bt,
                                        const int* gt, int g, bool live, GroupK<BITS>& K) {
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int n = lane & 15, g4 = lane >> 4, m = lane & 15;
   g = live ? g : 0;
   bool ok = live;
@@ -285,7 +285,7 @@ __device__ __forceinline__ void load_k(const DecodeArgs& a, int kh, int head_off
 template <int BITS>
 __device__ __forceinline__ void load_v(const DecodeArgs& a, int kh, int head_off,
                                        const GroupK<BITS>& K, GroupV<BITS>& V) {
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int n = lane & 15;
   const uint8_t* vrow = a.pages + (long)K.vpg * a.page_bytes + head_off + 256 * BITS + n * 2 * BITS;
 #pragma unroll
@@ -308,7 +308,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
                                               float (&O)[GP][2], float sq_row, int trow) {
   constexpr int LPR = 64 / GP;  // lanes per compact softmax row
   constexpr int d = BITS == 4 ? 2 : 4;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int n = lane & 15, g4 = lane >> 4;
   const int rr = lane / LPR, cc = lane % LPR;
   const int nrow = min(n, GP);  // P~ row this lane reads (GP: unused rows)
@@ -410,7 +410,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
                                               false);
         L.wbias[r] = (int)row_sum<16>((float)bp);  // every lane of the row: the same value
       }
-      __syncthreads();
+      wave_sync();
       v4i bhi[2], blo[2];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
@@ -462,7 +462,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         for (int mb = 0; mb < 4; ++mb)
           reinterpret_cast<int4*>(a.trace + TURBO_TRACE_S)[4 * mb + g4] = sv[mb];
       }
-      __syncthreads();
+      wave_sync();
       // ---- compact softmax: lane (rr, cc) holds tokens cc*GP .. +GP-1 -----
       bool renorm;
       {
@@ -527,7 +527,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         // every lane of the row holds the same values
         L.rowv[rr] = make_float4(gsc, __int_as_float(psum), rf, 0.0f);
       }
-      __syncthreads();
+      wave_sync();
       // ---- O = Q(P~) V on the raw codes (A = P rows, B = V codes) -------
       const v4i pop = *reinterpret_cast<const v4i*>(&L.pbuf[nrow][16 * g4]);
 #pragma unroll
@@ -554,7 +554,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
           for (int r = 0; r < GP; ++r) L.obuf[16 * cb + n][r] = acc[r];
         }
       }
-      __syncthreads();
+      wave_sync();
       // ---- accumulator update: lane L owns channels 2L, 2L+1 of all rows --
       {
         int acc[2][GP];
@@ -611,6 +611,8 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
 template <int GP, bool kTrace>
 __device__ void decode_tail_body(const DecodeArgs& a, int bx);  // kv_tail.hip
 
+// One wave per (b, KV head, chunk of groups); with several chunks each
+// writes its state to the workspace and k_decode_combine merges them.
 template <int GP, bool kTrace>
 __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decode(DecodeArgs a) {
   // the last B * Hkv work-groups (when there is a buffer): its chunk
@@ -620,13 +622,12 @@ __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decod
     return;
   }
   __shared__ DecodeLds<GP> L;
-  constexpr int LPR = 64 / GP;
-  const int lane = threadIdx.x;
-  if (lane < 8) L.lut[lane] = kLut[lane];
-
   const int s = blockIdx.x % a.nsplit;
   const int kh = (blockIdx.x / a.nsplit) % a.Hkv;
   const int b = blockIdx.x / (a.nsplit * a.Hkv);
+  constexpr int LPR = 64 / GP;
+  const int lane = threadIdx.x & 63;
+  if (lane < 8) L.lut[lane] = kLut[lane];
   const int n = lane & 15, g4 = lane >> 4;
   const int rr = lane / LPR, cc = lane % LPR;
   const int G = a.G;
@@ -639,72 +640,74 @@ __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decod
     return;
   }
 
-  const int bits = ((a.int2_mask >> kh) & 1ull) ? 2 : 4;
-  const int head_off = 512 * (4 * kh - 2 * __popcll(a.int2_mask & ((1ull << kh) - 1ull)));
-
-  // ---- q -> int8 per (b, query head) (Algorithm 2; eq. step1bpq) ---------
-  // lane (n, g4) holds channels 32*g4 .. 32*g4+31 of row n (zero if n >= G)
-  int q8w[8];
-  {
-    const bool rowok = n < G;
-    uint4 raw[4];
-    float amax = 0.0f;
-    const uint4* src = a.q + ((long)b * a.Hq + kh * G + (rowok ? n : 0)) * 16;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      raw[u] = rowok ? src[4 * g4 + u] : make_uint4(0, 0, 0, 0);
-      f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[u]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
-    }
-    amax = max_xor16(amax);
-    amax = max_xor32(amax);
-    float inv = 0.0f, sq = 0.0f;
-    if (amax > 0.0f) {
-      sq = amax / kQmax;
-      inv = kQmax / amax;
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[u]);
-      int qv[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
-      q8w[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
-      q8w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
-    }
-    if (g4 == 0) L.sq[n] = sq;
-    if (n < kWRows<GP>) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) *reinterpret_cast<int*>(&L.qbuf[n][32 * g4 + 4 * i]) = q8w[i];
-    }
-  }
-  // traced row of this wave (-1: none); the wave whose chunk holds group tr_g
-  const int trow = kTrace && b == a.tr_b && kh == a.tr_h / G && g0 <= a.tr_g && a.tr_g < g1
-                       ? a.tr_h % G : -1;
-  if (trow >= 0 && n == trow) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) reinterpret_cast<int*>(a.trace + TURBO_TRACE_Q8)[8 * g4 + i] = q8w[i];
-    if (g4 == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = L.sq[n];
-  }
-  __syncthreads();
-  const float sq_row = L.sq[rr];
-
   float O[GP][2];
 #pragma unroll
   for (int r = 0; r < GP; ++r) O[r][0] = O[r][1] = 0.0f;
-  float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f;
-  if (bits == 4)
-    decode_groups<GP, 4, kTrace>(a, L, b, kh, g0, g1, head_off, mrow, lpart, beta, O, sq_row, trow);
-  else
-    decode_groups<GP, 2, kTrace>(a, L, b, kh, g0, g1, head_off, mrow, lpart, beta, O, sq_row, trow);
+  float mrow = -INFINITY, lpart = 0.0f, beta = 1.0f, l = 0.0f;
+  {
+    const int bits = ((a.int2_mask >> kh) & 1ull) ? 2 : 4;
+    const int head_off = 512 * (4 * kh - 2 * __popcll(a.int2_mask & ((1ull << kh) - 1ull)));
 
-  // ---- epilogue: per-row (m, l, beta) from the softmax lanes -------------
-  const float l = row_sum<LPR>(lpart);
-  __syncthreads();
-  if (cc == 0) L.rowv[rr] = make_float4(mrow, l, beta, 0.0f);
-  __syncthreads();
-  if (sq_.nparts == 1) {  // the only state: O / l and L directly
+    // ---- q -> int8 per (b, query head) (Algorithm 2; eq. step1bpq) -------
+    // lane (n, g4) holds channels 32*g4 .. 32*g4+31 of row n (zero if n >= G)
+    int q8w[8];
+    {
+      const bool rowok = n < G;
+      uint4 raw[4];
+      float amax = 0.0f;
+      const uint4* src = a.q + ((long)b * a.Hq + kh * G + (rowok ? n : 0)) * 16;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        raw[u] = rowok ? src[4 * g4 + u] : make_uint4(0, 0, 0, 0);
+        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[u]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
+      }
+      amax = max_xor16(amax);
+      amax = max_xor32(amax);
+      float inv = 0.0f, sq = 0.0f;
+      if (amax > 0.0f) {
+        sq = amax / kQmax;
+        inv = kQmax / amax;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        f16x8_t hv = __builtin_bit_cast(f16x8_t, raw[u]);
+        int qv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qv[e] = rne_mul((float)hv[e], inv);
+        q8w[2 * u] = pack4(qv[0], qv[1], qv[2], qv[3]);
+        q8w[2 * u + 1] = pack4(qv[4], qv[5], qv[6], qv[7]);
+      }
+      if (g4 == 0) L.sq[n] = sq;
+      if (n < kWRows<GP>) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) *reinterpret_cast<int*>(&L.qbuf[n][32 * g4 + 4 * i]) = q8w[i];
+      }
+    }
+    // traced row of this wave (-1: none); the wave whose chunk holds group tr_g
+    const int trow = kTrace && b == a.tr_b && kh == a.tr_h / G && g0 <= a.tr_g && a.tr_g < g1
+                         ? a.tr_h % G : -1;
+    if (trow >= 0 && n == trow) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) reinterpret_cast<int*>(a.trace + TURBO_TRACE_Q8)[8 * g4 + i] = q8w[i];
+      if (g4 == 0) *reinterpret_cast<float*>(a.trace + TURBO_TRACE_SQ) = L.sq[n];
+    }
+    wave_sync();
+    const float sq_row = L.sq[rr];
+
+    if (bits == 4)
+      decode_groups<GP, 4, kTrace>(a, L, b, kh, g0, g1, head_off, mrow, lpart, beta, O, sq_row, trow);
+    else
+      decode_groups<GP, 2, kTrace>(a, L, b, kh, g0, g1, head_off, mrow, lpart, beta, O, sq_row, trow);
+
+    // ---- epilogue: per-row (m, l, beta) from the softmax lanes -----------
+    l = row_sum<LPR>(lpart);
+    wave_sync();
+    if (cc == 0) L.rowv[rr] = make_float4(mrow, l, beta, 0.0f);
+    wave_sync();
+  }
+  if (sq_.nparts == 1) {  // the only state (chunk 0): O / l and L directly
 #pragma unroll
     for (int r = 0; r < GP; ++r) {
       if (r >= G) break;
@@ -716,19 +719,20 @@ __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decod
     }
     if (a.lse && cc == 0 && rr < G)
       a.lse[(long)b * a.Hq + kh * G + rr] = mrow + logf(l);
-  } else {
+    return;
+  }
+  // several states: O beta, m and l of each row, to the workspace
 #pragma unroll
-    for (int r = 0; r < GP; ++r) {
-      if (r >= G) break;
-      const float be = L.rowv[r].z;
-      float* w = a.ws + (((long)b * a.Hq + kh * G + r) * a.nws + s) * kWsStride;
-      *reinterpret_cast<float2*>(w + kWsO + 2 * lane) = make_float2(O[r][0] * be, O[r][1] * be);
-    }
-    if (cc == 0 && rr < G) {
-      float* w = a.ws + (((long)b * a.Hq + kh * G + rr) * a.nws + s) * kWsStride;
-      w[0] = mrow;
-      w[1] = l;
-    }
+  for (int r = 0; r < GP; ++r) {
+    if (r >= G) break;
+    const float be = L.rowv[r].z;
+    float* w = a.ws + (((long)b * a.Hq + kh * G + r) * a.nws + s) * kWsStride;
+    *reinterpret_cast<float2*>(w + kWsO + 2 * lane) = make_float2(O[r][0] * be, O[r][1] * be);
+  }
+  if (cc == 0 && rr < G) {
+    float* w = a.ws + (((long)b * a.Hq + kh * G + rr) * a.nws + s) * kWsStride;
+    w[0] = mrow;
+    w[1] = l;
   }
 }
 
@@ -741,7 +745,7 @@ __global__ __launch_bounds__(64, (GP <= 8 && !kTrace) ? 3 : 2) void k_attn_decod
 __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
   __shared__ float lut[8];
   __shared__ float cwt[64], cl[64];  // merge weights and l of up to 64 chunks
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int bh = blockIdx.x;
   const int b = bh / a.Hq;
   const int ns = decode_seq(a, b).nparts;
@@ -790,9 +794,9 @@ __global__ __launch_bounds__(64) void k_decode_combine(DecodeArgs a) {
 }
 
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
+  const int gp = a.G <= 1 ? 1 : a.G <= 2 ? 2 : a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
   // group chunks, then one work-group per (sequence, KV head) for the buffer
   const int total = a.B * a.Hkv * a.nsplit + (a.tk ? a.B * a.Hkv : 0);
-  const int gp = a.G <= 1 ? 1 : a.G <= 2 ? 2 : a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
   if (a.trace) {
     switch (gp) {
       case 1: hipLaunchKernelGGL((k_attn_decode<1, true>), dim3(total), dim3(64), 0, stream, a); break;

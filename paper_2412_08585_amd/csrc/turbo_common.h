@@ -45,6 +45,16 @@ __device__ __forceinline__ float acc_unseed(int r) { return __int_as_float(r) - 
 // 32-bit literal).  Callers multiply by the negated factor.
 __device__ __forceinline__ float acc_unseed_neg(int r) { return kAccSeedF - __int_as_float(r); }
 
+// Ordering of one wave's own LDS exchanges (lanes writing what other lanes
+// of the same wave read next): the LDS executes a wave's accesses in order,
+// so only the compiler has to be kept from reordering them -- no s_barrier
+// and no wait, unlike __syncthreads.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // SAS (Sec. 4): e^{-y} ~ LUT[floor y] * POLY(y - floor y) for y = m - s in
 // [0, 6]; zero for y > 6 (n_r = -6, Sec. 5.2).  LUT[k] = e^{-k} rounded to
 // binary32; POLY coefficients as printed in Sec. 4, rounded to binary32.
