@@ -122,14 +122,38 @@ typedef short s16x2 __attribute__((ext_vector_type(2)));
 
 // Reductions over the 64/GP consecutive lanes of a compact row (every lane
 // of the row receives the result).
+// Integer forms (the DPP moves fuse into the max / add).
 template <int LPR>
-__device__ __forceinline__ float row_max(float v) {
-  if (LPR >= 2) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false)));
-  if (LPR >= 4) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xf, 0xf, false)));
-  if (LPR >= 8) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false)));
-  if (LPR >= 16) v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false)));
-  if (LPR >= 32) v = max_xor16(v);
-  if (LPR >= 64) v = max_xor32(v);
+__device__ __forceinline__ int row_max_i(int v) {
+  if (LPR >= 2) v = max(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xf, 0xf, true));
+  if (LPR >= 4) v = max(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xf, 0xf, true));
+  if (LPR >= 8) v = max(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xf, 0xf, true));
+  if (LPR >= 16) v = max(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xf, 0xf, true));
+  if (LPR >= 32) {
+    auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+    v = max((int)r[0], (int)r[1]);
+  }
+  if (LPR >= 64) {
+    auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+    v = max((int)r[0], (int)r[1]);
+  }
+  return v;
+}
+
+template <int LPR>
+__device__ __forceinline__ int row_sum_i(int v) {
+  if (LPR >= 2) v += __builtin_amdgcn_mov_dpp(v, 0xB1, 0xf, 0xf, true);
+  if (LPR >= 4) v += __builtin_amdgcn_mov_dpp(v, 0x4E, 0xf, 0xf, true);
+  if (LPR >= 8) v += __builtin_amdgcn_mov_dpp(v, 0x141, 0xf, 0xf, true);
+  if (LPR >= 16) v += __builtin_amdgcn_mov_dpp(v, 0x140, 0xf, 0xf, true);
+  if (LPR >= 32) {
+    auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+    v = (int)r[0] + (int)r[1];
+  }
+  if (LPR >= 64) {
+    auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+    v = (int)r[0] + (int)r[1];
+  }
   return v;
 }
 
@@ -408,7 +432,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         const int bp = __builtin_amdgcn_sdot4(wqn[t][0], (int)zA,
                                               __builtin_amdgcn_sdot4(wqn[t][1], (int)zB, 0, false),
                                               false);
-        L.wbias[r] = (int)row_sum<16>((float)bp);  // every lane of the row: the same value
+        L.wbias[r] = row_sum_i<16>(bp);  // every lane of the row: the same value
       }
       wave_sync();
       v4i bhi[2], blo[2];
@@ -477,29 +501,33 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
 #pragma unroll
           for (int e = 0; e < GP; ++e) si[e] = L.sbuf[rr][cc * GP + e];
         }
+        // c >= 0 (sm_scale > 0, the scales are non-negative) and both
+        // roundings of p = float(S) * c are monotonic: the row maximum of p is
+        // float(max S) * c, taken on the integers
         const float c = (sq_row * cur.skg) * a.sm_scale;
         float p[GP];
-        float smax = -INFINITY;
+        int imax = si[0];
 #pragma unroll
         for (int e = 0; e < GP; ++e) {
           p[e] = (float)si[e] * c;
-          smax = fmaxf(smax, p[e]);
+          imax = max(imax, si[e]);
         }
-        smax = row_max<LPR>(smax);
+        const float smax = (float)row_max_i<LPR>(imax) * c;
         const float mnew = fmaxf(mrow, smax);
-        float rs = 0.0f, pmax = 0.0f;
+        float rs = 0.0f;
+        int pbits = 0;  // the maximum of the p >= 0, on their bits (same order)
 #pragma unroll
         for (int e = 0; e < GP; ++e) {
           p[e] = sas_y(mnew - p[e], L.lut);
           rs += p[e];
-          pmax = fmaxf(pmax, p[e]);
+          pbits = max(pbits, __float_as_int(p[e]));
         }
         // SAS(m_old - m_new): 0 when m_old = -inf, exactly 1 (e^0) when the
         // row's maximum did not move
         const float alpha = mnew > mrow ? sas_y(mnew - mrow, L.lut) : 1.0f;
         lpart = alpha * lpart + rs;
         mrow = mnew;
-        pmax = row_max<LPR>(pmax);
+        const float pmax = __int_as_float(row_max_i<LPR>(pbits));
         // rescale: O = beta * Ost; renormalize when beta underflows / is 0
         float nbeta = beta * alpha;
         renorm = __builtin_amdgcn_ballot_w64(nbeta < 0x1p-64f) != 0;
@@ -520,7 +548,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         }
         if (trace_g && rr == trow && cc == 0)
           *reinterpret_cast<float*>(a.trace + TURBO_TRACE_PMAX) = pmax;
-        const int psum = (int)row_sum<LPR>((float)ps);  // exact: < 2^24
+        const int psum = row_sum_i<LPR>(ps);
         // s_P s_V / beta scales the fp32 accumulator only (no integer depends
         // on it): s_P as pmax times the binary32 1/119
         const float gsc = ((pmax * (1.0f / kQmax)) * cur.svg) * __builtin_amdgcn_rcpf(beta);
@@ -530,21 +558,19 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
       wave_sync();
       // ---- O = Q(P~) V on the raw codes (A = P rows, B = V codes) -------
       const v4i pop = *reinterpret_cast<const v4i*>(&L.pbuf[nrow][16 * g4]);
-#pragma unroll
-      for (int cb = 0; cb < 8; ++cb) {
-        v4i vop;
+      auto vop_of = [&](int cb) {
         if (BITS == 4) {
           const unsigned x0 = cv.vraw[cb][0], x1 = cv.vraw[cb][BITS / 2 - 1];
-          vop = v4i{(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
-                    (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
+          return v4i{(int)(x0 & 0x0F0F0F0Fu), (int)((x0 >> 4) & 0x0F0F0F0Fu),
+                     (int)(x1 & 0x0F0F0F0Fu), (int)((x1 >> 4) & 0x0F0F0F0Fu)};
         } else {
           const unsigned x = cv.vraw[cb][0];
-          vop = v4i{(int)(x & 0x03030303u), (int)((x >> 2) & 0x03030303u),
-                    (int)((x >> 4) & 0x03030303u), (int)((x >> 6) & 0x03030303u)};
+          return v4i{(int)(x & 0x03030303u), (int)((x >> 2) & 0x03030303u),
+                     (int)((x >> 4) & 0x03030303u), (int)((x >> 6) & 0x03030303u)};
         }
-        v4i acc = {};
-        acc = mfma16x16x64(pop, vop, acc);
-        // lane (n, g4), register r <-> row 4*g4 + r, channel 16*cb + n
+      };
+      // lane (n, g4), register r <-> row 4*g4 + r, channel 16*cb + n
+      auto store = [&](int cb, const v4i& acc) {
         if (GP >= 4) {
           int* dst = obase + cb * ostep;
           *reinterpret_cast<int2*>(dst) = make_int2(acc[0], acc[1]);
@@ -553,6 +579,15 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
 #pragma unroll
           for (int r = 0; r < GP; ++r) L.obuf[16 * cb + n][r] = acc[r];
         }
+      };
+      // two channel blocks per step: the second MFMA runs while the first
+      // one's result is stored
+#pragma unroll
+      for (int cb = 0; cb < 8; cb += 2) {
+        const v4i acc0 = mfma16x16x64(pop, vop_of(cb), v4i{});
+        const v4i acc1 = mfma16x16x64(pop, vop_of(cb + 1), v4i{});
+        store(cb, acc0);
+        store(cb + 1, acc1);
       }
       wave_sync();
       // ---- accumulator update: lane L owns channels 2L, 2L+1 of all rows --
@@ -575,14 +610,20 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         const int s0 = (int)((cv.vs4 >> sh) & 0xffu), s1 = (int)((cv.vs4 >> (sh + 8)) & 0xffu);
         const int z0 = (int)(int8_t)((cv.vz4 >> sh) & 0xffu);
         const int z1 = (int)(int8_t)((cv.vz4 >> (sh + 8)) & 0xffu);
+        if (renorm) {  // wave-uniform and rare: a branch (the empty asm keeps
+                       // the compiler from turning it into selects)
+          asm volatile("");
+#pragma unroll
+          for (int r = 0; r < GP; ++r) {
+            const float rf = L.rowv[r].z;
+            O[r][0] *= rf;
+            O[r][1] *= rf;
+          }
+        }
 #pragma unroll
         for (int r = 0; r < GP; ++r) {
           const float4 rv = L.rowv[r];
           const int psum = __float_as_int(rv.y);
-          if (renorm) {
-            O[r][0] *= rv.z;
-            O[r][1] *= rv.z;
-          }
           // exact int32 PV of Algorithm 2: s * sum P*code + z * sum P (every
           // factor fits 24 bits: s <= 80, |z| <= 127, sum P <= 64*119,
           // |sum P*code| <= 64*119*15)

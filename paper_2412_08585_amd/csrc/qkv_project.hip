@@ -143,8 +143,6 @@ k_qkv_project(QkvArgs a) {
   // column 16 s + 8 hh + e of the stage for both operands
   const int aA = (128 * wm + m) * kPRow + 16 * hh;
   const int aB = kPOp + (128 * wn + m) * kPRow + 16 * hh;
-  // one stage: the operands of step s + 1 are read while the 16 MFMAs of
-  // step s run
   // one stage; the operands of step s + 1 are read while the 16 MFMAs of
   // step s run, and the next stage's chunks (register set S) are stored
   // into the other LDS buffer between the steps, so that the stores overlap
