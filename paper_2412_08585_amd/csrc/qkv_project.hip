@@ -15,19 +15,19 @@
 // fp16.
 //
 // Tiling.  A work-group of four waves computes a 256-token x 256-feature tile
-// (two heads).  The contraction runs in stages of 64 columns: the tile's 256
-// X rows and 256 W rows of a stage (128 bytes each) sit in LDS at a 144-byte
-// row pitch, so that the 16 lanes of each operand read hit 16 distinct
-// 4-bank groups.  There are two LDS stages and two register sets: each
-// thread loads its 16 chunks of stage k + 2 into registers at the top of
-// stage k and stores them to LDS during stage k + 1, between its MFMA steps
-// (one barrier per stage), which gives the loads -- a fifth of which miss
-// the XCD's L2 -- more than a stage to land.  Wave (wm, wn) owns tokens
-// 128 wm .. +127 and head wn of the pair: 4 x 4 MFMA blocks of 32 x 32, 256
-// fp32 accumulators per lane, which live in the AGPR file (one wave per SIMD;
-// this file is built as a translation unit of its own, without the VGPR-only
-// MFMA form of the attention kernels).  Every operand byte leaves L2 once per
-// work-group: X is read once per head pair and W once per 256-token tile.
+// (two heads).  The contraction runs in stages of 32 columns: the tile's 256
+// X rows and 256 W rows of a stage (64 bytes each, 16-byte chunks swizzled
+// by row so that the operand reads are free of bank conflicts) are loaded
+// straight into LDS by buffer loads, into a ring of four stage buffers, four
+// stages ahead.  Each wave reads the next stage's operands into registers
+// while the current stage's MFMAs run, and issues its part of the loads
+// spread between those MFMAs; one barrier per stage.  Wave (wm, wn) owns
+// tokens 128 wm .. +127 and head wn of the pair: 4 x 4 MFMA blocks of
+// 32 x 32, 256 fp32 accumulators per lane, which live in the AGPR file (one
+// wave per SIMD; this file is built as a translation unit of its own,
+// without the VGPR-only MFMA form of the attention kernels).  Every operand
+// byte leaves L2 once per work-group: X is read once per head pair and W
+// once per 256-token tile.
 #include "turbo_common.h"
 #include "quant_tiles.h"
 #include "qkv_project.h"
@@ -36,31 +36,36 @@ namespace turbo {
 
 typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kProjThreads = 256;
-constexpr int kPRow = 144;               // LDS bytes per staged row: 128 + 16 (bank spread)
+constexpr int kPRow = 64;                // LDS bytes per staged row: 32 fp16 columns
 constexpr int kPOp = 256 * kPRow;        // one operand (256 rows) of one stage
 constexpr int kPStage = 2 * kPOp;        // X rows, then W rows
 constexpr int kEpiTile = 64 * kTileStride;  // one 64 x 128 int8 block (k_quantize_kv layout)
-constexpr int kQkvLds = 2 * kPStage;
-static_assert(9 * kEpiTile <= kQkvLds, "the epilogue tiles fit in the stages");
+static_assert(3 * kEpiTile <= kPStage, "three epilogue tiles fit in a stage");
 
 __device__ __forceinline__ f32x16_t mfma_f16(uint4 a, uint4 b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8_t, a),
                                                 __builtin_bit_cast(h8_t, b), c, 0, 0, 0);
 }
 
-// Raw buffer resource over `bytes` bytes at p (gfx9 descriptor word 3: 32-bit
-// data format).  Loads at offsets >= bytes return zeros: the rows past N of
-// the last token tile and past F of an odd head count.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, 0x00020000);
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource over `bytes` bytes at p, as the four descriptor words
+// (word 3: 32-bit data format).  Loads at offsets >= bytes return zeros: the
+// rows past N of the last token tile and past F of an odd head count.
+__device__ __forceinline__ i32x4 rows_words(const void* p, int bytes) {
+  const unsigned long long a = (unsigned long long)p;
+  return i32x4{(int)(unsigned)a, (int)((unsigned)(a >> 32) & 0xffffu), bytes, 0x00020000};
 }
 
-__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
-  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
-  return make_uint4(v[0], v[1], v[2], v[3]);
+// 16 bytes per lane from the buffer (offsets voff + soff) into LDS at dst +
+// 16 * lane (the wave-uniform LDS address goes through M0; the nop keeps the
+// load one cycle away from the compiler's write of M0).
+__device__ __forceinline__ void lds_load16(i32x4 r, unsigned voff, unsigned soff, uint8_t* dst) {
+  const unsigned la = (unsigned)(unsigned long)(__attribute__((address_space(3))) uint8_t*)dst;
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :: "v"(voff), "s"(r), "s"(soff), "{m0}"(la) : "memory");
 }
 
 // Work-group order.  The dispatcher hands work-group x to XCD x % 8.  When
@@ -94,9 +99,11 @@ __device__ __forceinline__ void qkv_tile(int x, int ntiles, int npairs, int& til
 template <bool kY>
 __global__ __launch_bounds__(kProjThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 k_qkv_project(QkvArgs a) {
-  __shared__ __align__(16) uint8_t lds[kQkvLds];
+  // four stages, each its own array: the compiler then sees that the loads
+  // into one stage and the operand reads of another do not overlap
+  __shared__ __align__(16) uint8_t st0[kPStage], st1[kPStage], st2[kPStage], st3[kPStage];
   __shared__ float sblk[8];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wv & 1, wn = wv >> 1;
   const int m = lane & 31, hh = lane >> 5;
   const int nheads = a.Hq + 2 * a.Hkv;
@@ -107,30 +114,32 @@ k_qkv_project(QkvArgs a) {
   const int b = tile / a.ntile;
   const int t0 = (tile % a.ntile) * kQkvTileTokens;
 
-  // ---- staging: thread (row sr + 32 j, 16-byte chunk sc), j = 0..7 ---------
-  // one load instruction reads 8 whole 128-byte rows of a stage
-  const int sr = tid >> 3, sc = tid & 7;
+  // ---- staging: buffer loads straight into LDS, four stages of 32 columns ----
+  // chunk c of staged row r sits at chunk position c ^ ((r >> 2) & 3).  Per
+  // stage a wave issues 4 X and 4 W loads; load i of wave w fills rows
+  // 16 (4 w + i) .. +15 (1 KiB): lane L takes row + (L >> 2), position L & 3,
+  // i.e. source chunk (L & 3) ^ ((L >> 4) & 3).
   const unsigned D2 = 2u * (unsigned)a.D;  // bytes per row
-  const __amdgpu_buffer_rsrc_t xrs =
-      rows_rsrc(static_cast<const _Float16*>(a.x) + (long)b * a.N * a.D, a.N * (int)D2);
-  const __amdgpu_buffer_rsrc_t wrs = rows_rsrc(a.w, F * (int)D2);
-  const unsigned lv = (unsigned)sr * D2 + 16u * (unsigned)sc;  // lane part of both offsets
+  const unsigned vo = (unsigned)(lane >> 2) * D2 + 16u * (unsigned)((lane & 3) ^ ((lane >> 4) & 3));
   const unsigned xs0 = (unsigned)t0 * D2, ws0 = (unsigned)(256 * pair) * D2;
-  const unsigned sj = 32u * D2;  // 32 rows
-  const int sdst = sr * kPRow + 16 * sc;
-
-  // two register sets of a stage's 16 chunks (8 X, then 8 W): the loads of
-  // stage k + 2 are issued at the top of stage k and stored to LDS during
-  // stage k + 1
-  uint4 g[2][16];
-  auto gload = [&](auto setc, int kk) {
-    constexpr int S = decltype(setc)::value;
-    const unsigned kb = 128u * (unsigned)kk;  // 64 fp16 columns per stage
+  // The loads are written as inline assembly: the compiler then neither
+  // waits for them before every LDS read nor counts them in its own waits
+  // (no other vector-memory operation is in flight during the loop).
+  const i32x4 xr = rows_words(static_cast<const _Float16*>(a.x) + (long)b * a.N * a.D, a.N * (int)D2);
+  const i32x4 wr = rows_words(a.w, F * (int)D2);
+  // load j (0..7) of this wave's part of a stage: X rows (j even) or W rows
+  // (j odd) 16 (4 w + j / 2) .. +15
+  auto dma_j = [&](uint8_t* st, int kk, int j) {
+    const unsigned kb = 64u * (unsigned)kk;  // 32 fp16 columns per stage
+    const int r0 = 16 * (4 * wv + (j >> 1));
+    if (j & 1)
+      lds_load16(wr, vo, ws0 + (unsigned)r0 * D2 + kb, st + kPOp + r0 * kPRow);
+    else
+      lds_load16(xr, vo, xs0 + (unsigned)r0 * D2 + kb, st + r0 * kPRow);
+  };
+  auto dma = [&](uint8_t* st, int kk) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      g[S][j] = bload(xrs, lv, xs0 + j * sj + kb);
-      g[S][8 + j] = bload(wrs, lv, ws0 + j * sj + kb);
-    }
+    for (int j = 0; j < 8; ++j) dma_j(st, kk, j);
   };
   f32x16_t acc[4][4];
 #pragma unroll
@@ -138,80 +147,85 @@ k_qkv_project(QkvArgs a) {
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x16_t{};
 
-  // operand reads: A (X rows) row 128 wm + 32 mb + m, B (W rows) row
-  // 128 wn + 32 nb + m; contraction slot (step s, lane half hh, element e) is
-  // column 16 s + 8 hh + e of the stage for both operands
-  const int aA = (128 * wm + m) * kPRow + 16 * hh;
-  const int aB = kPOp + (128 * wn + m) * kPRow + 16 * hh;
-  // one stage; the operands of step s + 1 are read while the 16 MFMAs of
-  // step s run, and the next stage's chunks (register set S) are stored
-  // into the other LDS buffer between the steps, so that the stores overlap
-  // the MFMAs instead of stalling the barrier
-  auto compute = [&](int st, auto setc) {
-    constexpr int S = decltype(setc)::value;
-    const uint8_t* sa = lds + st * kPStage + aA;
-    const uint8_t* sb = lds + st * kPStage + aB;
-    uint8_t* d = lds + (st ^ 1) * kPStage + sdst;
-    uint4 A[2][4], Bo[2][4];
+  // operand reads: row 128 wm + 32 mb + m (A) / 128 wn + 32 nb + m (B);
+  // contraction slot (step s, half hh, element e) = column 16 s + 8 hh + e,
+  // chunk 2 s + hh at position (2 s + hh) ^ ((m >> 2) & 3)
+  const int sw = (m >> 2) & 3;
+  const int ao0 = m * kPRow + 16 * ((0 + hh) ^ sw), ao1 = m * kPRow + 16 * ((2 + hh) ^ sw);
+  const int aA = 128 * wm * kPRow, aB = kPOp + 128 * wn * kPRow;
+  // operands of one stage in registers: [k-step][block]
+  typedef uint4 StageOps[2][4];
+  auto read_stage = [&](const uint8_t* st, StageOps& A, StageOps& Bo) {
+    const uint8_t* sa = st + aA;
+    const uint8_t* sb = st + aB;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      A[0][i] = *reinterpret_cast<const uint4*>(sa + i * 32 * kPRow);
-      Bo[0][i] = *reinterpret_cast<const uint4*>(sb + i * 32 * kPRow);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int cu = s & 1, nx = cu ^ 1;
-      if (s < 3) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          A[nx][i] = *reinterpret_cast<const uint4*>(sa + i * 32 * kPRow + 32 * (s + 1));
-          Bo[nx][i] = *reinterpret_cast<const uint4*>(sb + i * 32 * kPRow + 32 * (s + 1));
-        }
-      }
-      // four of the next stage's 16 chunks per step: X chunks 0-3, X 4-7,
-      // W 0-3, W 4-7
-#pragma unroll
-      for (int q = 4 * s; q < 4 * s + 4; ++q) {
-        const int j = q & 7;
-        *reinterpret_cast<uint4*>(d + (q < 8 ? 0 : kPOp) + j * 32 * kPRow) = g[S][q];
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma_f16(A[cu][mb], Bo[cu][nb], acc[mb][nb]);
-      __builtin_amdgcn_sched_barrier(0);
+      A[0][i] = *reinterpret_cast<const uint4*>(sa + ao0 + i * 32 * kPRow);
+      Bo[0][i] = *reinterpret_cast<const uint4*>(sb + ao0 + i * 32 * kPRow);
+      A[1][i] = *reinterpret_cast<const uint4*>(sa + ao1 + i * 32 * kPRow);
+      Bo[1][i] = *reinterpret_cast<const uint4*>(sb + ao1 + i * 32 * kPRow);
     }
   };
-  const int nk = a.D / 64;
-  // every load is issued on every path (the stage index is clamped at the
-  // end), so the waits the compiler places before each use stay exact
-  gload(std::integral_constant<int, 0>{}, 0);
-  {
-    uint8_t* d = lds + sdst;  // stage 0 into LDS 0
+  auto mma = [&](const StageOps& A, const StageOps& Bo, int s) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      *reinterpret_cast<uint4*>(d + j * 32 * kPRow) = g[0][j];
-      *reinterpret_cast<uint4*>(d + kPOp + j * 32 * kPRow) = g[0][8 + j];
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma_f16(A[s][mb], Bo[s][nb], acc[mb][nb]);
+  };
+  const int nk = a.D / 32;
+  // The loads write LDS behind the compiler's back: their completion is
+  // waited for by hand (a wave's loads complete in order, eight per stage),
+  // and a plain s_barrier then covers the other waves' parts (__syncthreads
+  // would also wait for the loads still in flight).  Step k runs stage k's
+  // MFMAs from registers, reads stage k + 1 into the other register set and
+  // loads stage k + 4 into the slot of stage k; its closing barrier makes
+  // stage k + 2 visible (16 loads, stages k + 3 and k + 4, may still be in
+  // flight) and tells that every wave has read stage k + 1.  Past the end
+  // the last stage is loaded again, so that every step issues the same
+  // number of loads.
+  StageOps A0, B0, A1, B1;
+  dma(st0, 0);
+  dma(st1, min(1, nk - 1));
+  dma(st2, min(2, nk - 1));
+  dma(st3, min(3, nk - 1));
+  asm volatile("s_waitcnt vmcnt(24)\n\ts_barrier" ::: "memory");
+  read_stage(st0, A0, B0);
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
+  // step k: the slot of stage k (in registers since step k - 1, and every
+  // wave has passed the barrier after that read) takes stage k + 4
+  auto step = [&](uint8_t* slot_k, const uint8_t* slot_k1, StageOps& Ak, StageOps& Bk,
+                  StageOps& An, StageOps& Bn, int k) {
+    // the stage's 32 MFMAs in eight groups of four, each followed by one
+    // load of stage k + 4 and two operand reads of stage k + 1
+    const uint8_t* sa = slot_k1 + aA;
+    const uint8_t* sb = slot_k1 + aB;
+    const int kn = min(k + 4, nk - 1);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int s_ = g >> 2, q = g & 3;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) acc[q][nb] = mfma_f16(Ak[s_][q], Bk[s_][nb], acc[q][nb]);
+      __builtin_amdgcn_sched_barrier(0);
+      dma_j(slot_k, kn, g);
+      // reads: group g fetches block (g >> 1) of k-step (g & 1), A and B
+      const int rb = g >> 1, rs = g & 1;
+      An[rs][rb] = *reinterpret_cast<const uint4*>(sa + (rs ? ao1 : ao0) + rb * 32 * kPRow);
+      Bn[rs][rb] = *reinterpret_cast<const uint4*>(sb + (rs ? ao1 : ao0) + rb * 32 * kPRow);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    // lgkmcnt(0) through the builtin, so that the compiler knows the operand
+    // reads have landed; vmcnt(16) for the hidden loads by hand
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
+  };
+  for (int k = 0; k < nk; k += 4) {
+    step(st0, st1, A0, B0, A1, B1, k);
+    if (k + 1 < nk) step(st1, st2, A1, B1, A0, B0, k + 1);
+    if (k + 2 < nk) step(st2, st3, A0, B0, A1, B1, k + 2);
+    if (k + 3 < nk) step(st3, st0, A1, B1, A0, B0, k + 3);
   }
-  gload(std::integral_constant<int, 1>{}, min(1, nk - 1));
-  __syncthreads();
-  for (int kk = 0; kk + 1 < nk; kk += 2) {
-    // stage kk from LDS 0; set 0 (free) takes stage kk + 2; set 1 (stage
-    // kk + 1) goes to LDS 1, whose last readers finished before the barrier
-    gload(std::integral_constant<int, 0>{}, min(kk + 2, nk - 1));
-    // keep the prefetch at the top (the scheduler would sink it to its use)
-    __builtin_amdgcn_sched_barrier(0);
-    compute(0, std::integral_constant<int, 1>{});
-    __syncthreads();
-    gload(std::integral_constant<int, 1>{}, min(kk + 3, nk - 1));
-    __builtin_amdgcn_sched_barrier(0);
-    compute(1, std::integral_constant<int, 0>{});
-    __syncthreads();
-  }
-  if (nk & 1) compute(0, std::integral_constant<int, 1>{});  // the last stage of an odd count
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
   // ---- epilogue: fp16 outputs, FlashQ step 1 per 64-token block --------------
@@ -220,6 +234,11 @@ k_qkv_project(QkvArgs a) {
   // block i = mb >> 1 of the wave is block 2 wm + i of the tile
   const int head = 2 * pair + wn;
   const bool hv = head < nheads;  // wave-uniform (an odd head count leaves one out)
+  // epilogue tile t (0..8) in stage t / 3, slot t % 3
+  auto etile = [&](int t) -> uint8_t* {
+    uint8_t* st = t < 3 ? st0 : (t < 6 ? st1 : st2);
+    return st + (t % 3) * kEpiTile;
+  };
   // one block at a time (128 accumulators of a lane), which bounds the
   // registers the AGPR -> VGPR copies take; the stages are free for the tiles
   // since the loop's last barrier
@@ -255,7 +274,7 @@ k_qkv_project(QkvArgs a) {
       sc_[i] = amax / kQmax;
       inv = kQmax / amax;
     }
-    int8_t* tw = reinterpret_cast<int8_t*>(lds) + (4 * wn + 2 * wm + i) * kEpiTile;
+    int8_t* tw = reinterpret_cast<int8_t*>(etile(4 * wn + 2 * wm + i));
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
@@ -287,7 +306,7 @@ k_qkv_project(QkvArgs a) {
   if (hv) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int8_t* tw = reinterpret_cast<const int8_t*>(lds) + (4 * wn + 2 * wm + i) * kEpiTile;
+      const int8_t* tw = reinterpret_cast<const int8_t*>(etile(4 * wn + 2 * wm + i));
       const int jb = (t0 + 128 * wm + 64 * i) / 64;  // FlashQ block index in the sequence
       if (jb >= a.nb) continue;                      // wave-uniform
       if (head < a.Hq + a.Hkv) {
@@ -329,7 +348,7 @@ k_qkv_project(QkvArgs a) {
 
   // ---- step 2 and the cache write (K and V heads, full blocks) ---------------
   if (a.pages == nullptr) return;  // work-group uniform
-  uint8_t* ctile = lds + 8 * kEpiTile;
+  uint8_t* ctile = etile(8);
   for (int hl = 0; hl < 2; ++hl) {
     const int hd = 2 * pair + hl;
     if (hd < a.Hq || hd >= nheads) continue;  // work-group uniform
@@ -351,7 +370,7 @@ k_qkv_project(QkvArgs a) {
       const long slot = a.group_table[(long)b * a.max_groups + g];
       if (!ok || slot < 0 || slot >= a.num_slots) continue;  // uniform
       int8_t* meta = a.gmeta + (slot * a.Hkv + hkv) * 512;
-      const int8_t* tb = reinterpret_cast<const int8_t*>(lds) + (4 * hl + w) * kEpiTile;
+      const int8_t* tb = reinterpret_cast<const int8_t*>(etile(4 * hl + w));
       if (isk)
         compress_k(tb, ctile, bits, meta, a.gscale + (slot * a.Hkv + hkv) * 2 + 0, sblk[4 * hl + w],
                    page, a.pages, a.page_bytes, head_off);
