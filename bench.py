@@ -75,6 +75,29 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
+# Vector ALU issue peak of the MI355X: 1,024 SIMDs x 2.4 GHz / 4 clocks per
+# wave64 instruction (a 16-lane SIMD takes 4 clocks for 64 lanes).
+PEAK_VALU_GINST = 1024 * 2.4 / 4
+
+
+def measured_valu(kernel: str, workload: str):
+    """Non-MFMA vector ALU instructions per launch from the committed rocprofv3
+    SQ_INSTS_VALU - SQ_INSTS_MFMA summary (profiles/valu.txt), or None if the
+    kernel's sources changed since the counters were taken."""
+    srcs = {"k_attn_prefill16": ["paper_2412_08585_amd/csrc/attn_prefill.hip",
+                                 "paper_2412_08585_amd/csrc/turbo_common.h",
+                                 "paper_2412_08585_amd/build.py"]}.get(kernel)
+    path = os.path.join(ROOT, "profiles", "valu.txt")
+    if not srcs or not os.path.exists(path):
+        return None
+    digest = source_digest(srcs)
+    for line in open(path):
+        parts = line.split()
+        if len(parts) == 4 and parts[0] == kernel and parts[1] == workload and parts[2] == digest:
+            return float(parts[3])
+    return None
+
+
 def decode_bytes_per_token(bits: int) -> float:
     """Compressed K+V bytes read per cached token and KV head: codes plus the
     per-channel integer scale/zero (4 x 128 B per 64-token group) plus the
@@ -169,17 +192,45 @@ def measured_ceilings(dev):
     def mfma():
         ops[0] = ta.binding.probe_mfma_i8(4096, dev)
 
+    insts = [0]
+
+    def valu():
+        insts[0] = ta.binding.probe_valu(4096, dev)
+
     buf = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
     ramp_clocks(mfma, 0.1)
     t_m, _ = stats(launch_times(mfma, 5))
+    t_v, _ = stats(launch_times(valu, 5))
     t_r, _ = stats(launch_times(lambda: ta.binding.probe_read(buf), 5))
     nbytes = buf.numel() * 4
     del buf
     return {"int8_mfma_TOPS": round(ops[0] / (t_m * 1e-3) / 1e12, 1),
             "hbm_read_GBs": round(nbytes / (t_r * 1e-3) / 1e9, 1),
+            "valu_Ginst_per_s": round(insts[0] / (t_v * 1e-3) / 1e9, 1),
             "probes": "turbo_probe_mfma_i8 (8 chains of v_mfma_i32_16x16x64_i8 per wave, 2048 "
-                      "waves) and turbo_probe_read (1 GiB nontemporal streaming read, one "
-                      "32 KiB chunk per work-group), median of 5"}
+                      "waves), turbo_probe_valu (8 chains of v_fma_f32 per wave, 4096 waves) "
+                      "and turbo_probe_read (1 GiB nontemporal streaming read, one 32 KiB "
+                      "chunk per work-group), median of 5"}
+
+
+def valu_roofline(kernel: str, workload: str, ms: float, ceil: dict):
+    """The vector ALU roofline of a kernel: its committed non-MFMA VALU
+    instruction count per launch over its measured time, against the issue
+    peak and the probe's measured rate (None without a current count)."""
+    n = measured_valu(kernel, workload)
+    if n is None:
+        return None
+    rate = n / (ms * 1e-3) / 1e9
+    return {"kernel": kernel, "bound": "valu", "achieved": round(rate, 1),
+            "peak": PEAK_VALU_GINST, "unit": "G wave-instructions/s",
+            "frac": round(rate / PEAK_VALU_GINST, 4),
+            "frac_of_measured_ceiling": round(rate / ceil["valu_Ginst_per_s"], 4),
+            "instructions_per_launch": n,
+            "derivation": "1,024 SIMDs x 2.4 GHz / 4 clocks per wave64 instruction; "
+                          "instructions = SQ_INSTS_VALU - SQ_INSTS_MFMA from profiles/valu.txt",
+            "note": "on gfx950 the issue cost of a wave64 VALU instruction depends on the opcode "
+                    "and its operands (2.5-4.8 clocks measured for the opcodes of the softmax "
+                    "path); the peak takes 4, the measured ceiling is the FMA-chain probe"}
 
 
 def rel_l2(a, ref) -> float:
@@ -404,6 +455,7 @@ def main():
                      "frac_of_measured_ceiling": round(prefill_tops / ceil["int8_mfma_TOPS"], 4),
                      "valu_note": "issue-bound on the VALU (SAS + P quantization + accumulator "
                                   "update); see profiles/k_attn_prefill16_phi3m-prefill-4k.md"},
+        "roofline_valu": valu_roofline("k_attn_prefill16", w.name, ms_p, ceil),
         "ceilings_measured": ceil,
         "paper_context": PAPER_CONTEXT,
     }

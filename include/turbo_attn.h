@@ -559,11 +559,19 @@ size_t turbo_decode_workspace_bytes(int B, int Hq, int Hkv, int max_groups_per_s
  * (device, uint32 [1]) is written only if the folded data hit a fixed
  * pattern.  The read rate is bytes / elapsed.
  *
- * Both queue one launch on `stream`.  INVALID_ARG for iters < 1, null
+ * turbo_probe_valu — chains of fp32 FMAs (v_fma_f32, one value per lane),
+ * `iters` rounds of 8 per wave, 4096 waves (four per SIMD of 256 CUs); no
+ * memory traffic.  *insts (host) receives the wave-level vector ALU
+ * instructions the launch issues; sink (device, float [1024]) is written
+ * only if the folded chains hit a fixed value.  The vector ALU issue rate is
+ * *insts / elapsed (one wave64 instruction occupies a SIMD for 4 clocks).
+ *
+ * All queue one launch on `stream`.  INVALID_ARG for iters < 1, null
  * pointers, or a misaligned / zero-sized buffer.
  */
 int turbo_probe_mfma_i8(int iters, int* sink, int64_t* ops, hipStream_t stream);
 int turbo_probe_read(const void* src, size_t bytes, unsigned* sink, hipStream_t stream);
+int turbo_probe_valu(int iters, float* sink, int64_t* insts, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -77,6 +77,7 @@ def lib() -> ctypes.CDLL:
             "turbo_decode_default_split": ([I], I),
             "turbo_probe_mfma_i8": ([I, P, P, P], I),
             "turbo_probe_read": ([P, Z, P, P], I),
+            "turbo_probe_valu": ([I, P, P, P], I),
             "turbo_decode_workspace_bytes": ([I, I, I, I, I, I], Z),
         }
         for name, (args, res) in sig.items():
@@ -486,6 +487,15 @@ def probe_mfma_i8(iters: int, device="cuda") -> int:
     _check(lib().turbo_probe_mfma_i8(int(iters), _ptr(sink), ctypes.byref(ops),
                                      _stream(torch.device(device))), "turbo_probe_mfma_i8")
     return int(ops.value)
+
+
+def probe_valu(iters: int, device="cuda") -> int:
+    """Queues the vector-ALU issue probe; returns the wave instructions it issues."""
+    sink = torch.empty(1024, dtype=torch.float32, device=device)
+    n = ctypes.c_int64(0)
+    _check(lib().turbo_probe_valu(int(iters), _ptr(sink), ctypes.byref(n),
+                                  _stream(torch.device(device))), "turbo_probe_valu")
+    return int(n.value)
 
 
 def probe_read(buf: torch.Tensor) -> int:

@@ -1,11 +1,14 @@
-// Measurement probes (not part of the method): the two ceilings the attention
+// Measurement probes (not part of the method): the ceilings the attention
 // kernels are judged against, measured on the GPU itself.
 //   * k_probe_mfma_i8: every wave runs chains of v_mfma_i32_16x16x64_i8 on
 //     register operands -- the int8 matrix-core rate with no memory traffic
 //     and no VALU work between the MFMAs;
 //   * k_probe_read: a streaming read of a device buffer (nontemporal 16-byte
 //     loads, eight in flight per thread) -- the HBM read rate a kernel that
-//     only reads can reach.
+//     only reads can reach;
+//   * k_probe_valu: every wave runs chains of fp32 FMAs (v_fma_f32, one
+//     value per lane) -- the rate at which the SIMDs issue plain vector ALU
+//     instructions, the unit the prefill's softmax work runs on.
 // Each folds what it computes or reads into a word that a store depends on,
 // so nothing is eliminated.
 #include "turbo_common.h"
@@ -52,6 +55,32 @@ __global__ __launch_bounds__(256) void k_probe_read(const u32x4* src, long n16, 
   for (int u = 0; u < kProbeReadU; ++u) x ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
   // keeps the loads: a store that depends on every word read
   if (x == 0x9E3779B9u) sink[0] = x;
+}
+
+// kProbeChains independent FMA chains per lane; the loop's own counter and
+// branch are scalar instructions.
+__global__ __launch_bounds__(256) void k_probe_valu(int iters, float* sink) {
+  const float lane = (float)(threadIdx.x & 63);
+  const float m = 1.0f - 0x1p-20f, c = 0x1p-24f;
+  float x[kProbeChains];
+#pragma unroll
+  for (int k = 0; k < kProbeChains; ++k) x[k] = lane + (float)k;
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int k = 0; k < kProbeChains; ++k) x[k] = __builtin_fmaf(x[k], m, c);
+  }
+  float t = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kProbeChains; ++k) t += x[k];
+  if (t == 0.5f) sink[blockIdx.x] = t;
+}
+
+// Work-groups of the VALU probe: four per CU (four waves per SIMD).
+constexpr int kProbeValuBlocks = 1024;
+
+hipError_t launch_probe_valu(int iters, float* sink, hipStream_t stream) {
+  hipLaunchKernelGGL(k_probe_valu, dim3(kProbeValuBlocks), dim3(256), 0, stream, iters, sink);
+  return hipGetLastError();
 }
 
 // Work-groups of the MFMA probe: two per CU (8 waves per CU, two per SIMD).

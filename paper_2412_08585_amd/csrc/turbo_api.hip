@@ -619,6 +619,15 @@ int turbo_probe_mfma_i8(int iters, int* sink, int64_t* ops, hipStream_t stream) 
                                                                          : TURBO_ERR_HIP;
 }
 
+int turbo_probe_valu(int iters, float* sink, int64_t* insts, hipStream_t stream) {
+  if (iters < 1 || !sink || !insts) return TURBO_ERR_INVALID_ARG;
+  const int st = check_device();
+  if (st != TURBO_OK) return st;
+  // 4 waves per work-group, kProbeChains FMAs per round
+  *insts = (int64_t)turbo::kProbeValuBlocks * 4 * turbo::kProbeChains * iters;
+  return turbo::launch_probe_valu(iters, sink, stream) == hipSuccess ? TURBO_OK : TURBO_ERR_HIP;
+}
+
 int turbo_probe_read(const void* src, size_t bytes, unsigned* sink, hipStream_t stream) {
   if (!src || !sink || bytes < 16 || bytes % 16 != 0 || bytes > (size_t(1) << 40) ||
       reinterpret_cast<uintptr_t>(src) % 16 != 0)

@@ -206,4 +206,8 @@ def test_projection_priority_softmax_probes_stay_inside_outputs(ta, dev):
     src = torch.ones(1 << 18, dtype=torch.float32, device=dev)
     sink1 = g((1,), torch.int32)
     assert L.turbo_probe_read(_p(src), src.numel() * 4, _p(sink1), s) == 0
+    sink2 = g((1024,), torch.float32)
+    insts = ctypes.c_int64(0)
+    assert L.turbo_probe_valu(4, _p(sink2), ctypes.byref(insts), s) == 0
+    assert insts.value == 1024 * 4 * 8 * 4
     g.check("probes")
