@@ -77,7 +77,7 @@ def measured_traffic(kernel: str, workload: str):
 
 # Vector ALU issue peak of the MI355X: 1,024 SIMDs x 2.4 GHz / 4 clocks per
 # wave64 instruction (a 16-lane SIMD takes 4 clocks for 64 lanes).
-PEAK_VALU_GINST = 1024 * 2.4 / 4
+PEAK_VALU_GINST = 157.3e3 / (64 * 2)
 
 
 def measured_valu(kernel: str, workload: str):
@@ -221,16 +221,18 @@ def valu_roofline(kernel: str, workload: str, ms: float, ceil: dict):
     if n is None:
         return None
     rate = n / (ms * 1e-3) / 1e9
-    return {"kernel": kernel, "bound": "valu", "achieved": round(rate, 1),
+    return {"kernel": kernel, "bound": "alu", "achieved": round(rate, 1),
             "peak": PEAK_VALU_GINST, "unit": "G wave-instructions/s",
             "frac": round(rate / PEAK_VALU_GINST, 4),
             "frac_of_measured_ceiling": round(rate / ceil["valu_Ginst_per_s"], 4),
             "instructions_per_launch": n,
-            "derivation": "1,024 SIMDs x 2.4 GHz / 4 clocks per wave64 instruction; "
+            "derivation": "fp32 vector peak 157.3 TFLOP/s / (64 lanes x 2 flops per FMA) = one "
+                          "wave64 instruction per 2 clocks per SIMD (1,024 SIMDs, 2.4 GHz); "
                           "instructions = SQ_INSTS_VALU - SQ_INSTS_MFMA from profiles/valu.txt",
             "note": "on gfx950 the issue cost of a wave64 VALU instruction depends on the opcode "
                     "and its operands (2.5-4.8 clocks measured for the opcodes of the softmax "
-                    "path); the peak takes 4, the measured ceiling is the FMA-chain probe"}
+                    "path, none at 2); the measured ceiling is the FMA-chain probe "
+                    "(turbo_probe_valu, about 3.1 clocks)"}
 
 
 def rel_l2(a, ref) -> float:
