@@ -230,8 +230,9 @@ def valu_roofline(kernel: str, workload: str, ms: float, ceil: dict):
                           "wave64 instruction per 2 clocks per SIMD (1,024 SIMDs, 2.4 GHz); "
                           "instructions = SQ_INSTS_VALU - SQ_INSTS_MFMA from profiles/valu.txt",
             "note": "on gfx950 the issue cost of a wave64 VALU instruction depends on the opcode "
-                    "and its operands (2.5-4.8 clocks measured for the opcodes of the softmax "
-                    "path, none at 2); the measured ceiling is the FMA-chain probe "
+                    "and its operands: 2.6-3.2 clocks for VOP2 add/sub/mul/fmac with VGPR operands, "
+                    "4.3-4.8 for VOP3, SGPR operands, compares, selects, conversions, shifts and "
+                    "maxima (none at 2); the measured ceiling is the FMA-chain probe "
                     "(turbo_probe_valu, about 3.1 clocks)"}
 
 
