@@ -181,6 +181,36 @@ PAPER_CONTEXT = {
 }
 
 
+def fp16_attention_here(q, k, v, causal: bool, iters: int, ms_turbo: float, label: str):
+    """The paper's comparison measured on this GPU: torch's fp16
+    scaled_dot_product_attention (its flash or memory-efficient backend, a
+    library kernel; never the math path) on the same q, k, v, against the
+    TurboAttention time ms_turbo.  None when neither backend takes the shapes."""
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    G = q.shape[1] // k.shape[1]
+    for name, backend in (("flash", SDPBackend.FLASH_ATTENTION),
+                          ("memory-efficient", SDPBackend.EFFICIENT_ATTENTION)):
+        for gqa in (True, False):
+            try:
+                kk, vv = (k, v) if gqa else (k.repeat_interleave(G, dim=1).contiguous(),
+                                             v.repeat_interleave(G, dim=1).contiguous())
+                kw = {"enable_gqa": True} if gqa and G > 1 else {}
+                with sdpa_kernel([backend]):
+                    fn = lambda: torch.nn.functional.scaled_dot_product_attention(
+                        q, kk, vv, is_causal=causal, **kw)
+                    ramp_clocks(fn, 0.1)
+                    ms, _ = stats(launch_times(fn, iters))
+            except Exception:  # this backend does not take these shapes
+                continue
+            return {"library": f"torch {torch.__version__} scaled_dot_product_attention, fp16, "
+                               f"{name} backend" + (", GQA in the kernel" if gqa and G > 1 else
+                                                    ", K/V expanded to the query heads"),
+                    "workload": label, "ms": round(ms, 4),
+                    "turbo_ms": round(ms_turbo, 4), "turbo_speedup": round(ms / ms_turbo, 3)}
+    return None
+
+
 def measured_ceilings(dev):
     """The int8 MFMA rate and the HBM streaming-read rate of this GPU, from the
     library's probe kernels (median of 5 launches each)."""
@@ -462,6 +492,12 @@ def main():
         "ceilings_measured": ceil,
         "paper_context": PAPER_CONTEXT,
     }
+    # the paper's comparison (fp16 attention) measured here: the quantization
+    # of K and V counts on TurboAttention's side
+    fp16_here = fp16_attention_here(q, k, v, True, args.kernel_iters, ms_q + ms_p,
+                                    f"{w.name} prefill (quantize_kv + attn_prefill)")
+    if fp16_here is not None:
+        result["paper_context"] = dict(PAPER_CONTEXT, fp16_attention_here=fp16_here)
 
     # ---- the decode half of the headline: Phi-3-medium decode ---------------
     if not args.no_decode_half:
@@ -472,6 +508,9 @@ def main():
                                              dec["roofline"]["achieved"] / ceil["hbm_read_GBs"], 4),
                                          workload=wd.name, ms=dec["ms"], mean_ms=dec["mean_ms"],
                                          kv_split_groups=dec["split"])
+        if dec["fp16_here"] is not None:
+            result["paper_context"] = dict(result["paper_context"],
+                                           fp16_decode_here=dec["fp16_here"])
         if not args.no_error:
             result["error_vs_fp64"] = {"decode": decode_error(wd, dec, dev)}
         del dec
@@ -610,6 +649,24 @@ def decode_measure(args, w, dev, split: int, buffer_step: bool = False):
                          "per_launch_bytes": kv_bytes + qo_bytes})
     run()  # o of the first copy (both copies hold the same cache)
     torch.cuda.synchronize()
+    # the paper's comparison measured here: fp16 attention of the same query
+    # over an fp16 cache of the same shape (random values: only time is taken)
+    kf = torch.randn(B, Hkv, N, 128, dtype=torch.float16, device=dev)
+    vf = torch.randn_like(kf)
+    here = fp16_attention_here(q[:, :, None], kf, vf, False, max(args.steps, 20), ms,
+                               f"{w.name} decode (attn_decode + merge)")
+    del kf, vf
+    if here is not None:
+        # a decode reads its cache once: the fp16 cache at the HBM peak bounds
+        # any fp16 decode kernel, the library's included
+        fp16_bytes = 2 * B * Hkv * N * 128 * 2 + qo_bytes
+        bound_ms = fp16_bytes / (PEAK_HBM_GBS * 1e9) * 1e3
+        here.update(library_GBs=round(fp16_bytes / (here["ms"] * 1e-3) / 1e9, 1),
+                    fp16_bytes=fp16_bytes, fp16_hbm_bound_ms=round(bound_ms, 4),
+                    turbo_speedup_vs_fp16_hbm_bound=round(bound_ms / ms, 3),
+                    note="the library's kernel is not a split-KV decode kernel; the fp16 bound "
+                         "(the fp16 cache read once at 8 TB/s) is the fair comparison")
+    out["fp16_here"] = here
     if buffer_step:
         # the Sec. 3.3 decoding step: append the new token's K/V to the int8
         # buffer, then attend the cache plus the buffer (not the headline)
@@ -701,7 +758,8 @@ def bench_decode(args, w):
             dec["gbs"] / ceil["hbm_read_GBs"], 4), mean_ms=round(dec["mean_ms"], 4)),
         "ceilings_measured": ceil,
         "buffer_step": dec["buffer_step"],
-        "paper_context": PAPER_CONTEXT,
+        "paper_context": (PAPER_CONTEXT if dec["fp16_here"] is None
+                          else dict(PAPER_CONTEXT, fp16_decode_here=dec["fp16_here"])),
     }
     if not args.no_error:
         result["error_vs_fp64"] = {"decode": decode_error(w, dec, dev)}
