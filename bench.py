@@ -63,6 +63,7 @@ def measured_traffic(kernel: str, workload: str):
             "k_attn_decode": ["paper_2412_08585_amd/csrc/attn_decode.hip",
                               "paper_2412_08585_amd/csrc/kv_tail.hip",
                               "paper_2412_08585_amd/csrc/turbo_common.h",
+                              "paper_2412_08585_amd/csrc/stream_loads.h",
                               "paper_2412_08585_amd/build.py"]}.get(kernel)
     path = os.path.join(ROOT, "profiles", "traffic.txt")
     if not srcs or not os.path.exists(path):
@@ -75,8 +76,9 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
-# Vector ALU issue peak of the MI355X: 1,024 SIMDs x 2.4 GHz / 4 clocks per
-# wave64 instruction (a 16-lane SIMD takes 4 clocks for 64 lanes).
+# Vector ALU issue peak of the MI355X in G wave64 instructions/s: the fp32
+# vector peak of 157.3 TFLOP/s is one 64-lane FMA (2 flops a lane) per 2
+# clocks per SIMD (1,024 SIMDs at 2.4 GHz).
 PEAK_VALU_GINST = 157.3e3 / (64 * 2)
 
 

@@ -32,6 +32,7 @@
 //  * The accumulator is kept as O = beta * Ost (per-row beta) so the
 //    rescale by SAS(m_old - m_new) touches one value per row.
 #include "turbo_common.h"
+#include "stream_loads.h"
 
 namespace turbo {
 
@@ -281,14 +282,17 @@ __device__ __forceinline__ void load_k(const DecodeArgs& a, int kh, int head_off
   K.skg = gs[0];
   K.svg = gs[1];
   const int koff = head_off + m * 16 * BITS + 4 * BITS * g4;
+  // the codes are read once per launch: streaming loads.  The group's
+  // metadata stays on ordinary loads, since its block is read twice (the K
+  // scales and zeros here, the V ones by load_v)
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
     const uint8_t* krow = a.pages + (long)K.pg[mb] * a.page_bytes + koff;
     if constexpr (BITS == 4) {
-      const uint4 x = *reinterpret_cast<const uint4*>(krow);
+      const u32x4_t x = load_nt4(krow);
       K.kraw[mb][0] = x.x; K.kraw[mb][1] = x.y; K.kraw[mb][2] = x.z; K.kraw[mb][3] = x.w;
     } else {
-      const uint2 x = *reinterpret_cast<const uint2*>(krow);
+      const u32x2_t x = load_nt2(krow);
       K.kraw[mb][0] = x.x; K.kraw[mb][1] = x.y;
     }
   }
@@ -315,10 +319,10 @@ __device__ __forceinline__ void load_v(const DecodeArgs& a, int kh, int head_off
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb) {
     if constexpr (BITS == 4) {
-      const uint2 x = *reinterpret_cast<const uint2*>(vrow + cb * 32 * BITS);
+      const u32x2_t x = load_nt2(vrow + cb * 32 * BITS);
       V.vraw[cb][0] = x.x; V.vraw[cb][1] = x.y;
     } else {
-      V.vraw[cb][0] = *reinterpret_cast<const unsigned*>(vrow + cb * 32 * BITS);
+      V.vraw[cb][0] = load_nt1(vrow + cb * 32 * BITS);
     }
   }
   const int8_t* meta = a.gmeta + ((long)K.slot * a.Hkv + kh) * 512;

@@ -8,6 +8,7 @@
 // rows per work-group); longer rows use one 256-thread work-group, in
 // registers up to 16384 values and in three streaming passes beyond.
 #include "turbo_common.h"
+#include "stream_loads.h"
 
 namespace turbo {
 
@@ -31,11 +32,19 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // Loads of one row in chunks of four values: chunk i of thread t covers
-// columns 4 (t + T i) .. +3; columns past the row read as -inf.
-template <int T>
+// columns 4 (t + T i) .. +3; columns past the row read as -inf.  kNT: the row
+// is read once (held in registers), so the vector loads stream.
+template <int T, bool kNT = false>
 __device__ __forceinline__ float4 load4(const float* xr, int C, int vec, int t, int i) {
   const int c = 4 * (t + T * i);
-  if (vec && c + 3 < C) return *reinterpret_cast<const float4*>(xr + c);
+  if (vec && c + 3 < C) {
+    if (kNT) {
+      const u32x4_t u = load_nt4(xr + c);
+      return make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z),
+                         __uint_as_float(u.w));
+    }
+    return *reinterpret_cast<const float4*>(xr + c);
+  }
   float4 r;
   r.x = c < C ? xr[c] : -INFINITY;
   r.y = c + 1 < C ? xr[c + 1] : -INFINITY;
@@ -81,7 +90,7 @@ __global__ __launch_bounds__(256) void k_sas_softmax_wave(SasSoftmaxArgs a) {
   float m = -INFINITY;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    v[i] = load4<64>(xr, a.cols, a.vec, lane, i);
+    v[i] = load4<64, true>(xr, a.cols, a.vec, lane, i);
     m = fmaxf(m, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
   }
   m = wave_max_fast(m);
@@ -126,7 +135,7 @@ __global__ __launch_bounds__(256) void k_sas_softmax_block(SasSoftmaxArgs a) {
     float m = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      v[i] = load4<256>(xr, C, a.vec, t, i);
+      v[i] = load4<256, true>(xr, C, a.vec, t, i);
       m = fmaxf(m, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
     }
     m = block_reduce(m, red, true);
