@@ -32,7 +32,7 @@
 //  * The accumulator is kept as O = beta * Ost (per-row beta) so the
 //    rescale by SAS(m_old - m_new) touches one value per row.
 //  * Every code byte is read once per launch, through streaming loads: the
-//    launch's time follows the bytes its waves wait for.
+//    waves spend their time waiting on these loads.
 #include "turbo_common.h"
 #include "stream_loads.h"
 
