@@ -472,7 +472,9 @@ def main():
                             "frac_hbm": round(quant_bytes / ms_q / 1e6 / PEAK_HBM_GBS, 4)},
             "head_priority": {"ms": round(ms_h, 4), "GB/s": round(B * Hkv * N * d * 2 / ms_h / 1e6, 1),
                               "frac_hbm": round(B * Hkv * N * d * 2 / ms_h / 1e6 / PEAK_HBM_GBS, 4),
-                              "note": "Sec. 3.2 bit choice from the prefill K; not in the step"},
+                              "note": "Sec. 3.2 bit choice from the prefill K; not in the step; "
+                                      "K (B*Hkv*N*128 fp16) may stay in the 256 MB MALL across "
+                                      "the repeated launches"},
             "attn_prefill": {"ms": round(ms_p, 4), "mean_ms": round(mean_p, 4),
                              "TOPS": round(prefill_tops, 2),
                              "frac_int8_mfma": round(prefill_tops / PEAK_INT8_TOPS, 4)},
