@@ -395,8 +395,13 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   // latency.
   GroupK<BITS> KA, KB;
   load_k<BITS>(a, kh, head_off, bt, gt, g0, g0 < g1, KA);
+  // Issue priority (s_setprio) is raised from a group's start until its V
+  // loads are out, and for the K prefetch: a wave on its way to a load then
+  // goes ahead of the other waves of its SIMD, which are in their softmax or
+  // PV steps, so the loads leave earlier.
   auto process = [&](const GroupK<BITS>& cur, int g) {
     if (cur.ok) {
+      __builtin_amdgcn_s_setprio(2);
       // s^int pairs matching wq and z^int bytes matching wqn (see above)
       unsigned sA01, sA23, sB01, sB23, zA, zB;
       if constexpr (BITS == 4) {
@@ -482,6 +487,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
       }
       GroupV<BITS> cv;
       load_v<BITS>(a, kh, head_off, cur, cv);
+      __builtin_amdgcn_s_setprio(0);
       // lane (n, g4), register r of m-block mb: row n, token 16*mb + 4*g4 + r
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
@@ -644,10 +650,14 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
     }
   };
   for (int g = g0; g < g1; g += 2) {
+    __builtin_amdgcn_s_setprio(2);
     load_k<BITS>(a, kh, head_off, bt, gt, g + 1, g + 1 < g1, KB);
+    __builtin_amdgcn_s_setprio(0);
     process(KA, g);
     if (g + 1 < g1) {
+      __builtin_amdgcn_s_setprio(2);
       load_k<BITS>(a, kh, head_off, bt, gt, g + 2, g + 2 < g1, KA);
+      __builtin_amdgcn_s_setprio(0);
       process(KB, g + 1);
     }
   }
