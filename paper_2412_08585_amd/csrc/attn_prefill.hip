@@ -620,7 +620,12 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     constexpr int buf = decltype(bufc)::value;
     const float skn = skp[min(j + 1, jend)], svn = svp[min(j + 1, jend)];
     // ---- S^T_j = K_j Q^T on the MFMA -----------------------------------
+    // The MFMA steps (operand reads, MFMAs, the next tiles' loads) run at
+    // raised issue priority: a wave that reaches them goes ahead of the
+    // softmax arithmetic of the other waves of its SIMD, so that its MFMAs
+    // overlap their VALU work.
     v4i S[4];
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) {
       const v4i k0 = *reinterpret_cast<const v4i*>(&L.k[buf][kbase0 + 512 * mb]);
@@ -638,6 +643,7 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
     const int o2 = min(j + 2, jend) * 8192;
     kp0 = tile_load(krs, lane16, o2);
     if constexpr (kTwo) kp1 = tile_load(krs, lane16 + 4096u, o2);
+    __builtin_amdgcn_s_setprio(0);
     const bool trace_tile = traced && j == a.tr_j;
     if constexpr (kTrace) {
       if (trace_tile) {
@@ -764,12 +770,14 @@ __global__ __launch_bounds__(64 * kW, 4) void k_attn_prefill16(PrefillArgs a) {
 #pragma unroll
     for (int hv = 0; hv < 2; ++hv) {
       v4i acc[4];
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const v4i vop = *reinterpret_cast<const v4i*>(&L.v[buf][vbase + 1024 * (4 * hv + c)]);
         const v4i z = {kAccSeed, kAccSeed, kAccSeed, kAccSeed};
         acc[c] = mfma16x16x64(vop, pop, z);
       }
+      __builtin_amdgcn_s_setprio(0);
       if constexpr (kTrace) {
         if (trace_tile) {
           // register r of channel block cb <-> channel 16cb + 4g + r

@@ -92,11 +92,15 @@ __global__ __launch_bounds__(256) void k_sas_softmax_wave(SasSoftmaxArgs a) {
   float* yr = a.y + row * a.cols;
   float4 v[NV];
   float m = -INFINITY;
+  // The row's loads are issued at raised priority, ahead of the arithmetic
+  // of the other waves of the SIMD.
+  __builtin_amdgcn_s_setprio(2);
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    v[i] = load4<64, true>(xr, a.cols, a.vec, lane, i);
+  for (int i = 0; i < NV; ++i) v[i] = load4<64, true>(xr, a.cols, a.vec, lane, i);
+  __builtin_amdgcn_s_setprio(0);
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
     m = fmaxf(m, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
-  }
   m = wave_max_fast(m);
   float s = 0.0f;
 #pragma unroll
@@ -137,11 +141,13 @@ __global__ __launch_bounds__(256) void k_sas_softmax_block(SasSoftmaxArgs a) {
   if (NV > 0) {
     float4 v[NV > 0 ? NV : 1];
     float m = -INFINITY;
+    __builtin_amdgcn_s_setprio(2);  // the row's loads first (2 % on 4096-column rows)
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      v[i] = load4<256, true>(xr, C, a.vec, t, i);
+    for (int i = 0; i < NV; ++i) v[i] = load4<256, true>(xr, C, a.vec, t, i);
+    __builtin_amdgcn_s_setprio(0);
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
       m = fmaxf(m, fmaxf(fmaxf(v[i].x, v[i].y), fmaxf(v[i].z, v[i].w)));
-    }
     m = block_reduce(m, red, true);
     float s = 0.0f;
 #pragma unroll
