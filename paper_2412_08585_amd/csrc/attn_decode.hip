@@ -395,10 +395,11 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
   // latency.
   GroupK<BITS> KA, KB;
   load_k<BITS>(a, kh, head_off, bt, gt, g0, g0 < g1, KA);
-  // Issue priority (s_setprio) is raised from a group's start until its V
-  // loads are out, and for the K prefetch: a wave on its way to a load then
-  // goes ahead of the other waves of its SIMD, which are in their softmax or
-  // PV steps, so the loads leave earlier.
+  // Issue priority (s_setprio) is highest from a group's start until its V
+  // loads are out, and for the K prefetch, lower in the softmax and lowest in
+  // the PV and update steps: a wave on its way to a load goes ahead of the
+  // other waves of its SIMD, and a wave nearer its next load ahead of one
+  // that has just issued it, so the loads leave earlier.
   auto process = [&](const GroupK<BITS>& cur, int g) {
     if (cur.ok) {
       __builtin_amdgcn_s_setprio(2);
@@ -487,7 +488,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
       }
       GroupV<BITS> cv;
       load_v<BITS>(a, kh, head_off, cur, cv);
-      __builtin_amdgcn_s_setprio(0);
+      __builtin_amdgcn_s_setprio(1);
       // lane (n, g4), register r of m-block mb: row n, token 16*mb + 4*g4 + r
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
@@ -568,6 +569,7 @@ __device__ __forceinline__ void decode_groups(const DecodeArgs& a, DecodeLds<GP>
         L.rowv[rr] = make_float4(gsc, __int_as_float(psum), rf, 0.0f);
       }
       wave_sync();
+      __builtin_amdgcn_s_setprio(0);
       // ---- O = Q(P~) V on the raw codes (A = P rows, B = V codes) -------
       const v4i pop = *reinterpret_cast<const v4i*>(&L.pbuf[nrow][16 * g4]);
       auto vop_of = [&](int cb) {
